@@ -1,0 +1,60 @@
+"""Algorithmic work of one elastic-ViT forward per image, per DN mode.
+
+FLOPs are 2 x multiply-accumulates of the dense contractions: patch embedding,
+q/k/v, attention QK^T and PV, output projection, fc1, fc2 and the classifier,
+every token counted in every layer.  Element-wise work (LayerNorm, GELU,
+softmax, adds) is not counted.  ``paper_macs`` is the convention that matches
+the base ViT-B figure of Table 1: linear-layer MACs only (no QK^T / PV).
+
+Bytes are the algorithmic HBM bytes of the memory-bound kernels: a LayerNorm
+reads one bf16 activation row and writes one.
+"""
+from __future__ import annotations
+
+from typing import Dict
+
+import numpy as np
+
+from .inputs import ModelConfig
+
+
+def layer_widths(table, k: int):
+    return (np.asarray(table.n_heads[k], dtype=np.int64),
+            np.asarray(table.n_mlp[k], dtype=np.int64))
+
+
+def gemm_flops(cfg: ModelConfig, table, k: int) -> Dict[str, float]:
+    """Per-image FLOPs of each contraction kernel class in mode k."""
+    T, d, hd, P = cfg.tokens, cfg.dim, cfg.head_dim, cfg.patch
+    h, m = layer_widths(table, k)
+    return {
+        "patch": 2.0 * cfg.num_patches * cfg.patch_k * d,
+        "qkv": float(np.sum(2.0 * T * d * 3 * hd * h)),
+        "attn": float(np.sum(2.0 * 2 * T * T * hd * h)),
+        "proj": float(np.sum(2.0 * T * hd * h * d)),
+        "fc1": float(np.sum(2.0 * T * d * m)),
+        "fc2": float(np.sum(2.0 * T * m * d)),
+        "head": 2.0 * d * cfg.num_classes,
+    }
+
+
+def flops_per_image(cfg: ModelConfig, table, k: int) -> float:
+    return float(sum(gemm_flops(cfg, table, k).values()))
+
+
+def paper_macs(cfg: ModelConfig, table, k: int) -> float:
+    f = gemm_flops(cfg, table, k)
+    return (f["patch"] + f["qkv"] + f["proj"] + f["fc1"] + f["fc2"] + f["head"]) / 2.0
+
+
+def layernorm_bytes_per_image(cfg: ModelConfig, elem_bytes: int = 2) -> float:
+    """One LayerNorm over all tokens: read T*d + write T*d elements."""
+    return 2.0 * cfg.tokens * cfg.dim * elem_bytes
+
+
+def active_weight_elems(cfg: ModelConfig, table, k: int) -> int:
+    """Matrix elements a mode-k forward reads (biases and norms excluded)."""
+    d, hd, C = cfg.dim, cfg.head_dim, cfg.num_classes
+    h, m = layer_widths(table, k)
+    per_layer = 3 * hd * h * d + d * hd * h + m * d + d * m
+    return int(d * cfg.patch_k + per_layer.sum() + C * d)
