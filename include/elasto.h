@@ -1,0 +1,276 @@
+/*
+ * elasto.h -- C ABI of the MI355X (gfx950) elastic-ViT inference library.
+ *
+ * An elastic ViT holds several nested Descendant Networks (DNs) on ONE shared
+ * parameter set (Section 4.3; weight sharing, Eq. 8).  A DN mode keeps, per
+ * layer, a subset of attention heads and MLP hidden units; because the DNs are
+ * nested, every mode's subset is a prefix of one per-layer channel order.
+ * The library stores every weight matrix permuted into that order, so a mode
+ * reads a contiguous prefix (per row for the K-sliced projections) and never
+ * gathers.  A forward in mode k equals a standard ViT forward (Section 4.1:
+ * patch embedding, MHA of Eqs. 2-3, GELU MLP of Eq. 5, pre-norm residual
+ * blocks, class-token classifier) in which the pruned heads / units are
+ * removed, i.e. masked to zero as in Eqs. 4 and 6.  Switching modes
+ * (Section 6.2 measures the switch) is a host-side integer store.
+ *
+ * Conventions for every function:
+ *   - All functions are extern "C" and return elasto_status_t (0 = ELASTO_OK)
+ *     unless stated otherwise.
+ *   - On any error nothing is changed, and elasto_last_error() returns a
+ *     message for the calling thread.
+ *   - Every argument, config and table check runs before any HIP call, so the
+ *     validation paths work without a GPU.
+ *   - "device pointer" means memory from hipMalloc (e.g. a torch.cuda tensor's
+ *     data_ptr()); "host pointer" means ordinary CPU memory.
+ *   - A handle is not thread-safe: use one handle per host thread / stream.
+ */
+#ifndef ELASTO_H_
+#define ELASTO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct elasto_handle_s* elasto_handle_t;
+
+typedef enum {
+  ELASTO_OK = 0,
+  ELASTO_ERR_INVALID_ARG = 1,   /* null pointer, bad size, misaligned pointer   */
+  ELASTO_ERR_BAD_CONFIG = 2,    /* model shape the library does not support     */
+  ELASTO_ERR_BAD_TABLE = 3,     /* DN table inconsistent with the model         */
+  ELASTO_ERR_OUT_OF_MEMORY = 4, /* device or host allocation failed             */
+  ELASTO_ERR_HIP = 5,           /* a HIP runtime call or kernel launch failed   */
+  ELASTO_ERR_MODE_RANGE = 6,    /* mode index outside [0, num_modes)            */
+  ELASTO_ERR_BATCH_RANGE = 7    /* batch outside [1, max_batch]                 */
+} elasto_status_t;
+
+/* Arithmetic of the whole path.  BF16: matrices and activations in bf16, MFMA
+ * with fp32 accumulation, fp32 LayerNorm / softmax / GELU, fp32 biases and
+ * norm parameters.  FP32: fp32 everywhere (vector-ALU FMA, no reduced-
+ * precision matrix mode). */
+typedef enum { ELASTO_FP32 = 0, ELASTO_BF16 = 1 } elasto_dtype_t;
+
+/* Model shape.  tokens T = (img/patch)^2 + 1, head_dim = dim/heads.
+ * Supported (else ELASTO_ERR_BAD_CONFIG): img % patch == 0, dim % heads == 0,
+ * in_chans >= 1, every size >= 1, ln_eps > 0.  BF16 additionally needs
+ * head_dim == 64, patch % 8 == 0, dim % 8 == 0 and mlp_hidden % 8 == 0.
+ * Both paths need dim <= 2048. */
+typedef struct {
+  int32_t img, patch, in_chans, dim, depth, heads, mlp_hidden, num_classes;
+  int32_t max_batch; /* largest batch a forward may use; scratch is sized for it */
+  int32_t dtype;     /* elasto_dtype_t */
+  float ln_eps;      /* LayerNorm epsilon (1e-6 for ViT) */
+} elasto_config_t;
+
+/* HOST pointers to fp32 weights in canonical PyTorch order ([out, in]);
+ * per-layer tensors are stacked on a leading depth axis.  L = depth,
+ * d = dim, M = mlp_hidden, C = num_classes, P = patch, T = tokens.
+ * qkv_w rows are [q | k | v], each block head-major (head i owns rows
+ * i*head_dim .. (i+1)*head_dim-1 of the block); proj_w input columns are
+ * head-major the same way.  The caller keeps ownership; the library copies. */
+typedef struct {
+  const float* patch_w; /* [d][in_chans][P][P] */
+  const float* patch_b; /* [d] */
+  const float* cls;     /* [d] */
+  const float* pos;     /* [T][d] */
+  const float* ln1_g;   /* [L][d] */
+  const float* ln1_b;   /* [L][d] */
+  const float* qkv_w;   /* [L][3d][d] */
+  const float* qkv_b;   /* [L][3d] */
+  const float* proj_w;  /* [L][d][d] */
+  const float* proj_b;  /* [L][d] */
+  const float* ln2_g;   /* [L][d] */
+  const float* ln2_b;   /* [L][d] */
+  const float* fc1_w;   /* [L][M][d] */
+  const float* fc1_b;   /* [L][M] */
+  const float* fc2_w;   /* [L][d][M] */
+  const float* fc2_b;   /* [L][d] */
+  const float* norm_g;  /* [d] */
+  const float* norm_b;  /* [d] */
+  const float* head_w;  /* [C][d] */
+  const float* head_b;  /* [C] */
+} elasto_weights_t;
+
+/* DN table (HOST pointers, row-major int32).  Mode k, layer l keeps the first
+ * n_heads[k][l] heads of head_order[l] and the first n_mlp[k][l] units of
+ * mlp_order[l]; prefixes of one order make the modes nested (Eq. 8).
+ * Mode 0 conventionally is the widest.  ELASTO_ERR_BAD_TABLE unless:
+ * depth == cfg.depth, num_modes >= 1, 1 <= n_heads <= heads,
+ * 1 <= n_mlp <= mlp_hidden, and every order row is a permutation. */
+typedef struct {
+  int32_t num_modes, depth;
+  const int32_t* n_heads;    /* [num_modes][depth] */
+  const int32_t* n_mlp;      /* [num_modes][depth] */
+  const int32_t* head_order; /* [depth][heads] */
+  const int32_t* mlp_order;  /* [depth][mlp_hidden] */
+} elasto_dn_table_t;
+
+/* ---------------------------------------------------------------- lifecycle */
+
+/* Validates cfg and table, repacks the weights into the prefix layout (bf16
+ * rounded to nearest even on the BF16 path), makes one device allocation for
+ * the weights and one for max_batch activation scratch, and copies.  The
+ * current device at call time owns the handle.  Mode 0 is selected.
+ * *out receives the handle (unchanged on error). */
+elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t* w,
+                              const elasto_dn_table_t* table, elasto_handle_t* out);
+
+/* Frees all device and host memory of h; waits for nothing (the caller must
+ * make sure no enqueued forward still uses h).  h == NULL is accepted. */
+elasto_status_t elasto_destroy(elasto_handle_t h);
+
+/* Selects DN mode k for subsequent forwards (Eq. 11 picks k; this applies it).
+ * O(1) host store: no HIP call, no weight copy, no synchronisation.  A forward
+ * uses the mode current at its enqueue time.  ELASTO_ERR_MODE_RANGE if k is
+ * outside [0, num_modes). */
+elasto_status_t elasto_set_mode(elasto_handle_t h, int32_t k);
+elasto_status_t elasto_get_mode(elasto_handle_t h, int32_t* k);
+
+/* Enqueues one forward in the current mode on hip_stream (a hipStream_t;
+ * NULL = default stream) and returns without waiting.
+ *   images: device pointer, NCHW [batch][in_chans][img][img], contiguous,
+ *           16-byte aligned; bf16 on the BF16 path, fp32 on the FP32 path.
+ *   logits: device pointer, fp32 [batch][num_classes].
+ * Both stay owned by the caller and must stay valid until the stream work
+ * completes.  Allocates nothing and never synchronises; device faults
+ * surface at the caller's next synchronisation.  ELASTO_ERR_BATCH_RANGE if
+ * batch is outside [1, max_batch]; ELASTO_ERR_HIP if a launch fails. */
+elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t batch,
+                               float* logits, void* hip_stream);
+
+/* Thread-local message of the calling thread's last failing call ("" if none).
+ * Returns a string, not a status. */
+const char* elasto_last_error(void);
+
+/* Work of mode k per image: algorithmic FLOPs (2 x MACs of every contraction,
+ * attention included) and bytes of the weight matrices a forward reads. */
+elasto_status_t elasto_mode_info(elasto_handle_t h, int32_t k, double* flops_per_image,
+                                 int64_t* active_weight_bytes);
+
+/* Device bytes the handle holds: packed weights and activation scratch. */
+elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes,
+                                   int64_t* scratch_bytes);
+
+/* ------------------------------------------------- host-only layout helpers */
+/* These make no HIP call; they let a CPU-only caller check validation and the
+ * packed prefix layout. */
+
+elasto_status_t elasto_validate(const elasto_config_t* cfg, const elasto_dn_table_t* table);
+
+/* Tensor ids of the packed weight image. */
+typedef enum {
+  ELASTO_T_PATCH_W = 0, /* [d][in_chans*P*P], matrix dtype                     */
+  ELASTO_T_PATCH_B,     /* [d] fp32                                            */
+  ELASTO_T_CLS,         /* [d] fp32                                            */
+  ELASTO_T_POS,         /* [T][d] fp32                                         */
+  ELASTO_T_NORM_G,      /* [d] fp32                                            */
+  ELASTO_T_NORM_B,      /* [d] fp32                                            */
+  ELASTO_T_HEAD_W,      /* [C][d], matrix dtype                                */
+  ELASTO_T_HEAD_B,      /* [C] fp32                                            */
+  ELASTO_T_LN1_G,       /* per layer [d] fp32                                  */
+  ELASTO_T_LN1_B,
+  ELASTO_T_WQKV,        /* [heads*3*hd][d]: row s*3hd + t*hd + c = qkv_w row
+                           t*d + head_order[s]*hd + c (t = q,k,v)              */
+  ELASTO_T_BQKV,        /* [heads*3*hd] fp32, same row order                   */
+  ELASTO_T_WO,          /* [d][heads*hd]: column s*hd + c = proj_w column
+                           head_order[s]*hd + c                                */
+  ELASTO_T_BO,          /* [d] fp32                                            */
+  ELASTO_T_LN2_G,
+  ELASTO_T_LN2_B,
+  ELASTO_T_W1,          /* [M][d]: row s = fc1_w row mlp_order[s]              */
+  ELASTO_T_B1,          /* [M] fp32, same order                                */
+  ELASTO_T_W2,          /* [d][M]: column s = fc2_w column mlp_order[s]        */
+  ELASTO_T_B2,          /* [d] fp32                                            */
+  ELASTO_T_COUNT
+} elasto_tensor_t;
+
+/* Total bytes of the packed weight image for cfg. */
+elasto_status_t elasto_packed_bytes(const elasto_config_t* cfg, int64_t* bytes);
+
+/* Byte offset, row count, column count and element size (2 = bf16, 4 = fp32)
+ * of one tensor in the packed image; layer is ignored for global tensors. */
+elasto_status_t elasto_packed_layout(const elasto_config_t* cfg, int32_t tensor, int32_t layer,
+                                     int64_t* offset, int64_t* rows, int64_t* cols,
+                                     int32_t* elem_bytes);
+
+/* Writes the packed weight image (exactly what elasto_create copies to the
+ * device) into host memory dst of dst_bytes >= elasto_packed_bytes. */
+elasto_status_t elasto_pack_weights(const elasto_config_t* cfg, const elasto_weights_t* w,
+                                    const elasto_dn_table_t* table, void* dst, int64_t dst_bytes);
+
+/* -------------------------------------------------- per-kernel timing (HIP) */
+
+/* Kernel classes of one forward. */
+typedef enum {
+  ELASTO_K_PATCH = 0, /* patch-embedding GEMM (+bias, +position, class rows) */
+  ELASTO_K_LN,        /* LayerNorm (LN1, LN2, final norm on class rows)      */
+  ELASTO_K_QKV,       /* q/k/v GEMM over the active heads                    */
+  ELASTO_K_ATTN,      /* fused attention over the active heads               */
+  ELASTO_K_PROJ,      /* output projection GEMM + residual add               */
+  ELASTO_K_FC1,       /* fc1 GEMM + GELU over the active units               */
+  ELASTO_K_FC2,       /* fc2 GEMM + residual add                             */
+  ELASTO_K_HEAD,      /* classifier GEMM                                     */
+  ELASTO_K_COUNT
+} elasto_kernel_t;
+
+/* Starts recording a hipEvent pair around every launch of kernel class kc
+ * (kc = -1 stops) for at most max_launches launches; events are created here,
+ * not in the forward.  Recording adds two event records per launch. */
+elasto_status_t elasto_kernel_timing(elasto_handle_t h, int32_t kc, int32_t max_launches);
+
+/* Waits for the recorded events, returns the summed kernel time (ms) and the
+ * launch count since the last read, and resets the accumulation. */
+elasto_status_t elasto_kernel_timing_read(elasto_handle_t h, double* total_ms, int64_t* launches);
+
+/* Algorithmic work of one launch of class kc in mode k at the given batch
+ * summed over the forward: FLOPs (contractions) and bytes (LayerNorm rows
+ * read + written; for contractions the operand and result bytes) and the
+ * number of launches of that class in one forward. */
+elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, int32_t kc,
+                                   double* flops, double* bytes, int32_t* launches);
+
+/* ------------------------------------------- single-kernel entry points */
+/* Device-pointer access to the kernels one forward uses, for kernel-level
+ * tests.  dtype selects bf16 (MFMA) or fp32 kernels; activations have that
+ * dtype, gamma/beta/bias are fp32.  Strides are in elements. */
+
+/* out[r] = LayerNorm(x[r]) * g + b over d features, r < rows.  x row r starts
+ * at x + r*x_stride; out is contiguous [rows][d]. */
+elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride, void* out,
+                                    int64_t rows, int32_t d, const float* g, const float* b,
+                                    float eps, void* hip_stream);
+
+typedef enum {
+  ELASTO_EPI_BIAS = 0,     /* C = A W^T + bias                      */
+  ELASTO_EPI_BIAS_GELU,    /* C = GELU(A W^T + bias), exact erf     */
+  ELASTO_EPI_BIAS_RESID,   /* C = C + A W^T + bias (in place)       */
+  ELASTO_EPI_BIAS_F32OUT   /* C (fp32) = A W^T + bias               */
+} elasto_epilogue_t;
+
+/* C[m][n] = epi(sum_{k<K} A[m*lda + k] * W[n*ldw + k] + bias[n]), m < M,
+ * n < N.  Only the first K columns of A / W rows and the first N rows of W
+ * are read.  BF16 path: lda, ldw, ldc multiples of 8 and pointers 16-byte
+ * aligned. */
+elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A, int64_t lda,
+                                 const void* W, int64_t ldw, void* C, int64_t ldc,
+                                 const float* bias, int64_t M, int32_t N, int32_t K,
+                                 void* hip_stream);
+
+/* Multi-head attention (Eq. 3) over `heads` head slots of `batch` sequences
+ * of `tokens` rows.  qkv row (b*tokens + t) holds, for slot s, q at columns
+ * s*3*hd + [0,hd), k at + [hd,2hd), v at + [2hd,3hd), with row stride
+ * qkv_stride; o row holds slot s at columns s*hd + [0,hd), row stride
+ * o_stride.  Scores are scaled by `scale`.  BF16 path: head_dim == 64. */
+elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_stride, void* o,
+                                    int64_t o_stride, int32_t batch, int32_t tokens,
+                                    int32_t heads, int32_t head_dim, float scale,
+                                    void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ELASTO_H_ */

@@ -1,0 +1,472 @@
+// C ABI: handle lifecycle, mode switch, forward enqueue, kernel timing and
+// the single-kernel entry points.
+//
+// One forward in mode k on `batch` images (M = batch * tokens rows):
+//   patch GEMM (+bias, +pos; class rows = cls + pos[0])          -> x
+//   per layer l, with h = n_heads[k][l], m = n_mlp[k][l]:
+//     LN1(x)                                                     -> u
+//     q/k/v GEMM, N = 3*hd*h (prefix rows of WQKV)               -> qkv
+//     attention over h head slots                                -> o
+//     projection GEMM, K = hd*h (prefix of each WO row), + x     -> x
+//     LN2(x)                                                     -> u
+//     fc1 GEMM + GELU, N = m (prefix rows of W1)                 -> g
+//     fc2 GEMM, K = m (prefix of each W2 row), + x               -> x
+//   final LN on the class rows                                   -> ucls
+//   classifier GEMM (fp32 out)                                   -> logits
+// Nothing is allocated or synchronised here; the mode is read at enqueue.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "kernels.h"
+#include "layout.h"
+
+using namespace elasto;
+
+struct elasto_handle_s {
+  elasto_config_t cfg;
+  Dims dims;
+  Layout lay;
+  int device = 0;
+  int num_modes = 0;
+  std::vector<int32_t> n_heads, n_mlp;  // [num_modes][depth]
+  int mode = 0;
+  uint8_t* dw = nullptr;  // packed weights
+  uint8_t* ds = nullptr;  // activation scratch
+  int64_t wbytes = 0, sbytes = 0;
+  void *x = nullptr, *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr, *ucls = nullptr;
+  // kernel timing
+  int timed_class = -1;
+  std::vector<hipEvent_t> events;
+  int used = 0;
+  int64_t skipped = 0;
+};
+
+namespace {
+
+const void* W(const elasto_handle_s* h, int id, int layer = 0) {
+  return h->dw + h->lay.get(id, layer).offset;
+}
+const float* F(const elasto_handle_s* h, int id, int layer = 0) {
+  return reinterpret_cast<const float*>(W(h, id, layer));
+}
+
+void destroy_events(elasto_handle_s* h) {
+  for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
+  h->events.clear();
+  h->used = 0;
+  h->skipped = 0;
+  h->timed_class = -1;
+}
+
+template <class Fn>
+hipError_t timed(elasto_handle_s* h, int kc, hipStream_t s, Fn&& fn) {
+  if (kc != h->timed_class) return fn();
+  if ((size_t)(2 * h->used + 1) >= h->events.size()) {
+    ++h->skipped;
+    return fn();
+  }
+  hipError_t e = hipEventRecord(h->events[2 * h->used], s);
+  if (e != hipSuccess) return e;
+  e = fn();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(h->events[2 * h->used + 1], s);
+  ++h->used;
+  return e;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t* w,
+                              const elasto_dn_table_t* table, elasto_handle_t* out) {
+  if (!out) return fail(ELASTO_ERR_INVALID_ARG, "out is NULL");
+  if (!check_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
+  if (!check_table(cfg, table)) return ELASTO_ERR_BAD_TABLE;
+  if (!check_weights(w)) return ELASTO_ERR_INVALID_ARG;
+
+  elasto_handle_s* h = new (std::nothrow) elasto_handle_s();
+  if (!h) return fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
+  h->cfg = *cfg;
+  h->dims = dims_of(*cfg);
+  h->lay = make_layout(*cfg);
+  h->num_modes = table->num_modes;
+  const size_t nk = (size_t)table->num_modes * cfg->depth;
+  h->n_heads.assign(table->n_heads, table->n_heads + nk);
+  h->n_mlp.assign(table->n_mlp, table->n_mlp + nk);
+
+  std::vector<uint8_t> host;
+  try {
+    host.resize((size_t)h->lay.total);
+  } catch (...) {
+    delete h;
+    return fail(ELASTO_ERR_OUT_OF_MEMORY, "host staging allocation failed");
+  }
+  pack(*cfg, *w, *table, h->lay, host.data());
+
+  const int64_t eb = cfg->dtype == ELASTO_BF16 ? 2 : 4;
+  const int64_t rows = (int64_t)cfg->max_batch * h->dims.T, D = cfg->dim;
+  auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
+  const int64_t sz_x = al(rows * D * eb), sz_qkv = al(rows * 3 * D * eb),
+                sz_g = al(rows * (int64_t)cfg->mlp_hidden * eb),
+                sz_cls = al((int64_t)cfg->max_batch * D * eb);
+  h->sbytes = 3 * sz_x + sz_qkv + sz_g + sz_cls;
+  h->wbytes = h->lay.total;
+
+  hipError_t e = hipGetDevice(&h->device);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->dw), (size_t)h->wbytes);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->ds), (size_t)h->sbytes);
+  if (e == hipSuccess) e = hipMemcpy(h->dw, host.data(), (size_t)h->wbytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    const elasto_status_t st = (e == hipErrorOutOfMemory) ? ELASTO_ERR_OUT_OF_MEMORY : ELASTO_ERR_HIP;
+    if (h->dw) (void)hipFree(h->dw);
+    if (h->ds) (void)hipFree(h->ds);
+    delete h;
+    (void)hipGetLastError();
+    return fail(st, "create: %s", hipGetErrorString(e));
+  }
+  uint8_t* p = h->ds;
+  h->x = p; p += sz_x;
+  h->u = p; p += sz_x;
+  h->o = p; p += sz_x;
+  h->qkv = p; p += sz_qkv;
+  h->g = p; p += sz_g;
+  h->ucls = p;
+  *out = h;
+  clear_error();
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_destroy(elasto_handle_t h) {
+  if (!h) return ELASTO_OK;
+  destroy_events(h);
+  hipError_t e1 = hipSuccess, e2 = hipSuccess;
+  if (h->dw) e1 = hipFree(h->dw);
+  if (h->ds) e2 = hipFree(h->ds);
+  delete h;
+  if (e1 != hipSuccess || e2 != hipSuccess)
+    return fail(ELASTO_ERR_HIP, "destroy: %s", hipGetErrorString(e1 != hipSuccess ? e1 : e2));
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_set_mode(elasto_handle_t h, int32_t k) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (k < 0 || k >= h->num_modes) return fail(ELASTO_ERR_MODE_RANGE, "mode %d outside [0, %d)", k, h->num_modes);
+  h->mode = k;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_get_mode(elasto_handle_t h, int32_t* k) {
+  if (!h || !k) return fail(ELASTO_ERR_INVALID_ARG, "NULL argument");
+  *k = h->mode;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_mode_info(elasto_handle_t h, int32_t k, double* flops_per_image,
+                                 int64_t* active_weight_bytes) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (k < 0 || k >= h->num_modes) return fail(ELASTO_ERR_MODE_RANGE, "mode %d outside [0, %d)", k, h->num_modes);
+  const int32_t* nh = h->n_heads.data() + (size_t)k * h->cfg.depth;
+  const int32_t* nm = h->n_mlp.data() + (size_t)k * h->cfg.depth;
+  if (flops_per_image) *flops_per_image = mode_flops(h->cfg, nh, nm);
+  if (active_weight_bytes) *active_weight_bytes = mode_weight_bytes(h->cfg, nh, nm);
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes, int64_t* scratch_bytes) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (weight_bytes) *weight_bytes = h->wbytes;
+  if (scratch_bytes) *scratch_bytes = h->sbytes;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t batch, float* logits,
+                               void* hip_stream) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (!images || !logits) return fail(ELASTO_ERR_INVALID_ARG, "images / logits is NULL");
+  if (batch < 1 || batch > h->cfg.max_batch)
+    return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
+  const bool bf = h->cfg.dtype == ELASTO_BF16;
+  if (bf && !aligned(images, 16)) return fail(ELASTO_ERR_INVALID_ARG, "images must be 16-byte aligned");
+  if (!aligned(images, 4) || !aligned(logits, 4)) return fail(ELASTO_ERR_INVALID_ARG, "misaligned pointer");
+
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device) {
+    if (hipSetDevice(h->device) != hipSuccess) return fail(ELASTO_ERR_HIP, "cannot select device %d", h->device);
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const elasto_config_t& c = h->cfg;
+  const Dims& d = h->dims;
+  const int k = h->mode;
+  const int L = c.depth, D = c.dim, Mh = c.mlp_hidden;
+  const int64_t rows = (int64_t)batch * d.T;
+  auto gemm = bf ? launch_gemm_bf16 : launch_gemm_f32;
+  auto ln = bf ? launch_layernorm_bf16 : launch_layernorm_f32;
+  auto attn = bf ? launch_attention_bf16 : launch_attention_f32;
+  const float scale = 1.0f / sqrtf((float)d.hd);
+
+  hipError_t e;
+  {
+    GemmArgs a;
+    a.W = W(h, ELASTO_T_PATCH_W);
+    a.ldw = d.patch_k;
+    a.C = h->x;
+    a.ldc = D;
+    a.bias = F(h, ELASTO_T_PATCH_B);
+    a.M = rows;
+    a.N = D;
+    a.K = d.patch_k;
+    a.img = images;
+    a.img_size = c.img;
+    a.patch = c.patch;
+    a.chans = c.in_chans;
+    a.grid = d.grid;
+    a.tokens = d.T;
+    a.cls = F(h, ELASTO_T_CLS);
+    a.pos = F(h, ELASTO_T_POS);
+    e = timed(h, ELASTO_K_PATCH, s, [&] { return gemm(Epi::Patch, a, s); });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "patch embedding: %s", hipGetErrorString(e));
+  }
+  for (int l = 0; l < L; ++l) {
+    const int hh = h->n_heads[(size_t)k * L + l], mm = h->n_mlp[(size_t)k * L + l];
+    e = timed(h, ELASTO_K_LN, s, [&] {
+      return ln(h->x, D, h->u, rows, D, F(h, ELASTO_T_LN1_G, l), F(h, ELASTO_T_LN1_B, l), c.ln_eps, s);
+    });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln1 layer %d: %s", l, hipGetErrorString(e));
+    GemmArgs q;
+    q.A = h->u; q.lda = D;
+    q.W = W(h, ELASTO_T_WQKV, l); q.ldw = D;
+    q.C = h->qkv; q.ldc = 3 * D;
+    q.bias = F(h, ELASTO_T_BQKV, l);
+    q.M = rows; q.N = 3 * d.hd * hh; q.K = D;
+    e = timed(h, ELASTO_K_QKV, s, [&] { return gemm(Epi::Bias, q, s); });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "qkv layer %d: %s", l, hipGetErrorString(e));
+    AttnArgs at;
+    at.qkv = h->qkv; at.qkv_stride = 3 * D;
+    at.o = h->o; at.o_stride = D;
+    at.batch = batch; at.tokens = d.T; at.heads = hh; at.head_dim = d.hd; at.scale = scale;
+    e = timed(h, ELASTO_K_ATTN, s, [&] { return attn(at, s); });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "attention layer %d: %s", l, hipGetErrorString(e));
+    GemmArgs pr;
+    pr.A = h->o; pr.lda = D;
+    pr.W = W(h, ELASTO_T_WO, l); pr.ldw = D;
+    pr.C = h->x; pr.ldc = D;
+    pr.bias = F(h, ELASTO_T_BO, l);
+    pr.M = rows; pr.N = D; pr.K = d.hd * hh;
+    e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
+    e = timed(h, ELASTO_K_LN, s, [&] {
+      return ln(h->x, D, h->u, rows, D, F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l), c.ln_eps, s);
+    });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln2 layer %d: %s", l, hipGetErrorString(e));
+    GemmArgs f1;
+    f1.A = h->u; f1.lda = D;
+    f1.W = W(h, ELASTO_T_W1, l); f1.ldw = D;
+    f1.C = h->g; f1.ldc = Mh;
+    f1.bias = F(h, ELASTO_T_B1, l);
+    f1.M = rows; f1.N = mm; f1.K = D;
+    e = timed(h, ELASTO_K_FC1, s, [&] { return gemm(Epi::BiasGelu, f1, s); });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc1 layer %d: %s", l, hipGetErrorString(e));
+    GemmArgs f2;
+    f2.A = h->g; f2.lda = Mh;
+    f2.W = W(h, ELASTO_T_W2, l); f2.ldw = Mh;
+    f2.C = h->x; f2.ldc = D;
+    f2.bias = F(h, ELASTO_T_B2, l);
+    f2.M = rows; f2.N = D; f2.K = mm;
+    e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
+  }
+  e = timed(h, ELASTO_K_LN, s, [&] {
+    return ln(h->x, (int64_t)d.T * D, h->ucls, batch, D, F(h, ELASTO_T_NORM_G), F(h, ELASTO_T_NORM_B),
+              c.ln_eps, s);
+  });
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "final norm: %s", hipGetErrorString(e));
+  GemmArgs hg;
+  hg.A = h->ucls; hg.lda = D;
+  hg.W = W(h, ELASTO_T_HEAD_W); hg.ldw = D;
+  hg.C = logits; hg.ldc = c.num_classes;
+  hg.bias = F(h, ELASTO_T_HEAD_B);
+  hg.M = batch; hg.N = c.num_classes; hg.K = D;
+  e = timed(h, ELASTO_K_HEAD, s, [&] { return gemm(Epi::BiasF32, hg, s); });
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "head: %s", hipGetErrorString(e));
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_kernel_timing(elasto_handle_t h, int32_t kc, int32_t max_launches) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (kc < -1 || kc >= ELASTO_K_COUNT) return fail(ELASTO_ERR_INVALID_ARG, "kernel class %d out of range", kc);
+  destroy_events(h);
+  if (kc < 0) return ELASTO_OK;
+  if (max_launches < 1 || max_launches > (1 << 20))
+    return fail(ELASTO_ERR_INVALID_ARG, "max_launches %d outside [1, 2^20]", max_launches);
+  h->events.resize((size_t)2 * max_launches, nullptr);
+  for (auto& ev : h->events) {
+    if (hipEventCreate(&ev) != hipSuccess) {
+      ev = nullptr;
+      destroy_events(h);
+      return fail(ELASTO_ERR_HIP, "hipEventCreate failed");
+    }
+  }
+  h->timed_class = kc;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_kernel_timing_read(elasto_handle_t h, double* total_ms, int64_t* launches) {
+  if (!h || !total_ms || !launches) return fail(ELASTO_ERR_INVALID_ARG, "NULL argument");
+  double sum = 0.0;
+  for (int i = 0; i < h->used; ++i) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(h->events[2 * i + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, h->events[2 * i], h->events[2 * i + 1]);
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "event read: %s", hipGetErrorString(e));
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = h->used;
+  h->used = 0;
+  h->skipped = 0;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, int32_t kc,
+                                   double* flops, double* bytes, int32_t* launches) {
+  if (!h || !flops || !bytes || !launches) return fail(ELASTO_ERR_INVALID_ARG, "NULL argument");
+  if (k < 0 || k >= h->num_modes) return fail(ELASTO_ERR_MODE_RANGE, "mode %d outside [0, %d)", k, h->num_modes);
+  if (batch < 1) return fail(ELASTO_ERR_BATCH_RANGE, "batch must be >= 1");
+  if (kc < 0 || kc >= ELASTO_K_COUNT) return fail(ELASTO_ERR_INVALID_ARG, "kernel class %d out of range", kc);
+  const elasto_config_t& c = h->cfg;
+  const Dims& d = h->dims;
+  const double eb = c.dtype == ELASTO_BF16 ? 2.0 : 4.0;
+  const double B = batch, T = d.T, D = c.dim, hd = d.hd, Np = (double)d.grid * d.grid;
+  const double Mr = B * T;
+  double f = 0, by = 0;
+  int n = 0;
+  switch (kc) {
+    case ELASTO_K_PATCH:
+      f = 2.0 * B * Np * d.patch_k * D;
+      by = (B * c.in_chans * (double)c.img * c.img + D * d.patch_k + Mr * D) * eb;
+      n = 1;
+      break;
+    case ELASTO_K_LN:
+      by = (2.0 * c.depth * Mr * D + B * D) * 2.0 * eb;
+      n = 2 * c.depth + 1;
+      break;
+    case ELASTO_K_HEAD:
+      f = 2.0 * B * c.num_classes * D;
+      by = (B * D + (double)c.num_classes * D) * eb + B * c.num_classes * 4.0;
+      n = 1;
+      break;
+    default:
+      for (int l = 0; l < c.depth; ++l) {
+        const double hh = h->n_heads[(size_t)k * c.depth + l], mm = h->n_mlp[(size_t)k * c.depth + l];
+        switch (kc) {
+          case ELASTO_K_QKV:
+            f += 2.0 * Mr * 3 * hd * hh * D;
+            by += (Mr * D + 3 * hd * hh * D + Mr * 3 * hd * hh) * eb;
+            break;
+          case ELASTO_K_ATTN:
+            f += 4.0 * B * hh * T * T * hd;
+            by += (Mr * 3 * hd * hh + Mr * hd * hh) * eb;
+            break;
+          case ELASTO_K_PROJ:
+            f += 2.0 * Mr * D * hd * hh;
+            by += (Mr * hd * hh + D * hd * hh + 2.0 * Mr * D) * eb;
+            break;
+          case ELASTO_K_FC1:
+            f += 2.0 * Mr * mm * D;
+            by += (Mr * D + mm * D + Mr * mm) * eb;
+            break;
+          case ELASTO_K_FC2:
+            f += 2.0 * Mr * D * mm;
+            by += (Mr * mm + D * mm + 2.0 * Mr * D) * eb;
+            break;
+        }
+      }
+      n = c.depth;
+  }
+  *flops = f;
+  *bytes = by;
+  *launches = n;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride, void* out,
+                                    int64_t rows, int32_t d, const float* g, const float* b,
+                                    float eps, void* hip_stream) {
+  if (!x || !out || !g || !b) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if (rows < 0 || d < 1 || d > 2048 || x_stride < d || !(eps > 0.0f))
+    return fail(ELASTO_ERR_INVALID_ARG, "bad layernorm sizes");
+  hipError_t e;
+  if (dtype == ELASTO_BF16) {
+    if (d % 4 != 0 || x_stride % 4 != 0 || !aligned(x, 8) || !aligned(out, 8) || !aligned(g, 16) || !aligned(b, 16))
+      return fail(ELASTO_ERR_INVALID_ARG, "bf16 layernorm needs d, stride % 4 == 0 and aligned pointers");
+    e = launch_layernorm_bf16(x, x_stride, out, rows, d, g, b, eps, static_cast<hipStream_t>(hip_stream));
+  } else if (dtype == ELASTO_FP32) {
+    e = launch_layernorm_f32(x, x_stride, out, rows, d, g, b, eps, static_cast<hipStream_t>(hip_stream));
+  } else {
+    return fail(ELASTO_ERR_INVALID_ARG, "bad dtype %d", dtype);
+  }
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "layernorm: %s", hipGetErrorString(e));
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A, int64_t lda,
+                                 const void* Wt, int64_t ldw, void* C, int64_t ldc,
+                                 const float* bias, int64_t M, int32_t N, int32_t K,
+                                 void* hip_stream) {
+  if (!A || !Wt || !C || !bias) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if (M < 0 || M >= ((int64_t)1 << 31) || N < 1 || K < 1 || lda < K || ldw < K || ldc < N)
+    return fail(ELASTO_ERR_INVALID_ARG, "bad linear sizes");
+  if (epilogue < ELASTO_EPI_BIAS || epilogue > ELASTO_EPI_BIAS_F32OUT)
+    return fail(ELASTO_ERR_INVALID_ARG, "bad epilogue %d", epilogue);
+  GemmArgs a;
+  a.A = A; a.lda = lda; a.W = Wt; a.ldw = ldw; a.C = C; a.ldc = ldc; a.bias = bias;
+  a.M = M; a.N = N; a.K = K;
+  const Epi epi = static_cast<Epi>(epilogue);
+  hipError_t e;
+  if (dtype == ELASTO_BF16) {
+    if (lda % 8 || ldw % 8 || !aligned(A, 16) || !aligned(Wt, 16))
+      return fail(ELASTO_ERR_INVALID_ARG, "bf16 linear needs lda, ldw % 8 == 0 and 16-byte aligned A, W");
+    e = launch_gemm_bf16(epi, a, static_cast<hipStream_t>(hip_stream));
+  } else if (dtype == ELASTO_FP32) {
+    e = launch_gemm_f32(epi, a, static_cast<hipStream_t>(hip_stream));
+  } else {
+    return fail(ELASTO_ERR_INVALID_ARG, "bad dtype %d", dtype);
+  }
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "linear: %s", hipGetErrorString(e));
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_stride, void* o,
+                                    int64_t o_stride, int32_t batch, int32_t tokens,
+                                    int32_t heads, int32_t head_dim, float scale,
+                                    void* hip_stream) {
+  if (!qkv || !o) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if (batch < 0 || tokens < 1 || heads < 1 || head_dim < 1 || qkv_stride < 3LL * heads * head_dim ||
+      o_stride < (int64_t)heads * head_dim)
+    return fail(ELASTO_ERR_INVALID_ARG, "bad attention sizes");
+  AttnArgs a;
+  a.qkv = qkv; a.qkv_stride = qkv_stride; a.o = o; a.o_stride = o_stride;
+  a.batch = batch; a.tokens = tokens; a.heads = heads; a.head_dim = head_dim; a.scale = scale;
+  hipError_t e;
+  if (dtype == ELASTO_BF16) {
+    if (head_dim != 64 || tokens > kAttnMaxTokens || qkv_stride % 8 || !aligned(qkv, 16))
+      return fail(ELASTO_ERR_INVALID_ARG, "bf16 attention needs head_dim 64, tokens <= %d, aligned qkv", kAttnMaxTokens);
+    e = launch_attention_bf16(a, static_cast<hipStream_t>(hip_stream));
+  } else if (dtype == ELASTO_FP32) {
+    if (head_dim > 128) return fail(ELASTO_ERR_INVALID_ARG, "fp32 attention needs head_dim <= 128");
+    e = launch_attention_f32(a, static_cast<hipStream_t>(hip_stream));
+  } else {
+    return fail(ELASTO_ERR_INVALID_ARG, "bad dtype %d", dtype);
+  }
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "attention: %s", hipGetErrorString(e));
+  return ELASTO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,230 @@
+// Multi-head self-attention over the active heads (Eq. 3):
+// o = softmax(q k^T * scale) v per (sequence, head slot).
+//
+// bf16 path (head_dim 64): one workgroup per (sequence, head slot).  K is
+// staged whole in LDS (rows of 128 B, 16-byte chunks XOR-swizzled) and V is
+// staged transposed (V^T, one row per feature), zero-padded past the last
+// token.  Each wave takes 16-query blocks in turn and computes the score
+// block transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16: lane l then
+// holds the scores of query l%16 against keys 16j + 4*(l/16) + {0..3}.  The
+// softmax of a query is reduced over its 4 lanes with two xor-shuffles and
+// is exact (single pass: the whole key row fits in registers).  The
+// probabilities are rounded to bf16 and fed straight back as the A operand
+// of O = P V: a k-slot of the MFMA is only a label, so the 8 keys a lane
+// holds for two adjacent key tiles form its k-slots, and the V operand is
+// read from V^T with the same key-to-slot assignment (two 8-byte reads).
+// The 1/rowsum normalisation is applied to O in fp32.
+//
+// fp32 path: a plain per-query loop (two passes over the keys: max, then
+// exp-sum and weighted V sum), fp32 FMA throughout.
+#include "common.h"
+#include "kernels.h"
+
+namespace elasto {
+namespace {
+
+constexpr int kHd = 64;
+constexpr int kNtMax = 16;  // 16-key tiles held in registers: tokens <= 256
+
+__device__ __forceinline__ int k_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+
+struct AttnP {
+  const uint16_t* qkv;
+  int64_t qs;
+  uint16_t* o;
+  int64_t os;
+  int T, heads;
+  float scale_log2;
+};
+
+__global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int T = p.T;
+  const int nt = (T + 15) >> 4;           // 16-key tiles
+  const int tv = ((T + 31) >> 5) << 5;    // keys covered by 32-key PV blocks
+  const int vs = tv + 4;                  // V^T row stride (elements), breaks bank aliasing
+  char* kl = smem;
+  uint16_t* vt = reinterpret_cast<uint16_t*>(smem + nt * 16 * 128);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = blockIdx.x / p.heads, s = blockIdx.x - b * p.heads;
+  const uint16_t* base = p.qkv + (int64_t)b * T * p.qs + (int64_t)s * 3 * kHd;
+
+  for (int i = tid; i < nt * 16 * 8; i += 256) {
+    const int row = i >> 3, c = i & 7;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < T) v = *reinterpret_cast<const u32x4*>(base + (int64_t)row * p.qs + kHd + c * 8);
+    *reinterpret_cast<u32x4*>(kl + k_off(row, c)) = v;
+  }
+  for (int i = tid; i < tv * 8; i += 256) {
+    const int key = i >> 3, c = i & 7;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (key < T) v = *reinterpret_cast<const u32x4*>(base + (int64_t)key * p.qs + 2 * kHd + c * 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      vt[(c * 8 + e) * vs + key] = (uint16_t)((e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu));
+  }
+  __syncthreads();
+
+  const int lq = lane & 15, lg = lane >> 4;
+  for (int qb = wave; qb < nt; qb += 4) {
+    const int q0 = qb * 16;
+    bf16x8 qf[2];
+    {
+      const int q = min(q0 + lq, T - 1);
+      const uint16_t* qp = base + (int64_t)q * p.qs + lg * 8;
+      qf[0] = *reinterpret_cast<const bf16x8*>(qp);
+      qf[1] = *reinterpret_cast<const bf16x8*>(qp + 32);
+    }
+    f32x4 st[kNtMax];
+#pragma unroll
+    for (int j = 0; j < kNtMax; ++j) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if (j < nt) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + k_off(j * 16 + lq, kk * 4 + lg));
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], acc, 0, 0, 0);
+        }
+      }
+      st[j] = acc;
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kNtMax; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (j * 16 + 4 * lg + r < T) mx = fmaxf(mx, st[j][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < kNtMax; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float e = (j * 16 + 4 * lg + r < T) ? exp2f((st[j][r] - mx) * p.scale_log2) : 0.f;
+        st[j][r] = e;
+        sum += e;
+      }
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
+
+    f32x4 o[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) o[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < kNtMax / 2; ++kb) {
+      if (2 * kb < nt) {
+        bf16x8 pa;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pa[r] = static_cast<__bf16>(st[2 * kb][r]);
+          pa[4 + r] = static_cast<__bf16>(st[2 * kb + 1][r]);
+        }
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          const uint16_t* vp = vt + (n * 16 + lq) * vs + kb * 32 + 4 * lg;
+          const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
+          const u32x2 hi = *reinterpret_cast<const u32x2*>(vp + 16);
+          const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+          o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8, w), o[n],
+                                                         0, 0, 0);
+        }
+      }
+    }
+    const float inv = 1.0f / sum;  // for query lq
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qr = 4 * lg + r;
+      const float ir = __shfl(inv, qr, 64);
+      const int q = q0 + qr;
+      if (q < T) {
+        uint16_t* op = p.o + ((int64_t)b * T + q) * p.os + (int64_t)s * kHd + lq;
+#pragma unroll
+        for (int n = 0; n < 4; ++n) op[n * 16] = f32_to_bf16(o[n][r] * ir);
+      }
+    }
+  }
+}
+
+struct AttnF {
+  const float* qkv;
+  int64_t qs;
+  float* o;
+  int64_t os;
+  int T, heads, hd;
+  float scale;
+};
+
+constexpr int kHdMaxF32 = 128;
+
+__global__ __launch_bounds__(256) void attention_f32_kernel(AttnF p) {
+  const int b = blockIdx.x / p.heads, s = blockIdx.x - b * p.heads;
+  const int hd = p.hd;
+  const float* base = p.qkv + (int64_t)b * p.T * p.qs + (int64_t)s * 3 * hd;
+  for (int q = threadIdx.x; q < p.T; q += blockDim.x) {
+    float qv[kHdMaxF32];
+    const float* qp = base + (int64_t)q * p.qs;
+    for (int c = 0; c < hd; ++c) qv[c] = qp[c];
+    float mx = -INFINITY;
+    for (int j = 0; j < p.T; ++j) {
+      const float* kp = base + (int64_t)j * p.qs + hd;
+      float dot = 0.f;
+      for (int c = 0; c < hd; ++c) dot = fmaf(qv[c], kp[c], dot);
+      mx = fmaxf(mx, dot * p.scale);
+    }
+    float acc[kHdMaxF32];
+    for (int c = 0; c < hd; ++c) acc[c] = 0.f;
+    float sum = 0.f;
+    for (int j = 0; j < p.T; ++j) {
+      const float* kp = base + (int64_t)j * p.qs + hd;
+      const float* vp = kp + hd;
+      float dot = 0.f;
+      for (int c = 0; c < hd; ++c) dot = fmaf(qv[c], kp[c], dot);
+      const float e = expf(dot * p.scale - mx);
+      sum += e;
+      for (int c = 0; c < hd; ++c) acc[c] = fmaf(e, vp[c], acc[c]);
+    }
+    const float inv = 1.0f / sum;
+    float* op = p.o + ((int64_t)b * p.T + q) * p.os + (int64_t)s * hd;
+    for (int c = 0; c < hd; ++c) op[c] = acc[c] * inv;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.batch <= 0 || a.heads <= 0 || a.tokens <= 0) return hipSuccess;
+  if (a.head_dim != kHd || a.tokens > kAttnMaxTokens) return hipErrorInvalidValue;
+  AttnP p;
+  p.qkv = static_cast<const uint16_t*>(a.qkv);
+  p.qs = a.qkv_stride;
+  p.o = static_cast<uint16_t*>(a.o);
+  p.os = a.o_stride;
+  p.T = a.tokens;
+  p.heads = a.heads;
+  p.scale_log2 = a.scale * 1.4426950408889634f;
+  const int nt = (a.tokens + 15) / 16, tv = (a.tokens + 31) / 32 * 32;
+  const size_t lds = (size_t)nt * 16 * 128 + (size_t)kHd * (tv + 4) * 2;
+  hipLaunchKernelGGL(attention_bf16_kernel, dim3((unsigned)(a.batch * a.heads)), dim3(256), lds, s,
+                     p);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
+  if (a.batch <= 0 || a.heads <= 0 || a.tokens <= 0) return hipSuccess;
+  if (a.head_dim > kHdMaxF32 || a.head_dim <= 0) return hipErrorInvalidValue;
+  AttnF p;
+  p.qkv = static_cast<const float*>(a.qkv);
+  p.qs = a.qkv_stride;
+  p.o = static_cast<float*>(a.o);
+  p.os = a.o_stride;
+  p.T = a.tokens;
+  p.heads = a.heads;
+  p.hd = a.head_dim;
+  p.scale = a.scale;
+  hipLaunchKernelGGL(attention_f32_kernel, dim3((unsigned)(a.batch * a.heads)), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace elasto

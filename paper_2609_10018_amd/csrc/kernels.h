@@ -1,0 +1,62 @@
+// Internal launchers of the gfx950 kernels (host-side declarations).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace elasto {
+
+enum class Epi : int {
+  Bias = 0,      // C = acc + bias
+  BiasGelu = 1,  // C = GELU(acc + bias)
+  BiasResid = 2, // C = C + acc + bias
+  BiasF32 = 3,   // C (fp32) = acc + bias
+  Patch = 4,     // patch embedding: A rows are image patches (row t == 0 of
+                 // each sequence is the class row), C = acc + (cls|bias) + pos
+};
+
+// C[m][n] = epi(sum_k A[m][k] W[n][k] + bias[n]).
+struct GemmArgs {
+  const void* A = nullptr;
+  int64_t lda = 0;
+  const void* W = nullptr;
+  int64_t ldw = 0;
+  void* C = nullptr;
+  int64_t ldc = 0;
+  const float* bias = nullptr;
+  int64_t M = 0;
+  int N = 0;
+  int K = 0;
+  // Patch loader: A row m = b*tokens + t reads patch t-1 of image b.
+  const void* img = nullptr;
+  int img_size = 0, patch = 0, chans = 0, grid = 0, tokens = 0;
+  const float* cls = nullptr;
+  const float* pos = nullptr;
+};
+
+hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_f32(Epi epi, const GemmArgs& a, hipStream_t s);
+
+// out[r] = LN(x[r]) over d features; x row stride x_stride, out contiguous.
+hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, void* out, int64_t rows, int d,
+                                 const float* g, const float* b, float eps, hipStream_t s);
+hipError_t launch_layernorm_f32(const void* x, int64_t x_stride, void* out, int64_t rows, int d,
+                                const float* g, const float* b, float eps, hipStream_t s);
+
+struct AttnArgs {
+  const void* qkv = nullptr;
+  int64_t qkv_stride = 0;
+  void* o = nullptr;
+  int64_t o_stride = 0;
+  int batch = 0, tokens = 0, heads = 0, head_dim = 0;
+  float scale = 1.0f;
+};
+
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
+
+// Largest token count the bf16 attention kernel supports (K and V^T of one
+// head are staged whole in LDS).
+constexpr int kAttnMaxTokens = 240;
+
+}  // namespace elasto

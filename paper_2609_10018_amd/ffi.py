@@ -1,0 +1,262 @@
+"""ctypes binding of the C ABI in include/elasto.h (argument marshalling only).
+
+Every computation runs in the HIP library; this module converts numpy host
+arrays and torch device tensors into the plain pointers and sizes the C ABI
+takes, and turns status codes into exceptions.  If the library is not built
+this module raises: there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+from .inputs import BF16, FP32, DNTable, ModelConfig
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libelasto.so")
+
+c_i32, c_i64, c_f32, c_f64, c_vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                     ctypes.c_double, ctypes.c_void_p)
+
+STATUS = {0: "OK", 1: "INVALID_ARG", 2: "BAD_CONFIG", 3: "BAD_TABLE", 4: "OUT_OF_MEMORY",
+          5: "HIP", 6: "MODE_RANGE", 7: "BATCH_RANGE"}
+
+# Tensor ids (elasto_tensor_t).
+T_PATCH_W, T_PATCH_B, T_CLS, T_POS, T_NORM_G, T_NORM_B, T_HEAD_W, T_HEAD_B = range(8)
+(T_LN1_G, T_LN1_B, T_WQKV, T_BQKV, T_WO, T_BO, T_LN2_G, T_LN2_B, T_W1, T_B1, T_W2,
+ T_B2) = range(8, 20)
+# Kernel classes (elasto_kernel_t).
+KERNELS = ["patch", "ln", "qkv", "attn", "proj", "fc1", "fc2", "head"]
+# Epilogues (elasto_epilogue_t).
+EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESID, EPI_BIAS_F32OUT = range(4)
+
+WEIGHT_FIELDS = ["patch_w", "patch_b", "cls", "pos", "ln1_g", "ln1_b", "qkv_w", "qkv_b",
+                 "proj_w", "proj_b", "ln2_g", "ln2_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b",
+                 "norm_g", "norm_b", "head_w", "head_b"]
+
+
+class ElastoError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"elasto {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(n, c_i32) for n in ("img", "patch", "in_chans", "dim", "depth", "heads",
+                                     "mlp_hidden", "num_classes", "max_batch", "dtype")] + \
+               [("ln_eps", c_f32)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [(n, c_vp) for n in WEIGHT_FIELDS]
+
+
+class Table(ctypes.Structure):
+    _fields_ = [("num_modes", c_i32), ("depth", c_i32), ("n_heads", c_vp), ("n_mlp", c_vp),
+                ("head_order", c_vp), ("mlp_order", c_vp)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run __graft_entry__.build() or "
+                          f"python -m paper_2609_10018_amd.build")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    sig = {
+        "elasto_create": [P(Config), P(Weights), P(Table), P(c_vp)],
+        "elasto_destroy": [c_vp],
+        "elasto_set_mode": [c_vp, c_i32],
+        "elasto_get_mode": [c_vp, P(c_i32)],
+        "elasto_forward": [c_vp, c_vp, c_i32, c_vp, c_vp],
+        "elasto_mode_info": [c_vp, c_i32, P(c_f64), P(c_i64)],
+        "elasto_memory_info": [c_vp, P(c_i64), P(c_i64)],
+        "elasto_validate": [P(Config), P(Table)],
+        "elasto_packed_bytes": [P(Config), P(c_i64)],
+        "elasto_packed_layout": [P(Config), c_i32, c_i32, P(c_i64), P(c_i64), P(c_i64), P(c_i32)],
+        "elasto_pack_weights": [P(Config), P(Weights), P(Table), c_vp, c_i64],
+        "elasto_kernel_timing": [c_vp, c_i32, c_i32],
+        "elasto_kernel_timing_read": [c_vp, P(c_f64), P(c_i64)],
+        "elasto_kernel_work": [c_vp, c_i32, c_i32, c_i32, P(c_f64), P(c_f64), P(c_i32)],
+        "elasto_op_layernorm": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_vp, c_f32, c_vp],
+        "elasto_op_linear": [c_i32, c_i32, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
+                             c_i32, c_i32, c_vp],
+        "elasto_op_attention": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32,
+                                c_f32, c_vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = c_i32
+    lib.elasto_last_error.argtypes = []
+    lib.elasto_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load_library().elasto_last_error().decode()
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise ElastoError(status, last_error())
+
+
+def make_config(cfg: ModelConfig, max_batch: int) -> Config:
+    return Config(cfg.img, cfg.patch, cfg.in_chans, cfg.dim, cfg.depth, cfg.heads,
+                  cfg.mlp_hidden, cfg.num_classes, max_batch, cfg.dtype, cfg.ln_eps)
+
+
+class _HostWeights:
+    """Keeps contiguous fp32 copies alive while the C struct points at them."""
+
+    def __init__(self, w: Dict[str, np.ndarray]):
+        self.arrays = {k: np.ascontiguousarray(w[k], dtype=np.float32) for k in WEIGHT_FIELDS}
+        self.struct = Weights(*[a.ctypes.data for a in (self.arrays[k] for k in WEIGHT_FIELDS)])
+
+
+class _HostTable:
+    def __init__(self, t: DNTable):
+        self.arrays = [np.ascontiguousarray(a, dtype=np.int32)
+                       for a in (t.n_heads, t.n_mlp, t.head_order, t.mlp_order)]
+        self.struct = Table(int(t.n_heads.shape[0]), int(t.n_heads.shape[1]),
+                            *[a.ctypes.data for a in self.arrays])
+
+
+def validate(cfg: ModelConfig, table: DNTable, max_batch: int = 1) -> int:
+    c = make_config(cfg, max_batch)
+    t = _HostTable(table)
+    return load_library().elasto_validate(ctypes.byref(c), ctypes.byref(t.struct))
+
+
+def packed_bytes(cfg: ModelConfig) -> int:
+    out = c_i64()
+    check(load_library().elasto_packed_bytes(ctypes.byref(make_config(cfg, 1)), ctypes.byref(out)))
+    return out.value
+
+
+def packed_layout(cfg: ModelConfig, tensor: int, layer: int = 0):
+    off, rows, cols, eb = c_i64(), c_i64(), c_i64(), c_i32()
+    check(load_library().elasto_packed_layout(ctypes.byref(make_config(cfg, 1)), tensor, layer,
+                                              ctypes.byref(off), ctypes.byref(rows),
+                                              ctypes.byref(cols), ctypes.byref(eb)))
+    return off.value, rows.value, cols.value, eb.value
+
+
+def pack_weights(cfg: ModelConfig, w: Dict[str, np.ndarray], table: DNTable) -> np.ndarray:
+    n = packed_bytes(cfg)
+    dst = np.zeros(n, dtype=np.uint8)
+    hw, ht = _HostWeights(w), _HostTable(table)
+    check(load_library().elasto_pack_weights(ctypes.byref(make_config(cfg, 1)),
+                                             ctypes.byref(hw.struct), ctypes.byref(ht.struct),
+                                             dst.ctypes.data, n))
+    return dst
+
+
+def _stream_ptr(stream) -> int:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+class ElasticViT:
+    """One library handle: packed weights on the current device + scratch."""
+
+    def __init__(self, cfg: ModelConfig, w: Dict[str, np.ndarray], table: DNTable,
+                 max_batch: int):
+        self.lib = load_library()
+        self.cfg = cfg
+        self.max_batch = max_batch
+        self.num_modes = int(table.n_heads.shape[0])
+        c = make_config(cfg, max_batch)
+        hw, ht = _HostWeights(w), _HostTable(table)
+        h = c_vp()
+        check(self.lib.elasto_create(ctypes.byref(c), ctypes.byref(hw.struct),
+                                     ctypes.byref(ht.struct), ctypes.byref(h)))
+        self.h = h
+
+    def close(self) -> None:
+        if getattr(self, "h", None) is not None and self.h.value:
+            check(self.lib.elasto_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_mode(self, k: int) -> None:
+        check(self.lib.elasto_set_mode(self.h, int(k)))
+
+    def get_mode(self) -> int:
+        k = c_i32()
+        check(self.lib.elasto_get_mode(self.h, ctypes.byref(k)))
+        return k.value
+
+    def forward(self, images, logits, stream=None) -> None:
+        """images: device tensor NCHW (bf16 or fp32 per the path); logits: fp32 device tensor."""
+        if not images.is_contiguous() or not logits.is_contiguous():
+            raise ValueError("images and logits must be contiguous")
+        check(self.lib.elasto_forward(self.h, images.data_ptr(), int(images.shape[0]),
+                                      logits.data_ptr(), _stream_ptr(stream)))
+
+    def mode_info(self, k: int):
+        f, b = c_f64(), c_i64()
+        check(self.lib.elasto_mode_info(self.h, int(k), ctypes.byref(f), ctypes.byref(b)))
+        return f.value, b.value
+
+    def memory_info(self):
+        wb, sb = c_i64(), c_i64()
+        check(self.lib.elasto_memory_info(self.h, ctypes.byref(wb), ctypes.byref(sb)))
+        return wb.value, sb.value
+
+    def kernel_timing(self, kernel: str, max_launches: int) -> None:
+        kc = -1 if kernel is None else KERNELS.index(kernel)
+        check(self.lib.elasto_kernel_timing(self.h, kc, int(max_launches)))
+
+    def kernel_timing_read(self):
+        ms, n = c_f64(), c_i64()
+        check(self.lib.elasto_kernel_timing_read(self.h, ctypes.byref(ms), ctypes.byref(n)))
+        return ms.value, n.value
+
+    def kernel_work(self, k: int, batch: int, kernel: str):
+        f, b, n = c_f64(), c_f64(), c_i32()
+        check(self.lib.elasto_kernel_work(self.h, int(k), int(batch), KERNELS.index(kernel),
+                                          ctypes.byref(f), ctypes.byref(b), ctypes.byref(n)))
+        return f.value, b.value, n.value
+
+
+def op_layernorm(dtype: int, x, x_stride: int, out, rows: int, d: int, g, b, eps: float,
+                 stream=None) -> None:
+    check(load_library().elasto_op_layernorm(dtype, x.data_ptr(), x_stride, out.data_ptr(), rows,
+                                             d, g.data_ptr(), b.data_ptr(), eps,
+                                             _stream_ptr(stream)))
+
+
+def op_linear(dtype: int, epilogue: int, A, lda: int, W, ldw: int, C, ldc: int, bias,
+              M: int, N: int, K: int, stream=None) -> None:
+    check(load_library().elasto_op_linear(dtype, epilogue, A.data_ptr(), lda, W.data_ptr(), ldw,
+                                          C.data_ptr(), ldc, bias.data_ptr(), M, N, K,
+                                          _stream_ptr(stream)))
+
+
+def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int, tokens: int,
+                 heads: int, head_dim: int, scale: float, stream=None) -> None:
+    check(load_library().elasto_op_attention(dtype, qkv.data_ptr(), qkv_stride, o.data_ptr(),
+                                             o_stride, batch, tokens, heads, head_dim, scale,
+                                             _stream_ptr(stream)))
+
+
+__all__ = ["ElasticViT", "ElastoError", "load_library", "validate", "packed_bytes",
+           "packed_layout", "pack_weights", "op_layernorm", "op_linear", "op_attention",
+           "KERNELS", "FP32", "BF16"]

@@ -1,0 +1,165 @@
+"""C-ABI checks that need no GPU: exported symbols, validation error codes,
+and the packed prefix layout against a numpy gather (CPU only)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_10018_amd import ffi, inputs
+from paper_2609_10018_amd.inputs import CONFIGS, DNTable
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "elasto.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ffi.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(elasto_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function(lib):
+    names = declared_functions()
+    assert "elasto_create" in names and "elasto_forward" in names and "elasto_set_mode" in names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _table_copy(t):
+    return DNTable(t.n_heads.copy(), t.n_mlp.copy(), t.head_order.copy(), t.mlp_order.copy())
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_valid_tables_pass(lib, name):
+    cfg = CONFIGS[name]
+    assert ffi.validate(cfg, inputs.make_dn_table(cfg), cfg.batch) == 0
+
+
+def test_bad_tables_rejected(lib):
+    cfg = CONFIGS["vit_ti"]
+    base = inputs.make_dn_table(cfg)
+    bad = []
+    t = _table_copy(base); t.n_heads[1, 3] = 0; bad.append(t)
+    t = _table_copy(base); t.n_heads[0, 0] = cfg.heads + 1; bad.append(t)
+    t = _table_copy(base); t.n_mlp[2, 5] = cfg.mlp_hidden + 1; bad.append(t)
+    t = _table_copy(base); t.n_mlp[2, 5] = -3; bad.append(t)
+    t = _table_copy(base); t.head_order[4, 0] = t.head_order[4, 1]; bad.append(t)
+    t = _table_copy(base); t.mlp_order[0, 7] = cfg.mlp_hidden; bad.append(t)
+    t = DNTable(base.n_heads[:, :5].copy(), base.n_mlp[:, :5].copy(), base.head_order[:5].copy(),
+                base.mlp_order[:5].copy()); bad.append(t)
+    for t in bad:
+        assert ffi.validate(cfg, t, 4) == 3, ffi.last_error()
+        assert ffi.last_error()
+
+
+@pytest.mark.parametrize("change,code", [
+    (dict(dim=190), 2),                # dim % heads != 0
+    (dict(img=220), 2),                # img % patch != 0
+    (dict(heads=4), 2),                # bf16 head_dim 48 != 64
+    (dict(patch=12, img=216), 2),      # bf16 patch % 8 != 0
+    (dict(mlp_hidden=0), 2),
+    (dict(ln_eps=0.0), 2),
+    (dict(dtype=7), 2),
+])
+def test_bad_configs_rejected(lib, change, code):
+    import dataclasses
+    cfg = dataclasses.replace(CONFIGS["vit_ti"], **change)
+    table = inputs.make_dn_table(CONFIGS["vit_ti"])
+    assert ffi.validate(cfg, table, 4) == code
+
+
+def test_create_rejects_before_any_hip_call(lib):
+    cfg = CONFIGS["tiny"]
+    w = inputs.make_weights(cfg)
+    t = inputs.make_dn_table(cfg)
+    t.n_heads[1, 0] = 5
+    with pytest.raises(ffi.ElastoError) as e:
+        ffi.ElasticViT(cfg, w, t, 4)
+    assert e.value.status == 3
+    import dataclasses
+    with pytest.raises(ffi.ElastoError) as e:
+        ffi.ElasticViT(dataclasses.replace(cfg, dim=63), w, inputs.make_dn_table(cfg), 4)
+    assert e.value.status == 2
+
+
+def test_null_handle_calls_fail_cleanly(lib):
+    assert lib.elasto_set_mode(None, 0) == 1
+    assert lib.elasto_forward(None, None, 1, None, None) == 1
+    assert lib.elasto_destroy(None) == 0
+    k = ctypes.c_int32()
+    assert lib.elasto_get_mode(None, ctypes.byref(k)) == 1
+
+
+def _view(buf, cfg, tensor, layer=0):
+    off, rows, cols, eb = ffi.packed_layout(cfg, tensor, layer)
+    assert off % 256 == 0
+    if eb == 2:
+        raw = buf[off:off + rows * cols * 2].view(np.uint16).reshape(rows, cols)
+        return (raw.astype(np.uint32) << 16).view(np.float32)
+    return buf[off:off + rows * cols * 4].view(np.float32).reshape(rows, cols)
+
+
+@pytest.mark.parametrize("name", ["tiny", "vit_ti"])
+def test_pack_equals_numpy_gather(lib, name):
+    cfg = CONFIGS[name]
+    w = inputs.make_weights(cfg)
+    t = inputs.make_dn_table(cfg)
+    buf = ffi.pack_weights(cfg, w, t)
+    sw = inputs.stored_weights(cfg, w)      # bf16-rounded matrices on the bf16 path
+    d, hd, H = cfg.dim, cfg.head_dim, cfg.heads
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_PATCH_W), sw["patch_w"].reshape(d, -1))
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_POS), sw["pos"])
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W), sw["head_w"])
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_CLS)[0], sw["cls"])
+    for l in range(cfg.depth):
+        ho, mo = t.head_order[l], t.mlp_order[l]
+        rows = np.array([tq * d + ho[s] * hd + c for s in range(H) for tq in range(3)
+                         for c in range(hd)])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_WQKV, l), sw["qkv_w"][l][rows])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_BQKV, l)[0], sw["qkv_b"][l][rows])
+        cols = np.array([ho[s] * hd + c for s in range(H) for c in range(hd)])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_WO, l), sw["proj_w"][l][:, cols])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W1, l), sw["fc1_w"][l][mo])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_B1, l)[0], sw["fc1_b"][l][mo])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W2, l), sw["fc2_w"][l][:, mo])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_LN2_G, l)[0], sw["ln2_g"][l])
+
+
+def test_packed_prefix_is_what_mode_k_reads(lib):
+    """The first n rows of WQKV / W1 are exactly mode k's active heads / units."""
+    cfg = CONFIGS["vit_ti"]
+    w = inputs.make_weights(cfg)
+    t = inputs.make_dn_table(cfg)
+    buf = ffi.pack_weights(cfg, w, t)
+    sw = inputs.stored_weights(cfg, w)
+    import oracle
+    for k in range(t.num_modes):
+        p = oracle.extract_dense(sw, cfg, t, k)
+        for l in range(cfg.depth):
+            h, m = int(t.n_heads[k, l]), int(t.n_mlp[k, l])
+            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W1, l)[:m], p["layers"][l]["fc1_w"])
+            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W2, l)[:, :m], p["layers"][l]["fc2_w"])
+            wo = _view(buf, cfg, ffi.T_WO, l)[:, :h * cfg.head_dim]
+            np.testing.assert_array_equal(wo, p["layers"][l]["proj_w"])
+            packed_q = _view(buf, cfg, ffi.T_WQKV, l)[:3 * cfg.head_dim * h]
+            pq = packed_q.reshape(h, 3, cfg.head_dim, cfg.dim).transpose(1, 0, 2, 3)
+            np.testing.assert_array_equal(pq.reshape(-1, cfg.dim), p["layers"][l]["qkv_w"])
+
+
+def test_bf16_rounding_agrees_with_numpy_rne(lib):
+    cfg = CONFIGS["vit_ti"]
+    w = inputs.make_weights(cfg)
+    rng = np.random.default_rng(3)
+    special = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -0.0, 65504.0, 1e-40, 3.3895e38],
+                       dtype=np.float32)
+    w["head_w"] = w["head_w"].copy()
+    w["head_w"].reshape(-1)[:special.size] = special
+    w["head_w"].reshape(-1)[special.size:special.size + 100] = rng.standard_normal(100) * 1e3
+    buf = ffi.pack_weights(cfg, w, inputs.make_dn_table(cfg))
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W), inputs.bf16_round(w["head_w"]))

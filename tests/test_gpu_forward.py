@@ -1,0 +1,160 @@
+"""End-to-end parity of the HIP forward (through the C ABI) with the fp64
+oracle, for every DN mode of every model config, plus the prefix-read
+(NaN-poison) test, mode switching and batch edge cases."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_10018_amd import ffi, inputs
+from paper_2609_10018_amd.inputs import CONFIGS
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import images_on_device, rel_err, top1_agreement  # noqa: E402
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+FP32_TOL = 1e-4
+BF16_TOL = 2e-2
+TOP1_MIN = 0.995
+
+
+def golden(name):
+    return np.load(os.path.join(GOLDEN, f"logits_{name}.npz"))["logits"]
+
+
+class Model:
+    def __init__(self, name, max_batch=None, weights=None):
+        self.cfg = CONFIGS[name]
+        self.w = weights if weights is not None else inputs.make_weights(self.cfg)
+        self.table = inputs.make_dn_table(self.cfg)
+        self.max_batch = max_batch or self.cfg.batch
+        self.vit = ffi.ElasticViT(self.cfg, self.w, self.table, self.max_batch)
+        self.x = inputs.make_images(self.cfg, self.max_batch)
+        self.xd = images_on_device(self.cfg, self.x)
+
+    def run(self, k, batch=None):
+        batch = batch or self.max_batch
+        self.vit.set_mode(k)
+        logits = torch.empty((batch, self.cfg.num_classes), dtype=torch.float32, device="cuda")
+        self.vit.forward(self.xd[:batch], logits)
+        torch.cuda.synchronize()
+        return logits.cpu().numpy()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ffi.load_library()
+
+
+_models = {}
+
+
+def model(name):
+    if name not in _models:
+        _models[name] = Model(name)
+    return _models[name]
+
+
+def test_tiny_fp32_all_modes():
+    m = model("tiny")
+    for k in range(m.table.num_modes):
+        got = m.run(k)
+        ref = oracle.elastic_forward(m.w, m.cfg, m.table, k, m.x)
+        err = rel_err(got, ref)
+        print(f"tiny mode {k}: rel err {err:.3e}")
+        assert err <= FP32_TOL
+
+
+@pytest.mark.parametrize("name", ["vit_ti", "vit_s", "vit_b"])
+def test_bf16_all_modes_match_oracle(name):
+    m = model(name)
+    gold = golden(name)
+    assert gold.shape == (m.table.num_modes, m.cfg.batch, m.cfg.num_classes)
+    for k in range(m.table.num_modes):
+        got = m.run(k)
+        assert np.isfinite(got).all()
+        err = rel_err(got, gold[k])
+        raw, tie = top1_agreement(got, gold[k])
+        print(f"{name} mode {k}: rel err {err:.3e}, top-1 raw {raw:.4f} tie-aware {tie:.4f}")
+        assert err <= BF16_TOL
+        assert tie >= TOP1_MIN
+
+
+def test_forward_is_deterministic_and_switch_copies_nothing():
+    m = model("vit_s")
+    a = m.run(2)
+    wb0, sb0 = m.vit.memory_info()
+    free0 = torch.cuda.mem_get_info()[0]
+    for i in range(1000):
+        m.vit.set_mode(i % m.table.num_modes)
+    assert torch.cuda.mem_get_info()[0] == free0
+    assert m.vit.memory_info() == (wb0, sb0)
+    b = m.run(2)
+    np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("batch", [1, 3, 255])
+def test_vit_b_partial_batches(batch):
+    m = model("vit_b")
+    gold = golden("vit_b")
+    for k in (0, 4):
+        got = m.run(k, batch)
+        assert rel_err(got, gold[k][:batch]) <= BF16_TOL
+
+
+def _poison_outside(w, cfg, table, k):
+    """Copy of w with every weight outside mode k's active heads / units = NaN."""
+    p = {key: np.array(v, copy=True) for key, v in w.items()}
+    d, hd = cfg.dim, cfg.head_dim
+    for l in range(cfg.depth):
+        act_h, act_m = oracle.active_sets(table, k, l)
+        off_h = np.setdiff1d(np.arange(cfg.heads), act_h)
+        off_m = np.setdiff1d(np.arange(cfg.mlp_hidden), act_m)
+        for i in off_h:
+            for t in range(3):
+                p["qkv_w"][l][t * d + i * hd:t * d + (i + 1) * hd] = np.nan
+                p["qkv_b"][l][t * d + i * hd:t * d + (i + 1) * hd] = np.nan
+            p["proj_w"][l][:, i * hd:(i + 1) * hd] = np.nan
+        p["fc1_w"][l][off_m] = np.nan
+        p["fc1_b"][l][off_m] = np.nan
+        p["fc2_w"][l][:, off_m] = np.nan
+    return p
+
+
+@pytest.mark.parametrize("name,k", [("tiny", 1), ("vit_s", 3), ("vit_s", 4), ("vit_b", 4)])
+def test_prefix_read_nan_poison(name, k):
+    """Mode k never reads a weight outside its prefix, ragged tails included."""
+    clean = model(name)
+    ref = clean.run(k)
+    poisoned = Model(name, weights=_poison_outside(clean.w, clean.cfg, clean.table, k))
+    got = poisoned.run(k)
+    poisoned.vit.close()
+    assert np.isfinite(got).all()
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_error_paths_on_device():
+    m = model("tiny")
+    logits = torch.empty((m.max_batch + 1, m.cfg.num_classes), device="cuda")
+    big = torch.zeros((m.max_batch + 1,) + tuple(m.xd.shape[1:]), device="cuda")
+    with pytest.raises(ffi.ElastoError) as e:
+        m.vit.forward(big, logits)
+    assert e.value.status == 7
+    with pytest.raises(ffi.ElastoError) as e:
+        m.vit.set_mode(m.table.num_modes)
+    assert e.value.status == 6
+    assert m.vit.get_mode() in range(m.table.num_modes)
+
+
+def test_mode_info_matches_cost_model():
+    from paper_2609_10018_amd import cost
+    m = model("vit_b")
+    for k in range(m.table.num_modes):
+        f, wbytes = m.vit.mode_info(k)
+        assert f == pytest.approx(cost.flops_per_image(m.cfg, m.table, k), rel=1e-12)
+        assert wbytes == 2 * cost.active_weight_elems(m.cfg, m.table, k)

@@ -1,0 +1,156 @@
+"""Kernel-level parity: each HIP kernel (through the C ABI's single-kernel
+entry points) against the oracle's fp64 pieces on the same inputs."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_10018_amd import ffi, inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import dev, rel_err  # noqa: E402
+
+BF16, FP32 = inputs.BF16, inputs.FP32
+
+
+def host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ffi.load_library()
+
+
+@pytest.mark.parametrize("dtype,rows,d", [(BF16, 1000, 768), (BF16, 197, 192), (BF16, 5, 384),
+                                          (FP32, 68, 64), (FP32, 300, 200)])
+def test_layernorm(dtype, rows, d):
+    rng = np.random.default_rng(rows + d)
+    x = (rng.standard_normal((rows, d)) * 2 + 0.5).astype(np.float32)
+    g = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(d)).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == BF16 else torch.float32
+    xd = dev(x, tdt)
+    out = torch.empty_like(xd)
+    gd, bd = dev(g, torch.float32), dev(b, torch.float32)
+    ffi.op_layernorm(dtype, xd, d, out, rows, d, gd, bd, 1e-6)
+    torch.cuda.synchronize()
+    ref = oracle.layer_norm(host(xd), g.astype(np.float64), b.astype(np.float64), 1e-6)
+    tol = 8e-3 if dtype == BF16 else 2e-6
+    assert rel_err(host(out), ref) < tol
+
+
+def test_layernorm_strided_rows():
+    rng = np.random.default_rng(1)
+    T, d, B = 197, 768, 4
+    x = rng.standard_normal((B * T, d)).astype(np.float32)
+    xd = dev(x, torch.bfloat16)
+    out = torch.empty((B, d), dtype=torch.bfloat16, device="cuda")
+    g = dev(np.ones(d), torch.float32)
+    b = dev(np.zeros(d), torch.float32)
+    ffi.op_layernorm(BF16, xd, T * d, out, B, d, g, b, 1e-6)
+    torch.cuda.synchronize()
+    ref = oracle.layer_norm(host(xd)[::T], np.ones(d), np.zeros(d), 1e-6)
+    assert rel_err(host(out), ref) < 8e-3
+
+
+def _linear_case(dtype, epi, M, N, K, lda, ldw, ldc, poison=False, seed=0):
+    rng = np.random.default_rng(seed)
+    tdt = torch.bfloat16 if dtype == BF16 else torch.float32
+    A = rng.standard_normal((M, lda)).astype(np.float32)
+    W = (rng.standard_normal((N + 7, ldw)) * 0.05).astype(np.float32)
+    if poison:
+        A[:, K:] = np.nan
+        W[:, K:] = np.nan
+        W[N:, :] = np.nan
+    bias = (0.1 * rng.standard_normal(N)).astype(np.float32)
+    C0 = rng.standard_normal((M, ldc)).astype(np.float32)
+    Ad, Wd = dev(A, tdt), dev(W, tdt)
+    out_f32 = epi == ffi.EPI_BIAS_F32OUT
+    Cd = dev(C0, torch.float32 if out_f32 else tdt)
+    C_before = host(Cd)
+    ffi.op_linear(dtype, epi, Ad, lda, Wd, ldw, Cd, ldc, dev(bias, torch.float32), M, N, K)
+    torch.cuda.synchronize()
+    a64, w64 = host(Ad)[:, :K], host(Wd)[:N, :K]
+    z = a64 @ w64.T + bias.astype(np.float64)
+    if epi == ffi.EPI_BIAS_GELU:
+        z = oracle.gelu(z)
+    elif epi == ffi.EPI_BIAS_RESID:
+        z = C_before[:, :N] + z
+    got = host(Cd)
+    return got[:, :N], z, got[:, N:], C_before[:, N:]
+
+
+LINEAR_CASES = [
+    # dtype, epilogue, M, N, K, lda, ldw, ldc
+    (BF16, ffi.EPI_BIAS, 1000, 2304, 768, 768, 768, 2304),
+    (BF16, ffi.EPI_BIAS_GELU, 777, 460, 768, 768, 768, 3072),
+    (BF16, ffi.EPI_BIAS_RESID, 513, 768, 460, 3072, 3072, 768),
+    (BF16, ffi.EPI_BIAS_RESID, 300, 384, 230, 1536, 1536, 384),
+    (BF16, ffi.EPI_BIAS_F32OUT, 256, 1000, 768, 768, 768, 1000),
+    (BF16, ffi.EPI_BIAS, 33, 192, 64, 192, 192, 576),
+    (BF16, ffi.EPI_BIAS, 1, 8, 8, 8, 8, 8),
+    (FP32, ffi.EPI_BIAS, 68, 192, 64, 64, 64, 192),
+    (FP32, ffi.EPI_BIAS_GELU, 70, 67, 61, 64, 61, 128),
+    (FP32, ffi.EPI_BIAS_RESID, 68, 64, 33, 64, 128, 64),
+    (FP32, ffi.EPI_BIAS_F32OUT, 4, 10, 64, 64, 64, 10),
+]
+
+
+@pytest.mark.parametrize("case", LINEAR_CASES, ids=[f"{c[0]}-{c[1]}-{c[2]}x{c[3]}x{c[4]}" for c in LINEAR_CASES])
+def test_linear(case):
+    dtype, epi, M, N, K, lda, ldw, ldc = case
+    got, ref, tail_after, tail_before = _linear_case(dtype, epi, M, N, K, lda, ldw, ldc)
+    tol = 1e-2 if dtype == BF16 else 1e-5
+    assert rel_err(got, ref) < tol
+    np.testing.assert_array_equal(tail_after, tail_before)  # columns >= N untouched
+
+
+@pytest.mark.parametrize("dtype", [BF16, FP32])
+def test_linear_reads_no_inactive_weights(dtype):
+    """NaN beyond the K prefix (A and W) and beyond the N rows of W never leaks."""
+    got, ref, _, _ = _linear_case(dtype, ffi.EPI_BIAS_RESID, 300, 460, 460, 512, 3072, 768,
+                                  poison=True)
+    assert np.isfinite(got).all()
+    assert rel_err(got, ref) < (1e-2 if dtype == BF16 else 1e-5)
+
+
+def _attention_ref(qkv, B, T, h, hd, scale):
+    out = np.zeros((B * T, h * hd))
+    for b in range(B):
+        for s in range(h):
+            blk = qkv[b * T:(b + 1) * T, s * 3 * hd:(s + 1) * 3 * hd]
+            q, k, v = blk[:, :hd], blk[:, hd:2 * hd], blk[:, 2 * hd:]
+            p = oracle.softmax_rows(q @ k.T * scale)
+            out[b * T:(b + 1) * T, s * hd:(s + 1) * hd] = p @ v
+    return out
+
+
+@pytest.mark.parametrize("dtype,B,T,h,hd,stride", [
+    (BF16, 3, 197, 5, 64, 2304),
+    (BF16, 2, 197, 1, 64, 576),
+    (BF16, 2, 17, 2, 64, 384),
+    (BF16, 1, 240, 3, 64, 576),
+    (BF16, 2, 1, 2, 64, 384),
+    (FP32, 4, 17, 2, 32, 192),
+    (FP32, 2, 197, 3, 64, 576),
+])
+def test_attention(dtype, B, T, h, hd, stride):
+    rng = np.random.default_rng(T + h)
+    qkv = (rng.standard_normal((B * T, stride)) * 1.5).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == BF16 else torch.float32
+    qd = dev(qkv, tdt)
+    o_stride = stride // 3
+    od = torch.zeros((B * T, o_stride), dtype=tdt, device="cuda")
+    scale = 1.0 / math.sqrt(hd)
+    ffi.op_attention(dtype, qd, stride, od, o_stride, B, T, h, hd, scale)
+    torch.cuda.synchronize()
+    ref = _attention_ref(host(qd), B, T, h, hd, scale)
+    got = host(od)[:, :h * hd]
+    assert rel_err(got, ref) < (2e-2 if dtype == BF16 else 1e-5)
+    assert (host(od)[:, h * hd:] == 0).all()
