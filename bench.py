@@ -1,0 +1,248 @@
+"""Throughput of the elastic-ViT forward on one MI355X, per DN mode.
+
+Workload: ViT-B/16-shaped elastic model, bf16, batch 256, 224x224x3 N(0,1)
+synthetic images, random-init weights, five DN modes (heads, MLP hidden) =
+(12, 3072), (9, 2304), (6, 1536), (3, 768), (2, 460).  A step is one
+set_mode + forward of the whole path over one batch already resident in HBM.
+
+`value` is images/s of the full-width mode (mode 0) over exactly --steps
+timed steps; `per_mode` gives every mode (median step time, p10/p90, MFU);
+`roofline` covers the kernel class with the largest time, timed with HIP
+events on the forward's stream during the timed region; `cpu_baseline` is the
+fp64 oracle on a bounded sample of the same workload on the host cores;
+`latency` is the batch-1 / batch-8 regime with a mode switch before every call.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 4096 FLOP/clk x 2.4 GHz
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_vit_b_b256.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_10018_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def percentile(xs, q):
+    return float(np.percentile(np.asarray(xs), q))
+
+
+def time_steps(torch, vit, mode, xd, logits, steps, stream):
+    """Per-step HIP-event times (ms) and the total over exactly `steps` steps."""
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for i in range(steps):
+        vit.set_mode(mode)
+        vit.forward(xd, logits, stream)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    return per, evs[0].elapsed_time(evs[-1]), wall
+
+
+def cpu_baseline(cfg, table, w_stored, x_stored, budget_s=12.0, max_images=64):
+    """fp64 oracle (mode 0) on consecutive images until the time budget is used."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    p = oracle.extract_dense(w_stored, cfg, table, 0)
+    n, t0 = 0, time.perf_counter()
+    while n < max_images and time.perf_counter() - t0 < budget_s:
+        oracle.vit_forward(p, x_stored[n:n + 2], cfg.head_dim, cfg.ln_eps)
+        n += 2
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "images/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} images of the same ViT-B/16 batch in DN mode 0 (full width), "
+                      f"fp64 numpy, {dt:.1f} s wall"}
+
+
+def latency_regime(torch, ffi, inputs, cfg, w, table, calls=1000, warmup=10):
+    out = {}
+    seq = inputs.mode_sequence(calls + warmup, table.num_modes)
+    for batch in (1, 8):
+        vit = ffi.ElasticViT(cfg, w, table, batch)
+        x = inputs.make_images(cfg, batch)
+        xd = torch.from_numpy(x).to(torch.bfloat16).cuda()
+        logits = torch.empty((batch, cfg.num_classes), device="cuda")
+        stream = torch.cuda.current_stream()
+        lat, sw = [], []
+        torch.cuda.synchronize()
+        for i, k in enumerate(seq):
+            t0 = time.perf_counter()
+            vit.set_mode(int(k))
+            t1 = time.perf_counter()
+            vit.forward(xd, logits, stream)
+            stream.synchronize()
+            t2 = time.perf_counter()
+            if i >= warmup:
+                lat.append((t2 - t0) * 1e3)
+                sw.append((t1 - t0) * 1e9)
+        vit.close()
+        out[f"b{batch}"] = {"p50_ms": percentile(lat, 50), "p99_ms": percentile(lat, 99),
+                            "mean_ms": float(np.mean(lat)), "set_mode_p50_ns": percentile(sw, 50)}
+    out["calls"] = calls
+    out["sequence"] = "seeded uniform over the 5 modes, a switch before every call"
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-latency", action="store_true", help="skip the batch-1/8 latency regime")
+    ap.add_argument("--modes", type=str, default="all",
+                    help="comma-separated DN modes to time (mode 0 is always timed)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the elastic-ViT forward is not sharded across GPUs "
+              "(each GPU would run its own batch share); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_10018_amd import cost, ffi, inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = inputs.CONFIGS["vit_b"]
+    B = cfg.batch
+    w = inputs.make_weights(cfg)
+    table = inputs.make_dn_table(cfg)
+    x = inputs.make_images(cfg, B)
+    vit = ffi.ElasticViT(cfg, w, table, B)
+    log("handle created")
+    xd = torch.from_numpy(x).to(torch.bfloat16).cuda().contiguous()
+    logits = torch.empty((B, cfg.num_classes), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    modes = list(range(table.num_modes)) if args.modes == "all" else \
+        sorted({0} | {int(v) for v in args.modes.split(",")})
+    # Warmup, then find the kernel class with the largest time in mode 0.
+    for k in modes:
+        vit.set_mode(k)
+        for _ in range(max(1, args.warmup)):
+            vit.forward(xd, logits, stream)
+    torch.cuda.synchronize()
+    class_ms = {}
+    for kc in ffi.KERNELS:
+        vit.kernel_timing(kc, 64)
+        vit.set_mode(0)
+        vit.forward(xd, logits, stream)
+        ms, n = vit.kernel_timing_read()
+        class_ms[kc] = ms
+    vit.kernel_timing(None, 0)
+    dominant = max(class_ms, key=class_ms.get)
+    log(f"warmup done; per-class ms in mode 0: {class_ms}")
+
+    per_mode = []
+    main_line = None
+    for k in modes:
+        if k == 0:
+            vit.kernel_timing(dominant, args.steps * 64)
+        per, total_ms, wall = time_steps(torch, vit, k, xd, logits, args.steps, stream)
+        gflop = cost.flops_per_image(cfg, table, k) / 1e9
+        med = statistics.median(per)
+        entry = {"mode": k, "heads": inputs.MODE_CAPS["vit_b"][k][0],
+                 "mlp": inputs.MODE_CAPS["vit_b"][k][1], "gflop_per_image": round(gflop, 4),
+                 "images_per_s": B * 1e3 / (total_ms / args.steps),
+                 "median_ms": med, "p10_ms": percentile(per, 10), "p90_ms": percentile(per, 90),
+                 "images_per_s_median": B * 1e3 / med}
+        entry["mfu"] = entry["images_per_s"] * gflop * 1e9 / (BF16_PEAK_TFLOPS * 1e12)
+        per_mode.append(entry)
+        log(f"mode {k}: {entry['images_per_s']:.0f} images/s, mfu {entry['mfu']:.3f}")
+        if k == 0:
+            dom_ms, dom_n = vit.kernel_timing_read()
+            vit.kernel_timing(None, 0)
+            main_line = (total_ms, wall, dom_ms, dom_n)
+    total_ms, wall, dom_ms, dom_n = main_line
+    base = per_mode[0]
+    for e in per_mode:
+        e["speedup_vs_mode0"] = e["images_per_s"] / base["images_per_s"]
+        e["flop_ratio_vs_mode0"] = e["gflop_per_image"] / base["gflop_per_image"]
+
+    f_all, b_all, n_launch = vit.kernel_work(0, B, dominant)
+    f_launch, b_launch = f_all / n_launch, b_all / n_launch
+    avg_s = dom_ms / dom_n / 1e3
+    if dominant == "ln":
+        roof = {"bound": "hbm", "achieved": b_launch / avg_s / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": f_launch / avg_s / 1e12, "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["kernel"] = dominant
+    roof["avg_launch_us"] = avg_s * 1e6
+    roof["launches_timed"] = dom_n
+    roof["algorithmic_per_launch"] = {"flops": f_launch, "bytes": b_launch}
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        tr = json.load(open(TRAFFIC_FILE))
+        if tr.get("kernel_class") == dominant and tr.get("source_hash") == kernel_source_hash():
+            traffic = tr.get("hbm_bytes_per_launch")
+    roof["traffic"] = traffic
+    roof["class_ms_mode0"] = {k: round(v, 4) for k, v in class_ms.items()}
+
+    result = {
+        "metric": "images/sec per DN mode, ViT-B/16 bf16 batch 256; MFMA util % of peak",
+        "value": B * 1e3 / (total_ms / args.steps),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "wall_s_timed": wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) images, random-init N(0,0.02) weights)",
+        "config": {"workload": "elastic ViT-B/16 forward, DN mode 0 (12 heads, MLP 3072), "
+                               "batch 256, 224x224x3, bf16",
+                   "batch": B, "tokens": cfg.tokens, "dim": cfg.dim, "depth": cfg.depth,
+                   "modes": table.num_modes, "parallelism": "single GPU"},
+        "mfu": base["mfu"],
+        "per_mode": per_mode,
+        "roofline": roof,
+    }
+    if not args.no_latency:
+        result["latency"] = latency_regime(torch, ffi, inputs, cfg, w, table)
+        log("latency regime done")
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(cfg, table, inputs.stored_weights(cfg, w),
+                                              inputs.stored_images(cfg, x))
+    vit.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -252,8 +252,8 @@ typedef enum {
 
 /* C[m][n] = epi(sum_{k<K} A[m*lda + k] * W[n*ldw + k] + bias[n]), m < M,
  * n < N.  Only the first K columns of A / W rows and the first N rows of W
- * are read.  BF16 path: lda, ldw, ldc multiples of 8 and pointers 16-byte
- * aligned. */
+ * are read.  BF16 path: lda and ldw multiples of 8, ldc a multiple of 8
+ * (bf16 out) or 4 (fp32 out), and A, W, C, bias 16-byte aligned. */
 elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A, int64_t lda,
                                  const void* W, int64_t ldw, void* C, int64_t ldc,
                                  const float* bias, int64_t M, int32_t N, int32_t K,

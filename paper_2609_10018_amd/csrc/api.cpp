@@ -431,8 +431,12 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
   const Epi epi = static_cast<Epi>(epilogue);
   hipError_t e;
   if (dtype == ELASTO_BF16) {
-    if (lda % 8 || ldw % 8 || !aligned(A, 16) || !aligned(Wt, 16))
-      return fail(ELASTO_ERR_INVALID_ARG, "bf16 linear needs lda, ldw % 8 == 0 and 16-byte aligned A, W");
+    const int64_t cvec = epilogue == ELASTO_EPI_BIAS_F32OUT ? 4 : 8;
+    if (lda % 8 || ldw % 8 || ldc % cvec || !aligned(A, 16) || !aligned(Wt, 16) || !aligned(C, 16) ||
+        !aligned(bias, 16))
+      return fail(ELASTO_ERR_INVALID_ARG,
+                  "bf16 linear needs lda, ldw % 8 == 0, ldc a multiple of 16 bytes and 16-byte "
+                  "aligned A, W, C, bias");
     e = launch_gemm_bf16(epi, a, static_cast<hipStream_t>(hip_stream));
   } else if (dtype == ELASTO_FP32) {
     e = launch_gemm_f32(epi, a, static_cast<hipStream_t>(hip_stream));

@@ -41,4 +41,21 @@ __device__ __forceinline__ float gelu_erf(float z) {
   return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
 }
 
+// GELU with erf from Abramowitz & Stegun, Handbook of Mathematical Functions,
+// formula 7.1.26: erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^{-x^2},
+// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7 (far below bf16 resolution).
+// With q = erfc(|z|/sqrt2) from that formula, GELU(z) = z (1 - q/2) for z >= 0
+// and z q / 2 for z < 0.
+__device__ __forceinline__ float gelu_as(float z) {
+  const float x = fabsf(z) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  const float q = poly * t * __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
+  const float half_zq = 0.5f * z * q;
+  return z >= 0.0f ? z - half_zq : half_zq;
+}
+
 }  // namespace elasto

@@ -6,14 +6,21 @@
 // active units: a contiguous prefix of the packed weight) or K (output
 // projection and fc2 read a prefix of each packed weight row).
 //
-// Tiling: a 256-thread workgroup (4 waves, 2 x 2) owns a BM x BN output tile
-// and walks K in steps of 64.  Each step's A and W tiles are staged in LDS
-// (double-buffered, one barrier per step) with a 16-byte-chunk XOR swizzle so
-// that the MFMA operand reads of 8 consecutive rows hit distinct banks.  Each
-// wave computes a (BM/2) x (BN/2) block with v_mfma_f32_32x32x16_bf16
-// (fp32 accumulate).  Ragged edges: rows past M / N re-read the last valid
-// row (results discarded), K past the end is zero-filled element-wise in both
-// operands, so inactive weights are never read into a product.
+// Tiling: a workgroup owns a BM x BN output tile and walks K in steps of 64.
+// Each step's A and W tiles land in LDS through direct global->LDS loads
+// (global_load_lds_dwordx4: no staging registers), double-buffered, so the
+// loads of step k+1 fly while step k is multiplied; one barrier per step.
+// A 1-KB LDS block holds 8 rows x 128 B; the 16-byte chunks of a row are
+// XOR-swizzled (chunk c of row r sits at c ^ ((r ^ r>>3) & 7)) so that the
+// MFMA operand reads of 8 or 16 consecutive rows hit distinct banks.  The
+// direct load writes lane l's 16 bytes at block + 16*l, so each lane fetches
+// the global chunk that the swizzle maps to its slot.  Each wave multiplies a
+// (BM/WM) x (BN/WN) block with v_mfma_f32_32x32x16_bf16 (fp32 accumulate).
+//
+// Ragged edges: rows past M / N re-read the last valid row (their results
+// are discarded); when K is not a multiple of 64, the last K-step goes
+// through registers instead, with every element at or past K zeroed in both
+// operands, so inactive weights never enter a product.
 //
 // Workgroups are renumbered so that each XCD (workgroup i runs on XCD i % 8)
 // receives a contiguous run of row-major tiles: the tiles sharing an A panel
@@ -24,8 +31,12 @@
 namespace elasto {
 namespace {
 
-constexpr int kBK = 64;
-constexpr int kRowBytes = kBK * 2;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
+
+constexpr int kBK = 64;        // K per step
+constexpr int kRowBytes = 128; // one LDS row: 64 bf16
+constexpr int kRowsPerBlock = 8;
 
 struct Params {
   const uint16_t* A;
@@ -43,8 +54,14 @@ struct Params {
   int tiles_n;
 };
 
-__device__ __forceinline__ int lds_off(int r, int c) {
-  return r * kRowBytes + ((c ^ (r & 7)) << 4);
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// and every LDS operation has completed.
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
 }
 
 // Keep elements [kbeg, kend) of the 8-element chunk starting at kbeg.
@@ -53,92 +70,100 @@ __device__ __forceinline__ u32x4 mask_tail(u32x4 v, int kbeg, int kend) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     const int e = kbeg + 2 * w;
-    const uint32_t lo = (e < kend) ? (v[w] & 0xffffu) : 0u;
-    const uint32_t hi = (e + 1 < kend) ? (v[w] & 0xffff0000u) : 0u;
-    o[w] = lo | hi;
+    const uint32_t lo = (e < kend) ? 0x0000ffffu : 0u;
+    const uint32_t hi = (e + 1 < kend) ? 0xffff0000u : 0u;
+    o[w] = v[w] & (lo | hi);
   }
   return o;
 }
 
-template <int BM, int BN, Epi E>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(Params p) {
-  constexpr int WM = 2, WN = 2;
+template <int BM, int BN, int WM, int WN, Epi E>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
+  constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int ACH = BM * 8 / 256, BCH = BN * 8 / 256;
+  constexpr int ABLK = BM / kRowsPerBlock, BBLK = BN / kRowsPerBlock;
+  constexpr int PER_WAVE = (ABLK + BBLK) / NW;
+  static_assert((ABLK + BBLK) % NW == 0, "blocks must split evenly over waves");
   constexpr int STAGE = (BM + BN) * kRowBytes;
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  constexpr int EPI_BYTES = (BM > 128 ? 128 : BM) * (BN + 8) * 4;
+  constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
   const int nblk = gridDim.x, b = blockIdx.x;
-  const int q = nblk >> 3, r = nblk & 7, xcd = b & 7, idx = b >> 3;
-  const int logical = (xcd < r) ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+  const int q = nblk >> 3, r8 = nblk & 7, xcd = b & 7, idx = b >> 3;
+  const int logical = (xcd < r8) ? xcd * (q + 1) + idx : r8 * (q + 1) + (xcd - r8) * q + idx;
   const int tile_m = logical / p.tiles_n, tile_n = logical - tile_m * p.tiles_n;
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
-  const int cc = tid & 7;  // this thread's 16-byte chunk within a 128-byte row
-  const uint16_t* asrc[ACH];
-  bool azero[ACH];
+  // Per block this lane loads: the row start, the logical 16-byte chunk, and
+  // the block's LDS offset within a stage.
+  const uint16_t* src[PER_WAVE];
+  int chunk[PER_WAVE];
+  int ldsoff[PER_WAVE];
+  const int prow = lane >> 3, pc = lane & 7;
 #pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    const int gm = min(m0 + (tid >> 3) + 32 * i, p.M - 1);
-    if constexpr (E == Epi::Patch) {
-      const int bi = gm / p.tokens, t = gm - bi * p.tokens;
-      const int n = t > 0 ? t - 1 : 0, py = n / p.grid, px = n - py * p.grid;
-      azero[i] = (t == 0);
-      asrc[i] = p.img + ((int64_t)bi * p.chans * p.img_size + (int64_t)py * p.patch) * p.img_size +
-                px * p.patch;
+  for (int i = 0; i < PER_WAVE; ++i) {
+    const int blk = wave * PER_WAVE + i;
+    if (blk < ABLK) {
+      const int r = blk * kRowsPerBlock + prow;
+      const int gm = min(m0 + r, p.M - 1);
+      chunk[i] = pc ^ swz(r);
+      ldsoff[i] = blk * 1024;
+      if constexpr (E == Epi::Patch) {
+        const int bi = gm / p.tokens, t = gm - bi * p.tokens;
+        const int n = t > 0 ? t - 1 : 0, py = n / p.grid, px = n - py * p.grid;
+        src[i] = p.img + ((int64_t)bi * p.chans * p.img_size + (int64_t)py * p.patch) * p.img_size +
+                 px * p.patch;
+      } else {
+        src[i] = p.A + (int64_t)gm * p.lda;
+      }
     } else {
-      azero[i] = false;
-      asrc[i] = p.A + (int64_t)gm * p.lda;
+      const int r = (blk - ABLK) * kRowsPerBlock + prow;
+      chunk[i] = pc ^ swz(r);
+      ldsoff[i] = BM * kRowBytes + (blk - ABLK) * 1024;
+      src[i] = p.W + (int64_t)min(n0 + r, p.N - 1) * p.ldw;
     }
   }
-  const uint16_t* bsrc[BCH];
-#pragma unroll
-  for (int j = 0; j < BCH; ++j) {
-    const int gn = min(n0 + (tid >> 3) + 32 * j, p.N - 1);
-    bsrc[j] = p.W + (int64_t)gn * p.ldw;
-  }
-
-  u32x4 ra[ACH], rb[BCH];
-  auto load = [&](int k0) {
-    const int k = k0 + cc * 8;
-    const bool in = k < p.K, tail = k + 8 > p.K;
-    int64_t aoff = k;
+  // Element offset of k-index k within a source row (im2col for patches).
+  auto koff = [&](int i, int k) -> int64_t {
     if constexpr (E == Epi::Patch) {
-      const int pp = p.patch * p.patch;
-      const int c = k / pp, rem = k - c * pp, ii = rem / p.patch, jj = rem - ii * p.patch;
-      aoff = ((int64_t)c * p.img_size + ii) * p.img_size + jj;
-    }
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (in && !azero[i]) {
-        v = *reinterpret_cast<const u32x4*>(asrc[i] + aoff);
-        if (tail) v = mask_tail(v, k, p.K);
+      if (wave * PER_WAVE + i < ABLK) {
+        const int pp = p.patch * p.patch;
+        const int c = k / pp, rem = k - c * pp, ii = rem / p.patch, jj = rem - ii * p.patch;
+        return ((int64_t)c * p.img_size + ii) * p.img_size + jj;
       }
-      ra[i] = v;
     }
-#pragma unroll
-    for (int j = 0; j < BCH; ++j) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (in) {
-        v = *reinterpret_cast<const u32x4*>(bsrc[j] + k);
-        if (tail) v = mask_tail(v, k, p.K);
-      }
-      rb[j] = v;
-    }
+    return k;
   };
-  auto store = [&](char* stage) {
+
+  const int nk_full = p.K / kBK;
+  const int nk = (p.K + kBK - 1) / kBK;
+  auto issue = [&](int stage, int kt) {
+    char* base = smem + stage * STAGE;
+    if (kt < nk_full) {
 #pragma unroll
-    for (int i = 0; i < ACH; ++i)
-      *reinterpret_cast<u32x4*>(stage + lds_off((tid >> 3) + 32 * i, cc)) = ra[i];
-    char* bst = stage + BM * kRowBytes;
+      for (int i = 0; i < PER_WAVE; ++i)
+        __builtin_amdgcn_global_load_lds(
+            (global_void*)(src[i] + koff(i, kt * kBK + chunk[i] * 8)),
+            (lds_void*)(base + ldsoff[i]), 16, 0, 0);
+    } else {
+      // Ragged last step: masked loads through registers.
+      u32x4 v[PER_WAVE];
 #pragma unroll
-    for (int j = 0; j < BCH; ++j)
-      *reinterpret_cast<u32x4*>(bst + lds_off((tid >> 3) + 32 * j, cc)) = rb[j];
+      for (int i = 0; i < PER_WAVE; ++i) {
+        const int k = kt * kBK + chunk[i] * 8;
+        const bool in = k < p.K;
+        v[i] = *reinterpret_cast<const u32x4*>(src[i] + koff(i, in ? k : 0));
+        v[i] = mask_tail(v[i], k, p.K);
+      }
+#pragma unroll
+      for (int i = 0; i < PER_WAVE; ++i)
+        *reinterpret_cast<u32x4*>(base + ldsoff[i] + lane * 16) = v[i];
+    }
   };
 
   f32x16 acc[TM][TN];
@@ -149,99 +174,172 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Params p) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  const int nk = (p.K + kBK - 1) / kBK;
-  load(0);
-  store(smem);
-  __syncthreads();
   const int lr = lane & 31, lg = lane >> 5;
+  issue(0, 0);
   for (int kt = 0; kt < nk; ++kt) {
+    wait_vm_lds<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + 1 < nk) issue((kt + 1) & 1, kt + 1);
     const char* cur = smem + (kt & 1) * STAGE;
-    if (kt + 1 < nk) load((kt + 1) * kBK);
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       const int c = kk * 2 + lg;
       bf16x8 af[TM], bf[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(cur + lds_off(wm * WTM + i * 32 + lr, c));
+      for (int i = 0; i < TM; ++i) {
+        const int r = wm * WTM + i * 32 + lr;
+        af[i] = *reinterpret_cast<const bf16x8*>(cur + r * kRowBytes + ((c ^ swz(r)) << 4));
+      }
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bf[j] = *reinterpret_cast<const bf16x8*>(cur + BM * kRowBytes +
-                                                 lds_off(wn * WTN + j * 32 + lr, c));
+      for (int j = 0; j < TN; ++j) {
+        const int r = wn * WTN + j * 32 + lr;
+        bf[j] = *reinterpret_cast<const bf16x8*>(cur + BM * kRowBytes + r * kRowBytes +
+                                                 ((c ^ swz(r)) << 4));
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store(smem + ((kt + 1) & 1) * STAGE);
-    __syncthreads();
   }
 
-  // D layout of the 32x32 block: element e of lane l is
-  // row 8*(e/4) + 4*(l/32) + e%4, column l%32.
+  // Epilogue.  The fp32 tile goes through LDS (in passes of up to 128 rows)
+  // so that bias, activation, residual and conversion run on 8-column chunks
+  // with 16-byte global loads and stores.  D layout of a 32x32 MFMA block:
+  // element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
+  constexpr int SR = BM > 128 ? 128 : BM;  // rows per pass
+  constexpr int SS = BN + 8;                // staged row stride (floats): the two
+                                            // half-waves land on distinct banks
+  constexpr int CPR = BN / 8;               // 8-column chunks per row
+  constexpr int NT = 64 * NW;
+  float* stg = reinterpret_cast<float*>(smem);
+  wait_vm_lds<0>();
+  __builtin_amdgcn_s_barrier();
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+  for (int pass = 0; pass < BM / SR; ++pass) {
+    if ((wm * WTM) / SR == pass) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * WTN + j * 32 + lr;
-      if (col >= p.N) continue;
-      const float bv = p.bias[col];
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * WTM + i * 32 + 8 * (e >> 2) + 4 * lg + (e & 3);
-        if (row >= p.M) continue;
-        float v = acc[i][j][e];
-        const int64_t o = (int64_t)row * p.ldc + col;
-        if constexpr (E == Epi::Bias) {
-          static_cast<uint16_t*>(p.C)[o] = f32_to_bf16(v + bv);
-        } else if constexpr (E == Epi::BiasGelu) {
-          static_cast<uint16_t*>(p.C)[o] = f32_to_bf16(gelu_erf(v + bv));
-        } else if constexpr (E == Epi::BiasResid) {
-          uint16_t* cp = static_cast<uint16_t*>(p.C);
-          cp[o] = f32_to_bf16(bf16_to_f32(cp[o]) + (v + bv));
-        } else if constexpr (E == Epi::BiasF32) {
-          static_cast<float*>(p.C)[o] = v + bv;
-        } else {  // Patch
-          const int t = row % p.tokens;
-          const float add = (t == 0 ? p.cls[col] : bv) + p.pos[(int64_t)t * p.N + col];
-          static_cast<uint16_t*>(p.C)[o] = f32_to_bf16(v + add);
-        }
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int rl = (wm * WTM) % SR + i * 32 + 8 * (e >> 2) + 4 * lg + (e & 3);
+            stg[rl * SS + wn * WTN + j * 32 + lr] = acc[i][j][e];
+          }
+    }
+    wait_vm_lds<0>();
+    __builtin_amdgcn_s_barrier();
+    for (int c = tid; c < SR * CPR; c += NT) {
+      const int rl = c / CPR, cc = c - rl * CPR;
+      const int row = m0 + pass * SR + rl, col = n0 + cc * 8;
+      if (row >= p.M || col >= p.N) continue;
+      const bool full = col + 8 <= p.N;
+      const f32x4 s0 = *reinterpret_cast<const f32x4*>(stg + rl * SS + cc * 8);
+      const f32x4 s1 = *reinterpret_cast<const f32x4*>(stg + rl * SS + cc * 8 + 4);
+      float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+      float bv[8];
+      if (full) {
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(p.bias + col);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(p.bias + col + 4);
+        bv[0] = b0[0]; bv[1] = b0[1]; bv[2] = b0[2]; bv[3] = b0[3];
+        bv[4] = b1[0]; bv[5] = b1[1]; bv[6] = b1[2]; bv[7] = b1[3];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bv[e] = col + e < p.N ? p.bias[col + e] : 0.0f;
       }
+      const int64_t o = (int64_t)row * p.ldc + col;
+      if constexpr (E == Epi::BiasF32) {
+        float* cp = static_cast<float*>(p.C) + o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += bv[e];
+        if (full) {
+          *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[1], v[2], v[3]};
+          *reinterpret_cast<f32x4*>(cp + 4) = f32x4{v[4], v[5], v[6], v[7]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (col + e < p.N) cp[e] = v[e];
+        }
+        continue;
+      }
+      uint16_t* cp = static_cast<uint16_t*>(p.C) + o;
+      if constexpr (E == Epi::Bias) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += bv[e];
+      } else if constexpr (E == Epi::BiasGelu) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = gelu_as(v[e] + bv[e]);
+      } else if constexpr (E == Epi::BiasResid) {
+        if (full) {
+          const u32x4 x = *reinterpret_cast<const u32x4*>(cp);
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16)) +
+                   (v[e] + bv[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = col + e < p.N ? bf16_to_f32(cp[e]) + (v[e] + bv[e]) : 0.0f;
+        }
+      } else {  // Patch: class rows (t == 0) take cls + pos[0] and drop the product
+        const int t = row % p.tokens;
+        const float* pp = p.pos + (int64_t)t * p.N + col;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (col + e < p.N) v[e] = (t == 0 ? p.cls[col + e] : v[e] + bv[e]) + pp[e];
+      }
+      if (full) {
+        u32x4 w;
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          w[h] = (uint32_t)f32_to_bf16(v[2 * h]) | ((uint32_t)f32_to_bf16(v[2 * h + 1]) << 16);
+        *reinterpret_cast<u32x4*>(cp) = w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (col + e < p.N) cp[e] = f32_to_bf16(v[e]);
+      }
+    }
+    if (pass + 1 < BM / SR) {
+      wait_vm_lds<0>();
+      __builtin_amdgcn_s_barrier();
     }
   }
 }
 
-template <int BM, int BN, Epi E>
+template <int BM, int BN, int WM, int WN, Epi E>
 hipError_t launch_cfg(const Params& p0, hipStream_t s) {
   Params p = p0;
   const int64_t tm = (p.M + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
   p.tiles_n = (int)tn;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, E>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E>), dim3((unsigned)blocks),
+                     dim3(64 * WM * WN), 0, s, p);
   return hipGetLastError();
 }
 
 template <Epi E>
 hipError_t launch_epi(const Params& p, hipStream_t s) {
   // Pick the tile that keeps the chip busiest: estimated time is the number
-  // of rounds of concurrent workgroups times the relative cost of one tile.
-  struct Cfg { int bm, bn, per_cu; double rel; };
-  const Cfg cfgs[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.55}, {128, 128, 2, 0.30}};
+  // of rounds of concurrent workgroups (one per CU) times the relative cost
+  // of one tile.
+  struct Cfg { int bm, bn; double rel; };
+  const Cfg cfgs[3] = {{256, 256, 1.0}, {256, 128, 0.62}, {128, 128, 0.36}};
   const int cus = 256;
   int best = 0;
   double best_t = 1e300;
   for (int i = 0; i < 3; ++i) {
     const int64_t tiles = ((p.M + cfgs[i].bm - 1) / cfgs[i].bm) * ((p.N + cfgs[i].bn - 1) / cfgs[i].bn);
-    const int64_t slots = (int64_t)cus * cfgs[i].per_cu;
-    const double t = (double)((tiles + slots - 1) / slots) * cfgs[i].rel * cfgs[i].per_cu;
+    const double t = (double)((tiles + cus - 1) / cus) * cfgs[i].rel;
     if (t < best_t - 1e-9) { best_t = t; best = i; }
   }
   switch (best) {
-    case 0: return launch_cfg<256, 256, E>(p, s);
-    case 1: return launch_cfg<256, 128, E>(p, s);
-    default: return launch_cfg<128, 128, E>(p, s);
+    case 0: return launch_cfg<256, 256, 2, 4, E>(p, s);
+    case 1: return launch_cfg<256, 128, 2, 2, E>(p, s);
+    default: return launch_cfg<128, 128, 2, 2, E>(p, s);
   }
 }
 
