@@ -47,10 +47,11 @@ typedef enum {
   ELASTO_ERR_BATCH_RANGE = 7    /* batch outside [1, max_batch]                 */
 } elasto_status_t;
 
-/* Arithmetic of the whole path.  BF16: matrices and activations in bf16, MFMA
- * with fp32 accumulation, fp32 LayerNorm / softmax / GELU, fp32 biases and
- * norm parameters.  FP32: fp32 everywhere (vector-ALU FMA, no reduced-
- * precision matrix mode). */
+/* Arithmetic of the whole path.  BF16: matrices and activations in bf16,
+ * MFMA with fp32 accumulation, fp32 LayerNorm / softmax / GELU, fp32 biases
+ * and norm parameters; the class-token rows of the residual stream (the only
+ * rows the logits depend on at the end) are kept in fp32.  FP32: fp32
+ * everywhere (vector-ALU FMA, no reduced-precision matrix mode). */
 typedef enum { ELASTO_FP32 = 0, ELASTO_BF16 = 1 } elasto_dtype_t;
 
 /* Model shape.  tokens T = (img/patch)^2 + 1, head_dim = dim/heads.
@@ -235,29 +236,37 @@ elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, 
 /* ------------------------------------------- single-kernel entry points */
 /* Device-pointer access to the kernels one forward uses, for kernel-level
  * tests.  dtype selects bf16 (MFMA) or fp32 kernels; activations have that
- * dtype, gamma/beta/bias are fp32.  Strides are in elements. */
+ * dtype, gamma/beta and bias are fp32.  Strides are in elements. */
 
 /* out[r] = LayerNorm(x[r]) * g + b over d features, r < rows.  x row r starts
- * at x + r*x_stride; out is contiguous [rows][d]. */
-elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride, void* out,
-                                    int64_t rows, int32_t d, const float* g, const float* b,
-                                    float eps, void* hip_stream);
+ * at x + r*x_stride; out is contiguous [rows][d].  BF16 path only: when x_cls
+ * is non-NULL, rows with r % tokens == 0 (class-token rows) are read as fp32
+ * from x_cls + (r / tokens) * d instead (tokens = 1: every row).  FP32 path:
+ * x_cls must be NULL. */
+elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride,
+                                    const float* x_cls, int32_t tokens, void* out, int64_t rows,
+                                    int32_t d, const float* g, const float* b, float eps,
+                                    void* hip_stream);
 
 typedef enum {
   ELASTO_EPI_BIAS = 0,     /* C = A W^T + bias                      */
-  ELASTO_EPI_BIAS_GELU,    /* C = GELU(A W^T + bias), exact erf     */
+  ELASTO_EPI_BIAS_GELU,    /* C = GELU(A W^T + bias)                */
   ELASTO_EPI_BIAS_RESID,   /* C = C + A W^T + bias (in place)       */
   ELASTO_EPI_BIAS_F32OUT   /* C (fp32) = A W^T + bias               */
 } elasto_epilogue_t;
 
 /* C[m][n] = epi(sum_{k<K} A[m*lda + k] * W[n*ldw + k] + bias[n]), m < M,
  * n < N.  Only the first K columns of A / W rows and the first N rows of W
- * are read.  BF16 path: lda and ldw multiples of 8, ldc a multiple of 8
- * (bf16 out) or 4 (fp32 out), and A, W, C, bias 16-byte aligned. */
+ * are read.  GELU is exact erf GELU (fp32 path: the device erff; bf16 path:
+ * erf to 1.5e-7 absolute).  BF16 path: lda and ldw multiples of 8, ldc a
+ * multiple of 8 (bf16 out) or 4 (fp32 out), A, W, C, bias 16-byte aligned;
+ * with ELASTO_EPI_BIAS_RESID a non-NULL C_cls holds the class-token rows
+ * (m % tokens == 0) of C in fp32, [M / tokens][N], and those rows of C are
+ * neither read nor written.  C_cls must be NULL otherwise. */
 elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A, int64_t lda,
-                                 const void* W, int64_t ldw, void* C, int64_t ldc,
-                                 const float* bias, int64_t M, int32_t N, int32_t K,
-                                 void* hip_stream);
+                                 const void* W, int64_t ldw, void* C, int64_t ldc, float* C_cls,
+                                 int32_t tokens, const float* bias, int64_t M, int32_t N,
+                                 int32_t K, void* hip_stream);
 
 /* Multi-head attention (Eq. 3) over `heads` head slots of `batch` sequences
  * of `tokens` rows.  qkv row (b*tokens + t) holds, for slot s, q at columns

@@ -7,7 +7,7 @@ softmax, adds) is not counted.  ``paper_macs`` is the convention that matches
 the base ViT-B figure of Table 1: linear-layer MACs only (no QK^T / PV).
 
 Bytes are the algorithmic HBM bytes of the memory-bound kernels: a LayerNorm
-reads one bf16 activation row and writes one.
+reads one fp32 residual-stream row and writes one bf16 activation row.
 """
 from __future__ import annotations
 
@@ -47,9 +47,9 @@ def paper_macs(cfg: ModelConfig, table, k: int) -> float:
     return (f["patch"] + f["qkv"] + f["proj"] + f["fc1"] + f["fc2"] + f["head"]) / 2.0
 
 
-def layernorm_bytes_per_image(cfg: ModelConfig, elem_bytes: int = 2) -> float:
-    """One LayerNorm over all tokens: read T*d + write T*d elements."""
-    return 2.0 * cfg.tokens * cfg.dim * elem_bytes
+def layernorm_bytes_per_image(cfg: ModelConfig, out_bytes: int = 2) -> float:
+    """One LayerNorm over all tokens: read T*d fp32 + write T*d activations."""
+    return cfg.tokens * cfg.dim * (4.0 + out_bytes)
 
 
 def active_weight_elems(cfg: ModelConfig, table, k: int) -> int:

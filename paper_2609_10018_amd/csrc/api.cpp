@@ -38,6 +38,7 @@ struct elasto_handle_s {
   uint8_t* ds = nullptr;  // activation scratch
   int64_t wbytes = 0, sbytes = 0;
   void *x = nullptr, *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr, *ucls = nullptr;
+  float* xcls = nullptr;  // fp32 class-token rows of the residual stream (bf16 path)
   // kernel timing
   int timed_class = -1;
   std::vector<hipEvent_t> events;
@@ -113,10 +114,14 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   const int64_t eb = cfg->dtype == ELASTO_BF16 ? 2 : 4;
   const int64_t rows = (int64_t)cfg->max_batch * h->dims.T, D = cfg->dim;
   auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
+  // x is the residual stream and u, o, qkv, g, ucls hold activations, all in
+  // the path's dtype; on the bf16 path the class-token rows of the residual
+  // stream are kept in fp32 in xcls (they alone decide the logits).
   const int64_t sz_x = al(rows * D * eb), sz_qkv = al(rows * 3 * D * eb),
                 sz_g = al(rows * (int64_t)cfg->mlp_hidden * eb),
-                sz_cls = al((int64_t)cfg->max_batch * D * eb);
-  h->sbytes = 3 * sz_x + sz_qkv + sz_g + sz_cls;
+                sz_cls = al((int64_t)cfg->max_batch * D * eb),
+                sz_xcls = al((int64_t)cfg->max_batch * D * 4);
+  h->sbytes = 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls;
   h->wbytes = h->lay.total;
 
   hipError_t e = hipGetDevice(&h->device);
@@ -137,7 +142,8 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   h->o = p; p += sz_x;
   h->qkv = p; p += sz_qkv;
   h->g = p; p += sz_g;
-  h->ucls = p;
+  h->ucls = p; p += sz_cls;
+  h->xcls = reinterpret_cast<float*>(p);
   *out = h;
   clear_error();
   return ELASTO_OK;
@@ -207,8 +213,13 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   const int L = c.depth, D = c.dim, Mh = c.mlp_hidden;
   const int64_t rows = (int64_t)batch * d.T;
   auto gemm = bf ? launch_gemm_bf16 : launch_gemm_f32;
-  auto ln = bf ? launch_layernorm_bf16 : launch_layernorm_f32;
   auto attn = bf ? launch_attention_bf16 : launch_attention_f32;
+  float* xcls = bf ? h->xcls : nullptr;
+  // LayerNorm over all rows of the residual stream.
+  auto ln = [&](const float* g, const float* b) {
+    return bf ? launch_layernorm_bf16(h->x, D, xcls, d.T, h->u, rows, D, g, b, c.ln_eps, s)
+              : launch_layernorm_f32(h->x, D, h->u, rows, D, g, b, c.ln_eps, s);
+  };
   const float scale = 1.0f / sqrtf((float)d.hd);
 
   hipError_t e;
@@ -230,14 +241,13 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     a.tokens = d.T;
     a.cls = F(h, ELASTO_T_CLS);
     a.pos = F(h, ELASTO_T_POS);
+    a.ccls = xcls;
     e = timed(h, ELASTO_K_PATCH, s, [&] { return gemm(Epi::Patch, a, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "patch embedding: %s", hipGetErrorString(e));
   }
   for (int l = 0; l < L; ++l) {
     const int hh = h->n_heads[(size_t)k * L + l], mm = h->n_mlp[(size_t)k * L + l];
-    e = timed(h, ELASTO_K_LN, s, [&] {
-      return ln(h->x, D, h->u, rows, D, F(h, ELASTO_T_LN1_G, l), F(h, ELASTO_T_LN1_B, l), c.ln_eps, s);
-    });
+    e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN1_G, l), F(h, ELASTO_T_LN1_B, l)); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs q;
     q.A = h->u; q.lda = D;
@@ -258,12 +268,12 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     pr.W = W(h, ELASTO_T_WO, l); pr.ldw = D;
     pr.C = h->x; pr.ldc = D;
     pr.bias = F(h, ELASTO_T_BO, l);
+    pr.ccls = xcls;
+    pr.tokens = d.T;
     pr.M = rows; pr.N = D; pr.K = d.hd * hh;
     e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
-    e = timed(h, ELASTO_K_LN, s, [&] {
-      return ln(h->x, D, h->u, rows, D, F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l), c.ln_eps, s);
-    });
+    e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l)); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln2 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f1;
     f1.A = h->u; f1.lda = D;
@@ -278,13 +288,18 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     f2.W = W(h, ELASTO_T_W2, l); f2.ldw = Mh;
     f2.C = h->x; f2.ldc = D;
     f2.bias = F(h, ELASTO_T_B2, l);
+    f2.ccls = xcls;
+    f2.tokens = d.T;
     f2.M = rows; f2.N = D; f2.K = mm;
     e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
   }
+  // Final norm on the class-token rows only.
   e = timed(h, ELASTO_K_LN, s, [&] {
-    return ln(h->x, (int64_t)d.T * D, h->ucls, batch, D, F(h, ELASTO_T_NORM_G), F(h, ELASTO_T_NORM_B),
-              c.ln_eps, s);
+    return bf ? launch_layernorm_bf16(xcls, D, xcls, 1, h->ucls, batch, D, F(h, ELASTO_T_NORM_G),
+                                      F(h, ELASTO_T_NORM_B), c.ln_eps, s)
+              : launch_layernorm_f32(h->x, (int64_t)d.T * D, h->ucls, batch, D,
+                                     F(h, ELASTO_T_NORM_G), F(h, ELASTO_T_NORM_B), c.ln_eps, s);
   });
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "final norm: %s", hipGetErrorString(e));
   GemmArgs hg;
@@ -354,7 +369,7 @@ elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, 
       n = 1;
       break;
     case ELASTO_K_LN:
-      by = (2.0 * c.depth * Mr * D + B * D) * 2.0 * eb;
+      by = 2.0 * c.depth * Mr * D * 2.0 * eb + B * D * (4.0 + eb);
       n = 2 * c.depth + 1;
       break;
     case ELASTO_K_HEAD:
@@ -396,17 +411,22 @@ elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, 
   return ELASTO_OK;
 }
 
-elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride, void* out,
-                                    int64_t rows, int32_t d, const float* g, const float* b,
-                                    float eps, void* hip_stream) {
+elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride,
+                                    const float* x_cls, int32_t tokens, void* out, int64_t rows,
+                                    int32_t d, const float* g, const float* b, float eps,
+                                    void* hip_stream) {
   if (!x || !out || !g || !b) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if (x_cls && (tokens < 1 || dtype != ELASTO_BF16 || !aligned(x_cls, 16)))
+    return fail(ELASTO_ERR_INVALID_ARG, "x_cls needs the bf16 path, tokens >= 1, 16-byte alignment");
   if (rows < 0 || d < 1 || d > 2048 || x_stride < d || !(eps > 0.0f))
     return fail(ELASTO_ERR_INVALID_ARG, "bad layernorm sizes");
   hipError_t e;
   if (dtype == ELASTO_BF16) {
-    if (d % 4 != 0 || x_stride % 4 != 0 || !aligned(x, 8) || !aligned(out, 8) || !aligned(g, 16) || !aligned(b, 16))
+    if (d % 4 != 0 || x_stride % 4 != 0 || !aligned(x, 8) || !aligned(out, 8) || !aligned(g, 16) ||
+        !aligned(b, 16))
       return fail(ELASTO_ERR_INVALID_ARG, "bf16 layernorm needs d, stride % 4 == 0 and aligned pointers");
-    e = launch_layernorm_bf16(x, x_stride, out, rows, d, g, b, eps, static_cast<hipStream_t>(hip_stream));
+    e = launch_layernorm_bf16(x, x_stride, x_cls, tokens, out, rows, d, g, b, eps,
+                              static_cast<hipStream_t>(hip_stream));
   } else if (dtype == ELASTO_FP32) {
     e = launch_layernorm_f32(x, x_stride, out, rows, d, g, b, eps, static_cast<hipStream_t>(hip_stream));
   } else {
@@ -417,10 +437,14 @@ elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stri
 }
 
 elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A, int64_t lda,
-                                 const void* Wt, int64_t ldw, void* C, int64_t ldc,
-                                 const float* bias, int64_t M, int32_t N, int32_t K,
-                                 void* hip_stream) {
+                                 const void* Wt, int64_t ldw, void* C, int64_t ldc, float* C_cls,
+                                 int32_t tokens, const float* bias, int64_t M, int32_t N,
+                                 int32_t K, void* hip_stream) {
   if (!A || !Wt || !C || !bias) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if (C_cls && (epilogue != ELASTO_EPI_BIAS_RESID || dtype != ELASTO_BF16 || tokens < 1 ||
+                !aligned(C_cls, 16) || N % 4 != 0))
+    return fail(ELASTO_ERR_INVALID_ARG,
+                "C_cls needs the bf16 residual epilogue, tokens >= 1, N % 4 == 0, 16-byte alignment");
   if (M < 0 || M >= ((int64_t)1 << 31) || N < 1 || K < 1 || lda < K || ldw < K || ldc < N)
     return fail(ELASTO_ERR_INVALID_ARG, "bad linear sizes");
   if (epilogue < ELASTO_EPI_BIAS || epilogue > ELASTO_EPI_BIAS_F32OUT)
@@ -428,6 +452,8 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
   GemmArgs a;
   a.A = A; a.lda = lda; a.W = Wt; a.ldw = ldw; a.C = C; a.ldc = ldc; a.bias = bias;
   a.M = M; a.N = N; a.K = K;
+  a.ccls = C_cls;
+  a.tokens = tokens;
   const Epi epi = static_cast<Epi>(epilogue);
   hipError_t e;
   if (dtype == ELASTO_BF16) {

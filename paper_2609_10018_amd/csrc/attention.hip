@@ -2,9 +2,10 @@
 // o = softmax(q k^T * scale) v per (sequence, head slot).
 //
 // bf16 path (head_dim 64): one workgroup per (sequence, head slot).  K is
-// staged whole in LDS (rows of 128 B, 16-byte chunks XOR-swizzled) and V is
-// staged transposed (V^T, one row per feature), zero-padded past the last
-// token.  Each wave takes 16-query blocks in turn and computes the score
+// staged whole in LDS by direct global->LDS loads (rows of 128 B, 16-byte
+// chunks XOR-swizzled) and V is staged transposed (V^T, one row per feature);
+// padding keys past the last token repeat that token and are masked (zero
+// probability).  Each wave takes 16-query blocks in turn and computes the score
 // block transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16: lane l then
 // holds the scores of query l%16 against keys 16j + 4*(l/16) + {0..3}.  The
 // softmax of a query is reduced over its 4 lanes with two xor-shuffles and
@@ -22,6 +23,9 @@
 
 namespace elasto {
 namespace {
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
 
 constexpr int kHd = 64;
 constexpr int kNtMax = 16;  // 16-key tiles held in registers: tokens <= 256
@@ -50,32 +54,55 @@ __global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
   const int b = blockIdx.x / p.heads, s = blockIdx.x - b * p.heads;
   const uint16_t* base = p.qkv + (int64_t)b * T * p.qs + (int64_t)s * 3 * kHd;
 
-  for (int i = tid; i < nt * 16 * 8; i += 256) {
-    const int row = i >> 3, c = i & 7;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (row < T) v = *reinterpret_cast<const u32x4*>(base + (int64_t)row * p.qs + kHd + c * 8);
-    *reinterpret_cast<u32x4*>(kl + k_off(row, c)) = v;
-  }
-  for (int i = tid; i < tv * 8; i += 256) {
-    const int key = i >> 3, c = i & 7;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (key < T) v = *reinterpret_cast<const u32x4*>(base + (int64_t)key * p.qs + 2 * kHd + c * 8);
+  const int lq = lane & 15, lg = lane >> 4;
+  // Q fragments of a 16-query block (B operand of S^T = K Q^T); rows past the
+  // last token re-read token T-1 and their outputs are dropped.
+  auto load_q = [&](int qb, bf16x8* qf) {
+    const int q = min(qb * 16 + lq, T - 1);
+    const uint16_t* qp = base + (int64_t)q * p.qs + lg * 8;
+    qf[0] = *reinterpret_cast<const bf16x8*>(qp);
+    qf[1] = *reinterpret_cast<const bf16x8*>(qp + 32);
+  };
+  bf16x8 qf[2];
+  if (wave < nt) load_q(wave, qf);
+
+  // K: direct global->LDS loads in 1-KB blocks of 8 rows.  Lane l lands at
+  // block + 16 l, i.e. row 8*blk + l/8, physical chunk l%8, so it fetches the
+  // logical chunk that k_off() places there.  Rows past the last token re-read
+  // token T-1: their scores are masked out of the softmax.
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      vt[(c * 8 + e) * vs + key] = (uint16_t)((e & 1) ? (v[e >> 1] >> 16) : (v[e >> 1] & 0xffffu));
+  for (int i = 0; i < (2 * kNtMax + 3) / 4; ++i) {
+    const int blk = wave + 4 * i;
+    if (blk < 2 * nt) {
+      const int r = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ (r & 7);
+      const uint16_t* src = base + (int64_t)min(r, T - 1) * p.qs + kHd + c * 8;
+      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)(kl + blk * 1024), 16, 0, 0);
+    }
+  }
+  // V: every 16-byte chunk load is issued before any transposed LDS write.
+  // Keys past the last token re-read token T-1: their probabilities are 0.
+  constexpr int kVLoads = (kNtMax * 16) * 8 / 256;
+  u32x4 vv[kVLoads];
+#pragma unroll
+  for (int i = 0; i < kVLoads; ++i) {
+    const int idx = tid + 256 * i, key = idx >> 3, c = idx & 7;
+    vv[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)min(key, T - 1) * p.qs + 2 * kHd + c * 8);
+  }
+#pragma unroll
+  for (int i = 0; i < kVLoads; ++i) {
+    const int idx = tid + 256 * i, key = idx >> 3, c = idx & 7;
+    if (key < tv) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        vt[(c * 8 + e) * vs + key] =
+            (uint16_t)((e & 1) ? (vv[i][e >> 1] >> 16) : (vv[i][e >> 1] & 0xffffu));
+    }
   }
   __syncthreads();
 
-  const int lq = lane & 15, lg = lane >> 4;
   for (int qb = wave; qb < nt; qb += 4) {
     const int q0 = qb * 16;
-    bf16x8 qf[2];
-    {
-      const int q = min(q0 + lq, T - 1);
-      const uint16_t* qp = base + (int64_t)q * p.qs + lg * 8;
-      qf[0] = *reinterpret_cast<const bf16x8*>(qp);
-      qf[1] = *reinterpret_cast<const bf16x8*>(qp + 32);
-    }
     f32x4 st[kNtMax];
 #pragma unroll
     for (int j = 0; j < kNtMax; ++j) {
@@ -89,6 +116,8 @@ __global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
       }
       st[j] = acc;
     }
+    bf16x8 qn[2];
+    if (qb + 4 < nt) load_q(qb + 4, qn);
     float mx = -INFINITY;
 #pragma unroll
     for (int j = 0; j < kNtMax; ++j)
@@ -144,6 +173,8 @@ __global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
         for (int n = 0; n < 4; ++n) op[n * 16] = f32_to_bf16(o[n][r] * ir);
       }
     }
+    qf[0] = qn[0];
+    qf[1] = qn[1];
   }
 }
 

@@ -51,6 +51,7 @@ struct Params {
   int img_size, patch, chans, grid, tokens;
   const float* cls;
   const float* pos;
+  float* ccls;
   int tiles_n;
 };
 
@@ -62,6 +63,18 @@ template <int N>
 __device__ __forceinline__ void wait_vm_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+}
+
+// Store 8 floats (the first `valid` of them when the chunk is ragged).
+__device__ __forceinline__ void store_f32x8(float* cp, const float* v, bool full, int valid) {
+  if (full) {
+    *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4*>(cp + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (e < valid) cp[e] = v[e];
+  }
 }
 
 // Keep elements [kbeg, kend) of the 8-element chunk starting at kbeg.
@@ -254,15 +267,17 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         float* cp = static_cast<float*>(p.C) + o;
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] += bv[e];
-        if (full) {
-          *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[1], v[2], v[3]};
-          *reinterpret_cast<f32x4*>(cp + 4) = f32x4{v[4], v[5], v[6], v[7]};
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (col + e < p.N) cp[e] = v[e];
-        }
+        store_f32x8(cp, v, full, p.N - col);
         continue;
+      }
+      // Residual stream: bf16 rows, except the class-token rows (row % tokens
+      // == 0), which live in fp32 in ccls when it is given.
+      float* cls_row = nullptr;
+      if constexpr (E == Epi::BiasResid || E == Epi::Patch) {
+        if (p.ccls != nullptr) {
+          const int bi = row / p.tokens;
+          if (row == bi * p.tokens) cls_row = p.ccls + (int64_t)bi * p.N + col;
+        }
       }
       uint16_t* cp = static_cast<uint16_t*>(p.C) + o;
       if constexpr (E == Epi::Bias) {
@@ -272,6 +287,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = gelu_as(v[e] + bv[e]);
       } else if constexpr (E == Epi::BiasResid) {
+        if (cls_row != nullptr) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = col + e < p.N ? cls_row[e] + (v[e] + bv[e]) : 0.0f;
+          store_f32x8(cls_row, v, full, p.N - col);
+          continue;
+        }
         if (full) {
           const u32x4 x = *reinterpret_cast<const u32x4*>(cp);
 #pragma unroll
@@ -289,6 +311,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (col + e < p.N) v[e] = (t == 0 ? p.cls[col + e] : v[e] + bv[e]) + pp[e];
+        if (cls_row != nullptr) {
+          store_f32x8(cls_row, v, full, p.N - col);
+          continue;
+        }
       }
       if (full) {
         u32x4 w;
@@ -347,6 +373,7 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if ((a.ccls != nullptr || epi == Epi::Patch) && a.tokens < 1) return hipErrorInvalidValue;
   Params p{};
   p.A = static_cast<const uint16_t*>(a.A);
   p.lda = a.lda;
@@ -366,6 +393,7 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.tokens = a.tokens;
   p.cls = a.cls;
   p.pos = a.pos;
+  p.ccls = a.ccls;
   switch (epi) {
     case Epi::Bias: return launch_epi<Epi::Bias>(p, s);
     case Epi::BiasGelu: return launch_epi<Epi::BiasGelu>(p, s);

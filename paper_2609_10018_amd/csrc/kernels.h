@@ -6,10 +6,14 @@
 
 namespace elasto {
 
+// Output element types: Bias, BiasGelu, BiasResid and Patch write the path's
+// activation type; BiasF32 writes fp32.  On the bf16 path the residual stream
+// (BiasResid, Patch) keeps its class-token rows (row % tokens == 0) in fp32
+// in `ccls` ([rows / tokens][N]) when that pointer is given.
 enum class Epi : int {
   Bias = 0,      // C = acc + bias
   BiasGelu = 1,  // C = GELU(acc + bias)
-  BiasResid = 2, // C = C + acc + bias
+  BiasResid = 2, // C = C + acc + bias (in place)
   BiasF32 = 3,   // C (fp32) = acc + bias
   Patch = 4,     // patch embedding: A rows are image patches (row t == 0 of
                  // each sequence is the class row), C = acc + (cls|bias) + pos
@@ -32,14 +36,18 @@ struct GemmArgs {
   int img_size = 0, patch = 0, chans = 0, grid = 0, tokens = 0;
   const float* cls = nullptr;
   const float* pos = nullptr;
+  float* ccls = nullptr;
 };
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_f32(Epi epi, const GemmArgs& a, hipStream_t s);
 
 // out[r] = LN(x[r]) over d features; x row stride x_stride, out contiguous.
-hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, void* out, int64_t rows, int d,
-                                 const float* g, const float* b, float eps, hipStream_t s);
+// bf16 variant: x is bf16, except that rows with r % tokens == 0 read fp32
+// xcls + (r / tokens) * d when xcls is given (the class-token rows).
+hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, const float* xcls, int tokens,
+                                 void* out, int64_t rows, int d, const float* g, const float* b,
+                                 float eps, hipStream_t s);
 hipError_t launch_layernorm_f32(const void* x, int64_t x_stride, void* out, int64_t rows, int d,
                                 const float* g, const float* b, float eps, hipStream_t s);
 

@@ -3,9 +3,10 @@
 // lane holding its share of the row in registers (two passes over registers,
 // one read of the row from HBM, one write).
 //
-// bf16 rows are read and written as 8-byte (4-element) vectors, so a wave
-// moves 512 contiguous bytes per instruction.  Row stride is free, which lets
-// the final norm read only the class-token rows of the residual stream.
+// The bf16 path reads and writes 8-byte (4-element) bf16 vectors, so a wave
+// moves 512 contiguous bytes per instruction; the class-token rows of the
+// residual stream are fp32 and come from their own buffer.  Row stride is
+// free.
 #include "common.h"
 #include "kernels.h"
 
@@ -16,6 +17,8 @@ constexpr int kMaxVecPerLane = 8;  // 4-element vectors per lane: d <= 2048
 
 __global__ __launch_bounds__(256) void layernorm_bf16_kernel(const uint16_t* __restrict__ x,
                                                              int64_t x_stride,
+                                                             const float* __restrict__ xcls,
+                                                             int tokens,
                                                              uint16_t* __restrict__ out,
                                                              int64_t rows, int d,
                                                              const float* __restrict__ g,
@@ -25,18 +28,29 @@ __global__ __launch_bounds__(256) void layernorm_bf16_kernel(const uint16_t* __r
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const int nvec = d >> 2;
+  const int64_t bi = xcls != nullptr ? row / tokens : 0;
+  const bool cls_row = xcls != nullptr && row == bi * tokens;  // uniform per wave
   const uint16_t* xr = x + row * x_stride;
+  const float* xc = cls_row ? xcls + bi * (int64_t)d : nullptr;
   float v[kMaxVecPerLane][4];
   float s = 0.0f;
 #pragma unroll
   for (int i = 0; i < kMaxVecPerLane; ++i) {
     const int vi = lane + 64 * i;
     if (vi < nvec) {
-      const u32x2 w = *reinterpret_cast<const u32x2*>(xr + 4 * vi);
-      v[i][0] = __uint_as_float(w[0] << 16);
-      v[i][1] = __uint_as_float(w[0] & 0xffff0000u);
-      v[i][2] = __uint_as_float(w[1] << 16);
-      v[i][3] = __uint_as_float(w[1] & 0xffff0000u);
+      if (cls_row) {
+        const f32x4 w = *reinterpret_cast<const f32x4*>(xc + 4 * vi);
+        v[i][0] = w[0];
+        v[i][1] = w[1];
+        v[i][2] = w[2];
+        v[i][3] = w[3];
+      } else {
+        const u32x2 w = *reinterpret_cast<const u32x2*>(xr + 4 * vi);
+        v[i][0] = __uint_as_float(w[0] << 16);
+        v[i][1] = __uint_as_float(w[0] & 0xffff0000u);
+        v[i][2] = __uint_as_float(w[1] << 16);
+        v[i][3] = __uint_as_float(w[1] & 0xffff0000u);
+      }
       s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
     } else {
       v[i][0] = v[i][1] = v[i][2] = v[i][3] = 0.0f;
@@ -112,13 +126,15 @@ __global__ __launch_bounds__(256) void layernorm_f32_kernel(const float* __restr
 
 }  // namespace
 
-hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, void* out, int64_t rows, int d,
-                                 const float* g, const float* b, float eps, hipStream_t s) {
+hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, const float* xcls, int tokens,
+                                 void* out, int64_t rows, int d, const float* g, const float* b,
+                                 float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  if (xcls != nullptr && tokens < 1) return hipErrorInvalidValue;
   const int64_t blocks = (rows + 3) / 4;
   hipLaunchKernelGGL(layernorm_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(x), x_stride, static_cast<uint16_t*>(out),
-                     rows, d, g, b, eps);
+                     static_cast<const uint16_t*>(x), x_stride, xcls, tokens,
+                     static_cast<uint16_t*>(out), rows, d, g, b, eps);
   return hipGetLastError();
 }
 

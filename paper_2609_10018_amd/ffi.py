@@ -85,9 +85,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "elasto_kernel_timing": [c_vp, c_i32, c_i32],
         "elasto_kernel_timing_read": [c_vp, P(c_f64), P(c_i64)],
         "elasto_kernel_work": [c_vp, c_i32, c_i32, c_i32, P(c_f64), P(c_f64), P(c_i32)],
-        "elasto_op_layernorm": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_vp, c_f32, c_vp],
-        "elasto_op_linear": [c_i32, c_i32, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
-                             c_i32, c_i32, c_vp],
+        "elasto_op_layernorm": [c_i32, c_vp, c_i64, c_vp, c_i32, c_vp, c_i64, c_i32, c_vp, c_vp,
+                                c_f32, c_vp],
+        "elasto_op_linear": [c_i32, c_i32, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i32,
+                             c_vp, c_i64, c_i32, c_i32, c_vp],
         "elasto_op_attention": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32,
                                 c_f32, c_vp],
     }
@@ -236,18 +237,22 @@ class ElasticViT:
         return f.value, b.value, n.value
 
 
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
 def op_layernorm(dtype: int, x, x_stride: int, out, rows: int, d: int, g, b, eps: float,
-                 stream=None) -> None:
-    check(load_library().elasto_op_layernorm(dtype, x.data_ptr(), x_stride, out.data_ptr(), rows,
-                                             d, g.data_ptr(), b.data_ptr(), eps,
-                                             _stream_ptr(stream)))
+                 x_cls=None, tokens: int = 1, stream=None) -> None:
+    check(load_library().elasto_op_layernorm(dtype, x.data_ptr(), x_stride, _ptr(x_cls), tokens,
+                                             out.data_ptr(), rows, d, g.data_ptr(), b.data_ptr(),
+                                             eps, _stream_ptr(stream)))
 
 
 def op_linear(dtype: int, epilogue: int, A, lda: int, W, ldw: int, C, ldc: int, bias,
-              M: int, N: int, K: int, stream=None) -> None:
+              M: int, N: int, K: int, C_cls=None, tokens: int = 1, stream=None) -> None:
     check(load_library().elasto_op_linear(dtype, epilogue, A.data_ptr(), lda, W.data_ptr(), ldw,
-                                          C.data_ptr(), ldc, bias.data_ptr(), M, N, K,
-                                          _stream_ptr(stream)))
+                                          C.data_ptr(), ldc, _ptr(C_cls), tokens, bias.data_ptr(),
+                                          M, N, K, _stream_ptr(stream)))
 
 
 def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int, tokens: int,

@@ -36,7 +36,7 @@ def test_layernorm(dtype, rows, d):
     b = (0.1 * rng.standard_normal(d)).astype(np.float32)
     tdt = torch.bfloat16 if dtype == BF16 else torch.float32
     xd = dev(x, tdt)
-    out = torch.empty_like(xd)
+    out = torch.empty((rows, d), dtype=tdt, device="cuda")
     gd, bd = dev(g, torch.float32), dev(b, torch.float32)
     ffi.op_layernorm(dtype, xd, d, out, rows, d, gd, bd, 1e-6)
     torch.cuda.synchronize()
@@ -59,7 +59,27 @@ def test_layernorm_strided_rows():
     assert rel_err(host(out), ref) < 8e-3
 
 
-def _linear_case(dtype, epi, M, N, K, lda, ldw, ldc, poison=False, seed=0):
+@pytest.mark.parametrize("tokens", [197, 1])
+def test_layernorm_fp32_class_rows(tokens):
+    """bf16 rows, with every tokens-th row read as fp32 from the class-row buffer."""
+    rng = np.random.default_rng(2)
+    B, d = 5, 768
+    rows = B * tokens
+    x = rng.standard_normal((rows, d)).astype(np.float32)
+    xc = (rng.standard_normal((B, d)) * 1e-3 + 0.25).astype(np.float32)  # needs fp32 precision
+    xd, xcd = dev(x, torch.bfloat16), dev(xc, torch.float32)
+    g = dev(1 + 0.1 * rng.standard_normal(d), torch.float32)
+    b = dev(0.1 * rng.standard_normal(d), torch.float32)
+    out = torch.empty((rows, d), dtype=torch.bfloat16, device="cuda")
+    ffi.op_layernorm(BF16, xd, d, out, rows, d, g, b, 1e-6, x_cls=xcd, tokens=tokens)
+    torch.cuda.synchronize()
+    xin = host(xd)
+    xin[::tokens] = xc.astype(np.float64)
+    ref = oracle.layer_norm(xin, host(g), host(b), 1e-6)
+    assert rel_err(host(out), ref) < 8e-3
+
+
+def _linear_case(dtype, epi, M, N, K, lda, ldw, ldc, poison=False, seed=0, tokens=0):
     rng = np.random.default_rng(seed)
     tdt = torch.bfloat16 if dtype == BF16 else torch.float32
     A = rng.standard_normal((M, lda)).astype(np.float32)
@@ -71,18 +91,28 @@ def _linear_case(dtype, epi, M, N, K, lda, ldw, ldc, poison=False, seed=0):
     bias = (0.1 * rng.standard_normal(N)).astype(np.float32)
     C0 = rng.standard_normal((M, ldc)).astype(np.float32)
     Ad, Wd = dev(A, tdt), dev(W, tdt)
-    out_f32 = epi == ffi.EPI_BIAS_F32OUT
-    Cd = dev(C0, torch.float32 if out_f32 else tdt)
+    Cd = dev(C0, torch.float32 if epi == ffi.EPI_BIAS_F32OUT else tdt)
     C_before = host(Cd)
-    ffi.op_linear(dtype, epi, Ad, lda, Wd, ldw, Cd, ldc, dev(bias, torch.float32), M, N, K)
+    ccls = None
+    if tokens:
+        ccls = dev(rng.standard_normal((M // tokens, N)) * 1e-3 + 0.5, torch.float32)
+        ccls_before = host(ccls)
+    ffi.op_linear(dtype, epi, Ad, lda, Wd, ldw, Cd, ldc, dev(bias, torch.float32), M, N, K,
+                  C_cls=ccls, tokens=max(tokens, 1))
     torch.cuda.synchronize()
     a64, w64 = host(Ad)[:, :K], host(Wd)[:N, :K]
     z = a64 @ w64.T + bias.astype(np.float64)
     if epi == ffi.EPI_BIAS_GELU:
         z = oracle.gelu(z)
     elif epi == ffi.EPI_BIAS_RESID:
-        z = C_before[:, :N] + z
+        base = C_before[:, :N].copy()
+        if tokens:
+            base[::tokens] = ccls_before
+        z = base + z
     got = host(Cd)
+    if tokens:
+        np.testing.assert_array_equal(got[::tokens], C_before[::tokens])  # class rows untouched in C
+        got[::tokens, :N] = host(ccls)
     return got[:, :N], z, got[:, N:], C_before[:, N:]
 
 
@@ -109,6 +139,16 @@ def test_linear(case):
     tol = 1e-2 if dtype == BF16 else 1e-5
     assert rel_err(got, ref) < tol
     np.testing.assert_array_equal(tail_after, tail_before)  # columns >= N untouched
+
+
+def test_linear_residual_fp32_class_rows():
+    """The bf16 residual epilogue keeps class-token rows in the fp32 side buffer."""
+    got, ref, tail_after, tail_before = _linear_case(BF16, ffi.EPI_BIAS_RESID, 4 * 197, 768, 460,
+                                                     3072, 3072, 768, tokens=197)
+    assert rel_err(got, ref) < 1e-2
+    cls_err = np.abs(got[::197] - ref[::197]).max() / np.abs(ref[::197]).max()
+    assert cls_err < 1e-5      # fp32 rows: no bf16 rounding of the class rows
+    np.testing.assert_array_equal(tail_after, tail_before)
 
 
 @pytest.mark.parametrize("dtype", [BF16, FP32])
