@@ -28,7 +28,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
 
 constexpr int kHd = 64;
-constexpr int kNtMax = 16;  // 16-key tiles held in registers: tokens <= 256
+constexpr int kNtMax = 15;  // 16-key tiles: tokens <= 240
 
 __device__ __forceinline__ int k_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
@@ -41,14 +41,16 @@ struct AttnP {
   float scale_log2;
 };
 
-__global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
+// NT = ceil(T / 16) key tiles, fixed at compile time so that every loop over
+// keys is fully unrolled and only the last tile carries the key < T mask.
+template <int NT>
+__global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
+  constexpr int TV = NT * 16;  // keys staged in V^T
+  constexpr int VS = TV + 4;   // V^T row stride (elements): rows land on distinct banks
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int T = p.T;
-  const int nt = (T + 15) >> 4;           // 16-key tiles
-  const int tv = ((T + 31) >> 5) << 5;    // keys covered by 32-key PV blocks
-  const int vs = tv + 4;                  // V^T row stride (elements), breaks bank aliasing
   char* kl = smem;
-  uint16_t* vt = reinterpret_cast<uint16_t*>(smem + nt * 16 * 128);
+  uint16_t* vt = reinterpret_cast<uint16_t*>(smem + NT * 16 * 128);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x / p.heads, s = blockIdx.x - b * p.heads;
@@ -64,16 +66,16 @@ __global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
     qf[1] = *reinterpret_cast<const bf16x8*>(qp + 32);
   };
   bf16x8 qf[2];
-  if (wave < nt) load_q(wave, qf);
+  if (wave < NT) load_q(wave, qf);
 
   // K: direct global->LDS loads in 1-KB blocks of 8 rows.  Lane l lands at
   // block + 16 l, i.e. row 8*blk + l/8, physical chunk l%8, so it fetches the
   // logical chunk that k_off() places there.  Rows past the last token re-read
   // token T-1: their scores are masked out of the softmax.
 #pragma unroll
-  for (int i = 0; i < (2 * kNtMax + 3) / 4; ++i) {
+  for (int i = 0; i < (2 * NT + 3) / 4; ++i) {
     const int blk = wave + 4 * i;
-    if (blk < 2 * nt) {
+    if (blk < 2 * NT) {
       const int r = blk * 8 + (lane >> 3);
       const int c = (lane & 7) ^ (r & 7);
       const uint16_t* src = base + (int64_t)min(r, T - 1) * p.qs + kHd + c * 8;
@@ -82,84 +84,95 @@ __global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
   }
   // V: every 16-byte chunk load is issued before any transposed LDS write.
   // Keys past the last token re-read token T-1: their probabilities are 0.
-  constexpr int kVLoads = (kNtMax * 16) * 8 / 256;
+  constexpr int kVLoads = (TV * 8 + 255) / 256;
   u32x4 vv[kVLoads];
 #pragma unroll
   for (int i = 0; i < kVLoads; ++i) {
-    const int idx = tid + 256 * i, key = idx >> 3, c = idx & 7;
-    vv[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)min(key, T - 1) * p.qs + 2 * kHd + c * 8);
+    const int idx = tid + 256 * i, key = min(idx >> 3, T - 1), c = idx & 7;
+    vv[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)key * p.qs + 2 * kHd + c * 8);
   }
 #pragma unroll
   for (int i = 0; i < kVLoads; ++i) {
     const int idx = tid + 256 * i, key = idx >> 3, c = idx & 7;
-    if (key < tv) {
+    if (key < TV) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        vt[(c * 8 + e) * vs + key] =
+        vt[(c * 8 + e) * VS + key] =
             (uint16_t)((e & 1) ? (vv[i][e >> 1] >> 16) : (vv[i][e >> 1] & 0xffffu));
     }
   }
   __syncthreads();
 
-  for (int qb = wave; qb < nt; qb += 4) {
+  const float c2 = p.scale_log2;
+  for (int qb = wave; qb < NT; qb += 4) {
     const int q0 = qb * 16;
-    f32x4 st[kNtMax];
+    f32x4 st[NT];
 #pragma unroll
-    for (int j = 0; j < kNtMax; ++j) {
+    for (int j = 0; j < NT; ++j) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      if (j < nt) {
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + k_off(j * 16 + lq, kk * 4 + lg));
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], acc, 0, 0, 0);
-        }
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + k_off(j * 16 + lq, kk * 4 + lg));
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], acc, 0, 0, 0);
       }
       st[j] = acc;
+      // Bound how far the scheduler hoists LDS reads (register pressure).
+      if ((j & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_sched_barrier(0);
     bf16x8 qn[2];
-    if (qb + 4 < nt) load_q(qb + 4, qn);
+    if (qb + 4 < NT) load_q(qb + 4, qn);
+    // Keys of the last tile at or past T do not exist.
+    bool valid[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) valid[r] = (NT - 1) * 16 + 4 * lg + r < T;
     float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < kNtMax; ++j)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        if (j * 16 + 4 * lg + r < T) mx = fmaxf(mx, st[j][r]);
+        mx = fmaxf(mx, (j < NT - 1 || valid[r]) ? st[j][r] : -INFINITY);
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float off = -mx * c2;
     float sum = 0.f;
 #pragma unroll
-    for (int j = 0; j < kNtMax; ++j)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float e = (j * 16 + 4 * lg + r < T) ? exp2f((st[j][r] - mx) * p.scale_log2) : 0.f;
+        float e = __builtin_amdgcn_exp2f(fmaf(st[j][r], c2, off));
+        if (j == NT - 1) e = valid[r] ? e : 0.f;
         st[j][r] = e;
         sum += e;
       }
     sum += __shfl_xor(sum, 16, 64);
     sum += __shfl_xor(sum, 32, 64);
+    __builtin_amdgcn_sched_barrier(0);
 
     f32x4 o[4];
 #pragma unroll
     for (int n = 0; n < 4; ++n) o[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < kNtMax / 2; ++kb) {
-      if (2 * kb < nt) {
-        bf16x8 pa;
+    for (int kb = 0; kb < (NT + 1) / 2; ++kb) {
+      const bool has_hi = 2 * kb + 1 < NT;
+      bf16x8 pa;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pa[r] = static_cast<__bf16>(st[2 * kb][r]);
-          pa[4 + r] = static_cast<__bf16>(st[2 * kb + 1][r]);
-        }
-#pragma unroll
-        for (int n = 0; n < 4; ++n) {
-          const uint16_t* vp = vt + (n * 16 + lq) * vs + kb * 32 + 4 * lg;
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vp + 16);
-          const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-          o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8, w), o[n],
-                                                         0, 0, 0);
-        }
+      for (int r = 0; r < 4; ++r) {
+        pa[r] = static_cast<__bf16>(st[2 * kb][r]);
+        pa[4 + r] = has_hi ? static_cast<__bf16>(st[has_hi ? 2 * kb + 1 : 2 * kb][r])
+                           : static_cast<__bf16>(0.f);
       }
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        const uint16_t* vp = vt + (n * 16 + lq) * VS + kb * 32 + 4 * lg;
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
+        u32x2 hi = {0u, 0u};
+        if (has_hi) hi = *reinterpret_cast<const u32x2*>(vp + 16);
+        const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+        o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8, w), o[n],
+                                                       0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     const float inv = 1.0f / sum;  // for query lq
 #pragma unroll
@@ -176,6 +189,14 @@ __global__ __launch_bounds__(256) void attention_bf16_kernel(AttnP p) {
     qf[0] = qn[0];
     qf[1] = qn[1];
   }
+}
+
+template <int NT>
+hipError_t launch_attn_nt(const AttnP& p, int batch, int heads, hipStream_t s) {
+  const size_t lds = (size_t)NT * 16 * 128 + (size_t)kHd * (NT * 16 + 4) * 2;
+  hipLaunchKernelGGL(attention_bf16_kernel<NT>, dim3((unsigned)(batch * heads)), dim3(256), lds, s,
+                     p);
+  return hipGetLastError();
 }
 
 struct AttnF {
@@ -235,11 +256,24 @@ hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   p.T = a.tokens;
   p.heads = a.heads;
   p.scale_log2 = a.scale * 1.4426950408889634f;
-  const int nt = (a.tokens + 15) / 16, tv = (a.tokens + 31) / 32 * 32;
-  const size_t lds = (size_t)nt * 16 * 128 + (size_t)kHd * (tv + 4) * 2;
-  hipLaunchKernelGGL(attention_bf16_kernel, dim3((unsigned)(a.batch * a.heads)), dim3(256), lds, s,
-                     p);
-  return hipGetLastError();
+  switch ((a.tokens + 15) / 16) {
+    case 1: return launch_attn_nt<1>(p, a.batch, a.heads, s);
+    case 2: return launch_attn_nt<2>(p, a.batch, a.heads, s);
+    case 3: return launch_attn_nt<3>(p, a.batch, a.heads, s);
+    case 4: return launch_attn_nt<4>(p, a.batch, a.heads, s);
+    case 5: return launch_attn_nt<5>(p, a.batch, a.heads, s);
+    case 6: return launch_attn_nt<6>(p, a.batch, a.heads, s);
+    case 7: return launch_attn_nt<7>(p, a.batch, a.heads, s);
+    case 8: return launch_attn_nt<8>(p, a.batch, a.heads, s);
+    case 9: return launch_attn_nt<9>(p, a.batch, a.heads, s);
+    case 10: return launch_attn_nt<10>(p, a.batch, a.heads, s);
+    case 11: return launch_attn_nt<11>(p, a.batch, a.heads, s);
+    case 12: return launch_attn_nt<12>(p, a.batch, a.heads, s);
+    case 13: return launch_attn_nt<13>(p, a.batch, a.heads, s);
+    case 14: return launch_attn_nt<14>(p, a.batch, a.heads, s);
+    case 15: return launch_attn_nt<15>(p, a.batch, a.heads, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
