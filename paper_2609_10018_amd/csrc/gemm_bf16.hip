@@ -23,8 +23,8 @@
 // operands, so inactive weights never enter a product.
 //
 // Workgroups are renumbered so that each XCD (workgroup i runs on XCD i % 8)
-// receives a contiguous run of row-major tiles: the tiles sharing an A panel
-// then share that XCD's L2.
+// receives a contiguous run of tiles, ordered in groups of row panels so that
+// the tiles an XCD runs at the same time share A and W panels in its L2.
 #include "common.h"
 #include "kernels.h"
 
@@ -37,6 +37,7 @@ typedef __attribute__((address_space(1))) void global_void;
 constexpr int kBK = 64;        // K per step
 constexpr int kRowBytes = 128; // one LDS row: 64 bf16
 constexpr int kRowsPerBlock = 8;
+constexpr int kGroupM = 16;    // row panels per rasterisation group
 
 struct Params {
   const uint16_t* A;
@@ -106,10 +107,17 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
+  // Tile order: workgroup i runs on XCD i % 8, so each XCD first receives a
+  // contiguous run of logical tile ids; logical ids then walk groups of
+  // kGroupM row panels, N tiles within a group, row panels innermost, so the
+  // tiles an XCD runs together share few A and W panels in its L2.
   const int nblk = gridDim.x, b = blockIdx.x;
   const int q = nblk >> 3, r8 = nblk & 7, xcd = b & 7, idx = b >> 3;
   const int logical = (xcd < r8) ? xcd * (q + 1) + idx : r8 * (q + 1) + (xcd - r8) * q + idx;
-  const int tile_m = logical / p.tiles_n, tile_n = logical - tile_m * p.tiles_n;
+  const int tiles_m = (p.M + BM - 1) / BM;
+  const int group = logical / (kGroupM * p.tiles_n), in_group = logical - group * kGroupM * p.tiles_n;
+  const int gm = min(kGroupM, tiles_m - group * kGroupM);
+  const int tile_n = in_group / gm, tile_m = group * kGroupM + (in_group - tile_n * gm);
   const int m0 = tile_m * BM, n0 = tile_n * BN;
 
   // Per block this lane loads: the row start, the logical 16-byte chunk, and
