@@ -53,6 +53,7 @@ struct Params {
   const float* cls;
   const float* pos;
   float* ccls;
+  int row0;     // this launch covers rows [row0, M)
   int tiles_n;
 };
 
@@ -114,11 +115,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   const int nblk = gridDim.x, b = blockIdx.x;
   const int q = nblk >> 3, r8 = nblk & 7, xcd = b & 7, idx = b >> 3;
   const int logical = (xcd < r8) ? xcd * (q + 1) + idx : r8 * (q + 1) + (xcd - r8) * q + idx;
-  const int tiles_m = (p.M + BM - 1) / BM;
+  const int tiles_m = (p.M - p.row0 + BM - 1) / BM;
   const int group = logical / (kGroupM * p.tiles_n), in_group = logical - group * kGroupM * p.tiles_n;
   const int gm = min(kGroupM, tiles_m - group * kGroupM);
   const int tile_n = in_group / gm, tile_m = group * kGroupM + (in_group - tile_n * gm);
-  const int m0 = tile_m * BM, n0 = tile_n * BN;
+  const int m0 = p.row0 + tile_m * BM, n0 = tile_n * BN;
 
   // Per block this lane loads: the row start, the logical 16-byte chunk, and
   // the block's LDS offset within a stage.
@@ -344,9 +345,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 }
 
 template <int BM, int BN, int WM, int WN, Epi E>
-hipError_t launch_cfg(const Params& p0, hipStream_t s) {
+hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   Params p = p0;
-  const int64_t tm = (p.M + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
+  p.row0 = row0;
+  const int64_t tm = (p.M - row0 + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
   p.tiles_n = (int)tn;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
@@ -357,23 +359,40 @@ hipError_t launch_cfg(const Params& p0, hipStream_t s) {
 
 template <Epi E>
 hipError_t launch_epi(const Params& p, hipStream_t s) {
-  // Pick the tile that keeps the chip busiest: estimated time is the number
-  // of rounds of concurrent workgroups (one per CU) times the relative cost
-  // of one tile.
+  // Pick the launch plan that keeps the chip busiest.  Estimated time is the
+  // number of rounds of concurrent workgroups (one per CU) times the relative
+  // cost of one tile.  Besides single launches of one tile shape there is a
+  // split plan against wave quantisation: the whole rounds of 256x256 tiles
+  // first, then the remaining row panels as 128x256 tiles in a second launch.
+  constexpr int kCUs = 256;
+  constexpr double kRel128x256 = 0.6;
+  auto rounds = [](int64_t tiles) { return (double)((tiles + kCUs - 1) / kCUs); };
   struct Cfg { int bm, bn; double rel; };
   const Cfg cfgs[3] = {{256, 256, 1.0}, {256, 128, 0.62}, {128, 128, 0.36}};
-  const int cus = 256;
   int best = 0;
   double best_t = 1e300;
   for (int i = 0; i < 3; ++i) {
     const int64_t tiles = ((p.M + cfgs[i].bm - 1) / cfgs[i].bm) * ((p.N + cfgs[i].bn - 1) / cfgs[i].bn);
-    const double t = (double)((tiles + cus - 1) / cus) * cfgs[i].rel;
+    const double t = rounds(tiles) * cfgs[i].rel;
     if (t < best_t - 1e-9) { best_t = t; best = i; }
   }
+  const int64_t tn = (p.N + 255) / 256, total = tn * ((p.M + 255) / 256);
+  const int64_t head_rows = (total / kCUs) * kCUs / tn * 256;  // rows in whole rounds
+  if (head_rows > 0 && head_rows < p.M) {
+    const int64_t tail_tiles = ((p.M - head_rows + 127) / 128) * tn;
+    const double t = rounds(head_rows / 256 * tn) + kRel128x256 * rounds(tail_tiles);
+    if (t < best_t - 0.1) {
+      Params head = p;
+      head.M = (int)head_rows;
+      hipError_t e = launch_cfg<256, 256, 2, 4, E>(head, 0, s);
+      if (e != hipSuccess) return e;
+      return launch_cfg<128, 256, 2, 4, E>(p, (int)head_rows, s);
+    }
+  }
   switch (best) {
-    case 0: return launch_cfg<256, 256, 2, 4, E>(p, s);
-    case 1: return launch_cfg<256, 128, 2, 2, E>(p, s);
-    default: return launch_cfg<128, 128, 2, 2, E>(p, s);
+    case 0: return launch_cfg<256, 256, 2, 4, E>(p, 0, s);
+    case 1: return launch_cfg<256, 128, 2, 2, E>(p, 0, s);
+    default: return launch_cfg<128, 128, 2, 2, E>(p, 0, s);
   }
 }
 

@@ -125,6 +125,9 @@ LINEAR_CASES = [
     (BF16, ffi.EPI_BIAS_F32OUT, 256, 1000, 768, 768, 768, 1000),
     (BF16, ffi.EPI_BIAS, 33, 192, 64, 192, 192, 576),
     (BF16, ffi.EPI_BIAS, 1, 8, 8, 8, 8, 8),
+    # enough 256x256 tiles for a second, 128x256-tile launch over the last rows
+    (BF16, ffi.EPI_BIAS_GELU, 21999, 3072, 768, 768, 768, 3072),
+    (BF16, ffi.EPI_BIAS_RESID, 22000, 768, 3072, 3072, 3072, 768),
     (FP32, ffi.EPI_BIAS, 68, 192, 64, 64, 64, 192),
     (FP32, ffi.EPI_BIAS_GELU, 70, 67, 61, 64, 61, 128),
     (FP32, ffi.EPI_BIAS_RESID, 68, 64, 33, 64, 128, 64),
@@ -141,10 +144,12 @@ def test_linear(case):
     np.testing.assert_array_equal(tail_after, tail_before)  # columns >= N untouched
 
 
-def test_linear_residual_fp32_class_rows():
-    """The bf16 residual epilogue keeps class-token rows in the fp32 side buffer."""
-    got, ref, tail_after, tail_before = _linear_case(BF16, ffi.EPI_BIAS_RESID, 4 * 197, 768, 460,
-                                                     3072, 3072, 768, tokens=197)
+@pytest.mark.parametrize("images", [4, 112])
+def test_linear_residual_fp32_class_rows(images):
+    """The bf16 residual epilogue keeps class-token rows in the fp32 side buffer
+    (112 images: the rows are split over two launches of different tiles)."""
+    got, ref, tail_after, tail_before = _linear_case(BF16, ffi.EPI_BIAS_RESID, images * 197, 768,
+                                                     460, 3072, 3072, 768, tokens=197)
     assert rel_err(got, ref) < 1e-2
     cls_err = np.abs(got[::197] - ref[::197]).max() / np.abs(ref[::197]).max()
     assert cls_err < 1e-5      # fp32 rows: no bf16 rounding of the class rows
