@@ -81,9 +81,24 @@ def cpu_baseline(cfg, table, w_stored, x_stored, budget_s=12.0, max_images=64):
         oracle.vit_forward(p, x_stored[n:n + 2], cfg.head_dim, cfg.ln_eps)
         n += 2
     dt = time.perf_counter() - t0
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        blas = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}"
+                                 for i in threadpool_info() if i.get("user_api") == "blas"}))
+    except Exception:
+        blas = "unknown"
     return {"value": n / dt, "unit": "images/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n} images of the same ViT-B/16 batch in DN mode 0 (full width), "
-                      f"fp64 numpy, {dt:.1f} s wall"}
+                      f"fp64 numpy, {dt:.1f} s wall",
+            "cpu_model": cpu_model, "blas": blas, "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
 def latency_regime(torch, ffi, inputs, cfg, w, table, calls=1000, warmup=10):
@@ -124,6 +139,11 @@ def main():
     ap.add_argument("--no-latency", action="store_true", help="skip the batch-1/8 latency regime")
     ap.add_argument("--modes", type=str, default="all",
                     help="comma-separated DN modes to time (mode 0 is always timed)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="end with three plain copies of 1 GiB (out = in * 1, fp32), the "
+                         "calibration dispatches for HBM byte counters")
+    ap.add_argument("--work-out", type=str, default=None,
+                    help="write the algorithmic work per kernel class (mode 0) to this JSON file")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the elastic-ViT forward is not sharded across GPUs "
@@ -240,7 +260,25 @@ def main():
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(cfg, table, inputs.stored_weights(cfg, w),
                                               inputs.stored_images(cfg, x))
+    if args.work_out:
+        classes = {}
+        for kc in ffi.KERNELS:
+            f, b, n = vit.kernel_work(0, B, kc)
+            classes[kc] = {"flops_per_launch": f / n, "bytes_per_launch": b / n,
+                           "launches_per_forward": n}
+        json.dump({"classes": classes, "dominant": dominant, "dominant_avg_us": avg_s * 1e6,
+                   "class_ms_mode0": class_ms, "source_hash": kernel_source_hash()},
+                  open(args.work_out, "w"), indent=1)
     vit.close()
+    if args.copy_probe:
+        n = (1 << 30) // 4
+        src = torch.empty(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log("copy probe done")
     print(json.dumps(result), flush=True)
 
 

@@ -1,0 +1,282 @@
+"""rocprofv3 runs and summaries for the elastic-ViT forward (ViT-B/16, bf16,
+batch 256, DN mode 0).
+
+    python -m paper_2609_10018_amd.pmc --out gpurun_out/pmc
+
+runs four profiled passes of ``bench.py`` (each a child process under its own
+time limit) and writes ``summary.md`` and ``traffic.json`` into ``--out``:
+
+1. ``--kernel-trace --stats``: per-dispatch durations; ``bench.py`` also
+   writes the library's algorithmic work per kernel class (``work.json``).
+2. ``--pmc FETCH_SIZE``  3. ``--pmc WRITE_SIZE``: L2-to-fabric kilobytes per
+   dispatch.  Both counters are scaled by what they read for a plain copy of
+   known size (``bench.py --copy-probe``: out = in * 1 over 1 GiB of fp32),
+   so the figures are bytes.
+4. ``--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE``: matrix-core busy
+   fraction per kernel class.
+
+Dispatches are assigned to the library's kernel classes (patch, ln, qkv,
+attn, proj, fc1, fc2, head) from their kernel names and order in the forward;
+one class launch may be two dispatches (the GEMM's whole-rounds launch and
+its tail launch), so per-launch figures sum over a class's consecutive
+dispatches.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import json
+import os
+import re
+import subprocess
+import sys
+from collections import defaultdict
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+BENCH = os.path.join(ROOT, "bench.py")
+COPY_PROBE_BYTES = 1 << 30          # bench.py --copy-probe: reads and writes this many bytes
+EPI_CLASS = {"0": "qkv", "1": "fc1", "3": "head", "4": "patch"}  # Epi 2 (residual): proj or fc2
+CLASSES = ["patch", "ln", "qkv", "attn", "proj", "fc1", "fc2", "head"]
+
+TRACE_ARGS = ["--steps", "20", "--warmup", "3", "--no-cpu", "--no-latency", "--modes", "0",
+              "--copy-probe"]
+PMC_ARGS = ["--steps", "2", "--warmup", "1", "--no-cpu", "--no-latency", "--modes", "0",
+            "--copy-probe"]
+PASSES = {
+    "fetch": ["FETCH_SIZE"],
+    "write": ["WRITE_SIZE"],
+    "mfma": ["SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"],
+}
+
+
+def log(msg: str) -> None:
+    print(f"[pmc] {msg}", flush=True)
+
+
+def classify(names):
+    """Kernel class of each dispatch, given the kernel names in dispatch order."""
+    out, last = [], None
+    for n in names:
+        if "gemm_bf16_kernel" in n or "gemm_f32_kernel" in n:
+            m = re.search(r"\(elasto::Epi\)(\d)", n)
+            e = m.group(1) if m else "?"
+            if e == "2":
+                # The residual GEMM after attention is the projection, after fc1 it is fc2.
+                c = last if last in ("proj", "fc2") else ("proj" if last == "attn" else "fc2")
+            else:
+                c = EPI_CLASS.get(e, "other")
+        elif "attention" in n:
+            c = "attn"
+        elif "layernorm" in n:
+            c = "ln"
+        elif "MulFunctor" in n:
+            c = "copy"
+        else:
+            c = "other"
+        out.append(c)
+        last = c
+    return out
+
+
+def launches(classes):
+    """Maximal runs of one class: (class, [dispatch indices])."""
+    runs = []
+    for i, c in enumerate(classes):
+        if runs and runs[-1][0] == c:
+            runs[-1][1].append(i)
+        else:
+            runs.append((c, [i]))
+    return runs
+
+
+def read_trace(d):
+    f = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)[0]
+    rows = sorted(csv.DictReader(open(f)), key=lambda r: int(r["Dispatch_Id"]))
+    names = [r["Kernel_Name"] for r in rows]
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3 for r in rows]  # us
+    return names, dur
+
+
+def read_counters(d):
+    """Per dispatch (in dispatch order): name and {counter: value}."""
+    f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+    disp = {}
+    for r in csv.DictReader(open(f)):
+        key = (r["Process_Id"], int(r["Dispatch_Id"]))
+        e = disp.setdefault(key, {"name": r["Kernel_Name"], "c": defaultdict(float)})
+        e["c"][r["Counter_Name"]] += float(r["Counter_Value"])
+    keys = sorted(disp)
+    return [disp[k]["name"] for k in keys], [disp[k]["c"] for k in keys]
+
+
+def simd_count(d):
+    for f in glob.glob(os.path.join(d, "**", "*agent_info.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r.get("Agent_Type") == "GPU":
+                return int(r["Simd_Count"])
+    return 1024
+
+
+def per_launch(classes, values):
+    """Per class: (number of launches, mean per launch of the summed values)."""
+    acc = defaultdict(lambda: [0, 0.0])
+    for c, idx in launches(classes):
+        acc[c][0] += 1
+        acc[c][1] += sum(values[i] for i in idx)
+    return {c: (n, s / n) for c, (n, s) in acc.items()}
+
+
+def run_pass(out, tag, rocprof_args, bench_args, limit):
+    d = os.path.join(out, tag)
+    cmd = ["timeout", "-s", "KILL", str(limit), "rocprofv3", *rocprof_args, "-f", "csv",
+           "-d", d, "-o", "run", "--", sys.executable, BENCH, *bench_args]
+    log(f"pass {tag}: {' '.join(cmd)}")
+    env = dict(os.environ, TMPDIR="/tmp")
+    with open(os.path.join(out, f"{tag}.log"), "w") as lf:
+        r = subprocess.run(cmd, cwd="/tmp", env=env, stdout=lf, stderr=subprocess.STDOUT)
+    log(f"pass {tag}: exit {r.returncode}")
+    if r.returncode != 0:
+        raise SystemExit(f"rocprofv3 pass {tag} failed with exit code {r.returncode}")
+    return d, cmd
+
+
+def _portable(cmd):
+    """A command as text, with this checkout's absolute paths shown as <repo>."""
+    return " ".join(cmd).replace(ROOT, "<repo>")
+
+
+def summarize(out, cmds):
+    work = json.load(open(os.path.join(out, "work.json")))
+    names, dur = read_trace(os.path.join(out, "trace"))
+    cls = classify(names)
+    t_launch = per_launch(cls, dur)
+
+    fetch_n, fetch_c = read_counters(os.path.join(out, "fetch"))
+    write_n, write_c = read_counters(os.path.join(out, "write"))
+    mfma_n, mfma_c = read_counters(os.path.join(out, "mfma"))
+    simds = simd_count(os.path.join(out, "mfma"))
+
+    def calibrated(names_, cvals, counter):
+        c_ = classify(names_)
+        vals = [v[counter] * 1024.0 for v in cvals]          # KiB -> bytes
+        copies = [vals[i] for i, c in enumerate(c_) if c == "copy"]
+        if not copies:
+            raise SystemExit("no copy-probe dispatch found for calibration")
+        scale = COPY_PROBE_BYTES / (sum(copies) / len(copies))
+        return per_launch(c_, [v * scale for v in vals]), scale, sum(copies) / len(copies)
+
+    rd, rd_scale, rd_copy = calibrated(fetch_n, fetch_c, "FETCH_SIZE")
+    wr, wr_scale, wr_copy = calibrated(write_n, write_c, "WRITE_SIZE")
+    mc = classify(mfma_n)
+    busy = per_launch(mc, [v["SQ_VALU_MFMA_BUSY_CYCLES"] for v in mfma_c])
+    # GRBM_GUI_ACTIVE comes summed over the 8 XCDs; each XCD counts the same cycles.
+    active = per_launch(mc, [v["GRBM_GUI_ACTIVE"] / 8.0 for v in mfma_c])
+
+    rows, table = [], {}
+    for c in CLASSES:
+        if c not in t_launch:
+            continue
+        n, us = t_launch[c]
+        wk = work["classes"][c]
+        flops, algo_b = wk["flops_per_launch"], wk["bytes_per_launch"]
+        hbm = rd[c][1] + wr[c][1] if c in rd and c in wr else None
+        util = busy[c][1] / (active[c][1] * simds) if c in busy and active[c][1] > 0 else None
+        e = {"launches": n, "avg_us": us, "flops": flops, "algo_bytes": algo_b,
+             "tflops": flops / us * 1e-6 if flops else None, "gbs": algo_b / us * 1e-3,
+             "fetch_bytes": rd.get(c, (0, None))[1], "write_bytes": wr.get(c, (0, None))[1],
+             "hbm_bytes": hbm, "mfma_util": util}
+        table[c] = e
+        rows.append(
+            f"| {c} | {n} | {us:.1f} | "
+            + (f"{e['tflops']:.0f} TF/s" if flops else "-") + f" | {e['gbs']:.0f} GB/s | "
+            + (f"{100 * util:.1f}%" if util is not None else "-") + " | "
+            + f"{algo_b / 1e6:.1f} | "
+            + (f"{e['fetch_bytes'] / 1e6:.1f} | {e['write_bytes'] / 1e6:.1f} | {hbm / algo_b:.2f}"
+               if hbm is not None else "- | - | -") + " |")
+
+    dom = work["dominant"]
+    traffic = {
+        "workload": "elastic ViT-B/16 forward, DN mode 0, batch 256, bf16",
+        "kernel_class": dom,
+        "source_hash": work["source_hash"],
+        "hbm_bytes_per_launch": table[dom]["hbm_bytes"],
+        "fetch_bytes_per_launch": table[dom]["fetch_bytes"],
+        "write_bytes_per_launch": table[dom]["write_bytes"],
+        "algorithmic_bytes_per_launch": table[dom]["algo_bytes"],
+        "calibration": {"copy_bytes": COPY_PROBE_BYTES, "fetch_scale": rd_scale,
+                        "write_scale": wr_scale, "fetch_copy_bytes_raw": rd_copy,
+                        "write_copy_bytes_raw": wr_copy},
+        "classes": table,
+        "commands": {k: _portable(v) for k, v in cmds.items()},
+    }
+    json.dump(traffic, open(os.path.join(out, "traffic.json"), "w"), indent=1)
+
+    md = [
+        "# Kernel classes of the elastic ViT-B/16 forward — bf16, batch 256, DN mode 0",
+        "",
+        "Commands (GPU box, run from `/tmp` with `TMPDIR=/tmp`; committed files only):",
+        "",
+        "    python -m paper_2609_10018_amd.pmc --out <repo>/gpurun_out/pmc",
+        "",
+        "which runs:",
+        "",
+    ]
+    md += [f"    {_portable(v)}" for v in cmds.values()]
+    md += [
+        "",
+        f"Per launch of each kernel class (a GEMM class launch can be two dispatches: whole "
+        f"rounds of 256x256 tiles, then the tail rows). Durations from the kernel trace "
+        f"({sum(n for n, _ in t_launch.values())} class launches). MFMA util = "
+        f"SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x {simds} SIMDs). Fetch / write = "
+        f"FETCH_SIZE / WRITE_SIZE scaled by the copy probe (1 GiB read + 1 GiB written; "
+        f"raw counters read {rd_copy / 2**30:.3f} GiB and {wr_copy / 2**30:.3f} GiB, "
+        f"scales {rd_scale:.3f} and {wr_scale:.3f}). Ratio = (fetch + write) / algorithmic bytes.",
+        "",
+        "| class | launches | avg µs | achieved (algorithmic FLOP) | algorithmic bytes / time "
+        "| MFMA util | algorithmic MB | fetch MB | write MB | ratio |",
+        "|---|---|---|---|---|---|---|---|---|---|",
+        *rows,
+        "",
+        f"Dominant class: **{dom}**, {table[dom]['avg_us']:.1f} µs per launch in the trace; "
+        f"bench.py's HIP-event timing in the traced run: {work['dominant_avg_us']:.1f} µs.",
+        f"Source hash of the kernels profiled: `{work['source_hash']}`.",
+        "",
+    ]
+    stats = glob.glob(os.path.join(out, "trace", "**", "*kernel_stats.csv"), recursive=True)
+    if stats:
+        md += ["rocprofv3 `--stats` per kernel name (trace pass, every dispatch of the run):", "",
+               "| kernel | calls | avg µs | min µs | max µs | share |", "|---|---|---|---|---|---|"]
+        for r in csv.DictReader(open(stats[0])):
+            name = re.sub(r"\(elasto::\(anonymous namespace\)::\w+\)$", "", r["Name"])
+            name = name.replace("elasto::(anonymous namespace)::", "").replace("void ", "")
+            md.append(f"| `{name[:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                      f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                      f"{float(r['Percentage']):.1f}% |")
+        md.append("")
+    open(os.path.join(out, "summary.md"), "w").write("\n".join(md))
+    log(f"wrote {out}/summary.md and traffic.json")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "pmc"))
+    ap.add_argument("--summarize-only", action="store_true")
+    args = ap.parse_args()
+    out = os.path.abspath(args.out)
+    os.makedirs(out, exist_ok=True)
+    cmds = {}
+    if not args.summarize_only:
+        _, cmds["trace"] = run_pass(out, "trace", ["--kernel-trace", "--stats"],
+                                    TRACE_ARGS + ["--work-out", os.path.join(out, "work.json")],
+                                    300)
+        for tag, counters in PASSES.items():
+            _, cmds[tag] = run_pass(out, tag, ["--pmc", *counters], PMC_ARGS, 180)
+        json.dump(cmds, open(os.path.join(out, "commands.json"), "w"))
+    else:
+        cmds = json.load(open(os.path.join(out, "commands.json")))
+    summarize(out, cmds)
+
+
+if __name__ == "__main__":
+    main()
