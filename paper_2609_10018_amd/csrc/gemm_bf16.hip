@@ -37,7 +37,6 @@ typedef __attribute__((address_space(1))) void global_void;
 constexpr int kBK = 64;        // K per step
 constexpr int kRowBytes = 128; // one LDS row: 64 bf16
 constexpr int kRowsPerBlock = 8;
-constexpr int kGroupM = 16;    // row panels per rasterisation group
 
 struct Params {
   const uint16_t* A;
@@ -55,6 +54,7 @@ struct Params {
   float* ccls;
   int row0;     // this launch covers rows [row0, M)
   int tiles_n;
+  int group_m;  // row panels per rasterisation group
 };
 
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
@@ -65,6 +65,12 @@ template <int N>
 __device__ __forceinline__ void wait_vm_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+}
+
+// Wait until every LDS operation of this wave has completed (vector memory
+// operations may still be in flight).
+__device__ __forceinline__ void wait_lds() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14));
 }
 
 // Store 8 floats (the first `valid` of them when the chunk is ragged).
@@ -110,15 +116,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 
   // Tile order: workgroup i runs on XCD i % 8, so each XCD first receives a
   // contiguous run of logical tile ids; logical ids then walk groups of
-  // kGroupM row panels, N tiles within a group, row panels innermost, so the
+  // group_m row panels, N tiles within a group, row panels innermost, so the
   // tiles an XCD runs together share few A and W panels in its L2.
   const int nblk = gridDim.x, b = blockIdx.x;
   const int q = nblk >> 3, r8 = nblk & 7, xcd = b & 7, idx = b >> 3;
   const int logical = (xcd < r8) ? xcd * (q + 1) + idx : r8 * (q + 1) + (xcd - r8) * q + idx;
   const int tiles_m = (p.M - p.row0 + BM - 1) / BM;
-  const int group = logical / (kGroupM * p.tiles_n), in_group = logical - group * kGroupM * p.tiles_n;
-  const int gm = min(kGroupM, tiles_m - group * kGroupM);
-  const int tile_n = in_group / gm, tile_m = group * kGroupM + (in_group - tile_n * gm);
+  const int group = logical / (p.group_m * p.tiles_n), in_group = logical - group * p.group_m * p.tiles_n;
+  const int gm = min(p.group_m, tiles_m - group * p.group_m);
+  const int tile_n = in_group / gm, tile_m = group * p.group_m + (in_group - tile_n * gm);
   const int m0 = p.row0 + tile_m * BM, n0 = tile_n * BN;
 
   // Per block this lane loads: the row start, the logical 16-byte chunk, and
@@ -235,11 +241,44 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
                                             // half-waves land on distinct banks
   constexpr int CPR = BN / 8;               // 8-column chunks per row
   constexpr int NT = 64 * NW;
+  constexpr int RSTEP = NT / CPR;           // rows between one thread's chunks
+  constexpr int ITER = SR / RSTEP;          // chunks per thread per pass
+  static_assert(NT % CPR == 0 && SR % RSTEP == 0, "epilogue chunking");
   float* stg = reinterpret_cast<float*>(smem);
-  wait_vm_lds<0>();
+
+  // A thread always handles the same 8 columns: load their bias once.
+  const int cc = tid % CPR, r_first = tid / CPR;
+  const int col = n0 + cc * 8;
+  const bool col_in = col < p.N, full = col + 8 <= p.N;
+  float bv[8];
+  if (full) {
+    const f32x4 b0 = *reinterpret_cast<const f32x4*>(p.bias + col);
+    const f32x4 b1 = *reinterpret_cast<const f32x4*>(p.bias + col + 4);
+    bv[0] = b0[0]; bv[1] = b0[1]; bv[2] = b0[2]; bv[3] = b0[3];
+    bv[4] = b1[0]; bv[5] = b1[1]; bv[6] = b1[2]; bv[7] = b1[3];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bv[e] = col + e < p.N ? p.bias[col + e] : 0.0f;
+  }
+
+  wait_lds();  // every wave has finished reading the last stage
   __builtin_amdgcn_s_barrier();
 #pragma unroll
   for (int pass = 0; pass < BM / SR; ++pass) {
+    const int row_base = m0 + pass * SR + r_first;
+    // Residual rows of this pass: issued before the staging so that their
+    // latency overlaps it.
+    u32x4 res[ITER];
+    if constexpr (E == Epi::BiasResid) {
+#pragma unroll
+      for (int it = 0; it < ITER; ++it) {
+        const int row = row_base + it * RSTEP;
+        res[it] = (full && row < p.M)
+                      ? *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.C) +
+                                                        (int64_t)row * p.ldc + col)
+                      : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
     if ((wm * WTM) / SR == pass) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -251,26 +290,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
             stg[rl * SS + wn * WTN + j * 32 + lr] = acc[i][j][e];
           }
     }
-    wait_vm_lds<0>();
+    wait_lds();
     __builtin_amdgcn_s_barrier();
-    for (int c = tid; c < SR * CPR; c += NT) {
-      const int rl = c / CPR, cc = c - rl * CPR;
-      const int row = m0 + pass * SR + rl, col = n0 + cc * 8;
-      if (row >= p.M || col >= p.N) continue;
-      const bool full = col + 8 <= p.N;
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int rl = r_first + it * RSTEP;
+      const int row = row_base + it * RSTEP;
+      if (row >= p.M || !col_in) continue;
       const f32x4 s0 = *reinterpret_cast<const f32x4*>(stg + rl * SS + cc * 8);
       const f32x4 s1 = *reinterpret_cast<const f32x4*>(stg + rl * SS + cc * 8 + 4);
       float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
-      float bv[8];
-      if (full) {
-        const f32x4 b0 = *reinterpret_cast<const f32x4*>(p.bias + col);
-        const f32x4 b1 = *reinterpret_cast<const f32x4*>(p.bias + col + 4);
-        bv[0] = b0[0]; bv[1] = b0[1]; bv[2] = b0[2]; bv[3] = b0[3];
-        bv[4] = b1[0]; bv[5] = b1[1]; bv[6] = b1[2]; bv[7] = b1[3];
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) bv[e] = col + e < p.N ? p.bias[col + e] : 0.0f;
-      }
       const int64_t o = (int64_t)row * p.ldc + col;
       if constexpr (E == Epi::BiasF32) {
         float* cp = static_cast<float*>(p.C) + o;
@@ -294,7 +323,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         for (int e = 0; e < 8; ++e) v[e] += bv[e];
       } else if constexpr (E == Epi::BiasGelu) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = gelu_as(v[e] + bv[e]);
+        for (int e = 0; e < 8; ++e) v[e] = gelu_poly(v[e] + bv[e]);
       } else if constexpr (E == Epi::BiasResid) {
         if (cls_row != nullptr) {
 #pragma unroll
@@ -304,7 +333,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           continue;
         }
         if (full) {
-          const u32x4 x = *reinterpret_cast<const u32x4*>(cp);
+          const u32x4 x = res[it];
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             v[e] = __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16)) +
@@ -317,9 +346,25 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       } else {  // Patch: class rows (t == 0) take cls + pos[0] and drop the product
         const int t = row % p.tokens;
         const float* pp = p.pos + (int64_t)t * p.N + col;
+        if (full) {
+          const f32x4 p0 = *reinterpret_cast<const f32x4*>(pp);
+          const f32x4 p1 = *reinterpret_cast<const f32x4*>(pp + 4);
+          const float pv[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
+          if (t == 0) {
+            const f32x4 c0 = *reinterpret_cast<const f32x4*>(p.cls + col);
+            const f32x4 c1 = *reinterpret_cast<const f32x4*>(p.cls + col + 4);
+            const float cv[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (col + e < p.N) v[e] = (t == 0 ? p.cls[col + e] : v[e] + bv[e]) + pp[e];
+            for (int e = 0; e < 8; ++e) v[e] = cv[e] + pv[e];
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = (v[e] + bv[e]) + pv[e];
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (col + e < p.N) v[e] = (t == 0 ? p.cls[col + e] : v[e] + bv[e]) + pp[e];
+        }
         if (cls_row != nullptr) {
           store_f32x8(cls_row, v, full, p.N - col);
           continue;
@@ -338,7 +383,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       }
     }
     if (pass + 1 < BM / SR) {
-      wait_vm_lds<0>();
+      wait_lds();  // staged rows read by every wave before the next pass overwrites them
       __builtin_amdgcn_s_barrier();
     }
   }
@@ -350,6 +395,9 @@ hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   p.row0 = row0;
   const int64_t tm = (p.M - row0 + BM - 1) / BM, tn = (p.N + BN - 1) / BN;
   p.tiles_n = (int)tn;
+  // Long K: tiles in flight stream whole A panels, so few panels per group
+  // keep each panel's N tiles together; short K: a wider group.
+  p.group_m = p.K >= 2048 ? 2 : 4;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E>), dim3((unsigned)blocks),
