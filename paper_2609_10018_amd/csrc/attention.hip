@@ -1,7 +1,8 @@
 // Multi-head self-attention over the active heads (Eq. 3):
 // o = softmax(q k^T * scale) v per (sequence, head slot).
 //
-// bf16 path (head_dim 64): one workgroup per (sequence, head slot).  K is
+// bf16 path (head_dim 64): one workgroup of 8 waves per (sequence, head
+// slot), so no wave takes more than two of the (up to 15) query blocks.  K is
 // staged whole in LDS by direct global->LDS loads (rows of 128 B, 16-byte
 // chunks XOR-swizzled) and V is staged transposed (V^T, one row per feature);
 // padding keys past the last token repeat that token and are masked (zero
@@ -14,7 +15,8 @@
 // of O = P V: a k-slot of the MFMA is only a label, so the 8 keys a lane
 // holds for two adjacent key tiles form its k-slots, and the V operand is
 // read from V^T with the same key-to-slot assignment (two 8-byte reads).
-// The 1/rowsum normalisation is applied to O in fp32.
+// The 1/rowsum normalisation is applied to O in fp32; each wave stages its
+// 16x64 O block in LDS and writes it as 16-byte row chunks.
 //
 // fp32 path: a plain per-query loop (two passes over the keys: max, then
 // exp-sum and weighted V sum), fp32 FMA throughout.
@@ -29,6 +31,10 @@ typedef __attribute__((address_space(1))) void global_void;
 
 constexpr int kHd = 64;
 constexpr int kNtMax = 15;  // 16-key tiles: tokens <= 240
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kOs = 72;     // O staging row stride (elements): 144 B, 16-byte aligned
+constexpr int kOStage = 16 * kOs * 2;  // bytes per wave
 
 __device__ __forceinline__ int k_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
@@ -44,7 +50,7 @@ struct AttnP {
 // NT = ceil(T / 16) key tiles, fixed at compile time so that every loop over
 // keys is fully unrolled and only the last tile carries the key < T mask.
 template <int NT>
-__global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
+__global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
   constexpr int TV = NT * 16;  // keys staged in V^T
   constexpr int VS = TV + 4;   // V^T row stride (elements): rows land on distinct banks
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -73,8 +79,8 @@ __global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
   // logical chunk that k_off() places there.  Rows past the last token re-read
   // token T-1: their scores are masked out of the softmax.
 #pragma unroll
-  for (int i = 0; i < (2 * NT + 3) / 4; ++i) {
-    const int blk = wave + 4 * i;
+  for (int i = 0; i < (2 * NT + kWaves - 1) / kWaves; ++i) {
+    const int blk = wave + kWaves * i;
     if (blk < 2 * NT) {
       const int r = blk * 8 + (lane >> 3);
       const int c = (lane & 7) ^ (r & 7);
@@ -84,16 +90,16 @@ __global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
   }
   // V: every 16-byte chunk load is issued before any transposed LDS write.
   // Keys past the last token re-read token T-1: their probabilities are 0.
-  constexpr int kVLoads = (TV * 8 + 255) / 256;
+  constexpr int kVLoads = (TV * 8 + kThreads - 1) / kThreads;
   u32x4 vv[kVLoads];
 #pragma unroll
   for (int i = 0; i < kVLoads; ++i) {
-    const int idx = tid + 256 * i, key = min(idx >> 3, T - 1), c = idx & 7;
+    const int idx = tid + kThreads * i, key = min(idx >> 3, T - 1), c = idx & 7;
     vv[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)key * p.qs + 2 * kHd + c * 8);
   }
 #pragma unroll
   for (int i = 0; i < kVLoads; ++i) {
-    const int idx = tid + 256 * i, key = idx >> 3, c = idx & 7;
+    const int idx = tid + kThreads * i, key = idx >> 3, c = idx & 7;
     if (key < TV) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
@@ -104,7 +110,8 @@ __global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
   __syncthreads();
 
   const float c2 = p.scale_log2;
-  for (int qb = wave; qb < NT; qb += 4) {
+  uint16_t* ost = reinterpret_cast<uint16_t*>(smem + NT * 16 * 128 + kHd * VS * 2 + wave * kOStage);
+  for (int qb = wave; qb < NT; qb += kWaves) {
     const int q0 = qb * 16;
     f32x4 st[NT];
 #pragma unroll
@@ -121,7 +128,7 @@ __global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
     }
     __builtin_amdgcn_sched_barrier(0);
     bf16x8 qn[2];
-    if (qb + 4 < NT) load_q(qb + 4, qn);
+    if (qb + kWaves < NT) load_q(qb + kWaves, qn);
     // Keys of the last tile at or past T do not exist.
     bool valid[4];
 #pragma unroll
@@ -179,12 +186,18 @@ __global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
     for (int r = 0; r < 4; ++r) {
       const int qr = 4 * lg + r;
       const float ir = __shfl(inv, qr, 64);
-      const int q = q0 + qr;
-      if (q < T) {
-        uint16_t* op = p.o + ((int64_t)b * T + q) * p.os + (int64_t)s * kHd + lq;
 #pragma unroll
-        for (int n = 0; n < 4; ++n) op[n * 16] = f32_to_bf16(o[n][r] * ir);
-      }
+      for (int n = 0; n < 4; ++n) ost[qr * kOs + n * 16 + lq] = f32_to_bf16(o[n][r] * ir);
+    }
+    // The block's own LDS writes are complete before its lanes read them back.
+    __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int qr = h * 8 + (lane >> 3), c = lane & 7;
+      const int q = q0 + qr;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(ost + qr * kOs + c * 8);
+      if (q < T)
+        *reinterpret_cast<u32x4*>(p.o + ((int64_t)b * T + q) * p.os + (int64_t)s * kHd + c * 8) = w;
     }
     qf[0] = qn[0];
     qf[1] = qn[1];
@@ -193,9 +206,10 @@ __global__ __launch_bounds__(256, 3) void attention_bf16_kernel(AttnP p) {
 
 template <int NT>
 hipError_t launch_attn_nt(const AttnP& p, int batch, int heads, hipStream_t s) {
-  const size_t lds = (size_t)NT * 16 * 128 + (size_t)kHd * (NT * 16 + 4) * 2;
-  hipLaunchKernelGGL(attention_bf16_kernel<NT>, dim3((unsigned)(batch * heads)), dim3(256), lds, s,
-                     p);
+  const size_t lds =
+      (size_t)NT * 16 * 128 + (size_t)kHd * (NT * 16 + 4) * 2 + (size_t)kWaves * kOStage;
+  hipLaunchKernelGGL(attention_bf16_kernel<NT>, dim3((unsigned)(batch * heads)), dim3(kThreads),
+                     lds, s, p);
   return hipGetLastError();
 }
 
