@@ -241,8 +241,9 @@ elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, 
 /* out[r] = LayerNorm(x[r]) * g + b over d features, r < rows.  x row r starts
  * at x + r*x_stride; out is contiguous [rows][d].  BF16 path only: when x_cls
  * is non-NULL, rows with r % tokens == 0 (class-token rows) are read as fp32
- * from x_cls + (r / tokens) * d instead (tokens = 1: every row).  FP32 path:
- * x_cls must be NULL. */
+ * from x_cls + (r / tokens) * d instead (tokens = 1: every row); d and
+ * x_stride must be multiples of 8 and x, out, x_cls, g, b 16-byte aligned.
+ * FP32 path: x_cls must be NULL. */
 elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stride,
                                     const float* x_cls, int32_t tokens, void* out, int64_t rows,
                                     int32_t d, const float* g, const float* b, float eps,

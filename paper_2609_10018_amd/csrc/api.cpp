@@ -422,9 +422,9 @@ elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stri
     return fail(ELASTO_ERR_INVALID_ARG, "bad layernorm sizes");
   hipError_t e;
   if (dtype == ELASTO_BF16) {
-    if (d % 4 != 0 || x_stride % 4 != 0 || !aligned(x, 8) || !aligned(out, 8) || !aligned(g, 16) ||
-        !aligned(b, 16))
-      return fail(ELASTO_ERR_INVALID_ARG, "bf16 layernorm needs d, stride % 4 == 0 and aligned pointers");
+    if (d % 8 != 0 || x_stride % 8 != 0 || !aligned(x, 16) || !aligned(out, 16) ||
+        !aligned(g, 16) || !aligned(b, 16))
+      return fail(ELASTO_ERR_INVALID_ARG, "bf16 layernorm needs d, stride % 8 == 0 and 16-byte aligned pointers");
     e = launch_layernorm_bf16(x, x_stride, x_cls, tokens, out, rows, d, g, b, eps,
                               static_cast<hipStream_t>(hip_stream));
   } else if (dtype == ELASTO_FP32) {

@@ -1,20 +1,29 @@
 // LayerNorm over the feature axis: u = (x - mean) / sqrt(var + eps) * g + b,
-// biased variance, statistics in fp32.  Memory-bound: one wave per row, each
-// lane holding its share of the row in registers (two passes over registers,
-// one read of the row from HBM, one write).
+// biased variance, statistics in fp32.  Memory-bound: each lane holds its
+// share of a row in registers (two passes over registers, one read of the row
+// from HBM, one write).
 //
-// The bf16 path reads and writes 8-byte (4-element) bf16 vectors, so a wave
-// moves 512 contiguous bytes per instruction; the class-token rows of the
-// residual stream are fp32 and come from their own buffer.  Row stride is
-// free.
+// The bf16 path gives each row half a wave and reads and writes 16-byte
+// (8-element) bf16 vectors; the class-token rows of the residual stream are
+// fp32 and come from their own buffer.  Row stride is free.
 #include "common.h"
 #include "kernels.h"
 
 namespace elasto {
 namespace {
 
-constexpr int kMaxVecPerLane = 8;  // 4-element vectors per lane: d <= 2048
+constexpr int kMaxChunks = 8;  // 8-element chunks per lane: d <= 2048
 
+__device__ __forceinline__ float half_sum(float v) {
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) v += __shfl_xor(v, off, 32);
+  return v;
+}
+
+// Two rows per wave (32 lanes each), so a load instruction moves 16 bytes per
+// lane; NC = ceil(d / 256) chunks per lane.  Rows past the end re-read the
+// last row and store nothing.
+template <int NC>
 __global__ __launch_bounds__(256) void layernorm_bf16_kernel(const uint16_t* __restrict__ x,
                                                              int64_t x_stride,
                                                              const float* __restrict__ xcls,
@@ -24,66 +33,79 @@ __global__ __launch_bounds__(256) void layernorm_bf16_kernel(const uint16_t* __r
                                                              const float* __restrict__ g,
                                                              const float* __restrict__ b,
                                                              float eps) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int nvec = d >> 2;
+  const int hl = threadIdx.x & 31;
+  const int64_t row_raw = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
+  const bool live = row_raw < rows;
+  const int64_t row = live ? row_raw : rows - 1;
+  const int nch = d >> 3;
   const int64_t bi = xcls != nullptr ? row / tokens : 0;
-  const bool cls_row = xcls != nullptr && row == bi * tokens;  // uniform per wave
+  const bool cls_row = xcls != nullptr && row == bi * tokens;  // uniform per half-wave
   const uint16_t* xr = x + row * x_stride;
   const float* xc = cls_row ? xcls + bi * (int64_t)d : nullptr;
-  float v[kMaxVecPerLane][4];
+  float v[NC][8];
   float s = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kMaxVecPerLane; ++i) {
-    const int vi = lane + 64 * i;
-    if (vi < nvec) {
+  for (int i = 0; i < NC; ++i) {
+    const int ci = hl + 32 * i;
+    if (ci < nch) {
       if (cls_row) {
-        const f32x4 w = *reinterpret_cast<const f32x4*>(xc + 4 * vi);
-        v[i][0] = w[0];
-        v[i][1] = w[1];
-        v[i][2] = w[2];
-        v[i][3] = w[3];
+        const f32x4 w0 = *reinterpret_cast<const f32x4*>(xc + 8 * ci);
+        const f32x4 w1 = *reinterpret_cast<const f32x4*>(xc + 8 * ci + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[i][e] = w0[e];
+          v[i][4 + e] = w1[e];
+        }
       } else {
-        const u32x2 w = *reinterpret_cast<const u32x2*>(xr + 4 * vi);
-        v[i][0] = __uint_as_float(w[0] << 16);
-        v[i][1] = __uint_as_float(w[0] & 0xffff0000u);
-        v[i][2] = __uint_as_float(w[1] << 16);
-        v[i][3] = __uint_as_float(w[1] & 0xffff0000u);
+        const u32x4 w = *reinterpret_cast<const u32x4*>(xr + 8 * ci);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[i][2 * e] = __uint_as_float(w[e] << 16);
+          v[i][2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+        }
       }
-      s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[i][e];
     } else {
-      v[i][0] = v[i][1] = v[i][2] = v[i][3] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[i][e] = 0.0f;
     }
   }
   const float inv_d = 1.0f / (float)d;
-  const float mean = wave_sum(s) * inv_d;
+  const float mean = half_sum(s) * inv_d;
   float ss = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kMaxVecPerLane; ++i) {
-    if (lane + 64 * i < nvec) {
+  for (int i = 0; i < NC; ++i) {
+    if (hl + 32 * i < nch) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
+      for (int e = 0; e < 8; ++e) {
         const float c = v[i][e] - mean;
         ss += c * c;
       }
     }
   }
-  const float rstd = rsqrtf(wave_sum(ss) * inv_d + eps);
+  const float rstd = rsqrtf(half_sum(ss) * inv_d + eps);
+  if (!live) return;
   uint16_t* orow = out + row * (int64_t)d;
 #pragma unroll
-  for (int i = 0; i < kMaxVecPerLane; ++i) {
-    const int vi = lane + 64 * i;
-    if (vi < nvec) {
-      const f32x4 gv = *reinterpret_cast<const f32x4*>(g + 4 * vi);
-      const f32x4 bv = *reinterpret_cast<const f32x4*>(b + 4 * vi);
-      uint16_t h[4];
+  for (int i = 0; i < NC; ++i) {
+    const int ci = hl + 32 * i;
+    if (ci < nch) {
+      const f32x4 g0 = *reinterpret_cast<const f32x4*>(g + 8 * ci);
+      const f32x4 g1 = *reinterpret_cast<const f32x4*>(g + 8 * ci + 4);
+      const f32x4 b0 = *reinterpret_cast<const f32x4*>(b + 8 * ci);
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(b + 8 * ci + 4);
+      const float gv[8] = {g0[0], g0[1], g0[2], g0[3], g1[0], g1[1], g1[2], g1[3]};
+      const float bv[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+      u32x4 w;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) h[e] = f32_to_bf16((v[i][e] - mean) * rstd * gv[e] + bv[e]);
-      u32x2 w;
-      w[0] = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-      w[1] = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-      *reinterpret_cast<u32x2*>(orow + 4 * vi) = w;
+      for (int e = 0; e < 4; ++e) {
+        const uint16_t lo = f32_to_bf16((v[i][2 * e] - mean) * rstd * gv[2 * e] + bv[2 * e]);
+        const uint16_t hi =
+            f32_to_bf16((v[i][2 * e + 1] - mean) * rstd * gv[2 * e + 1] + bv[2 * e + 1]);
+        w[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+      }
+      *reinterpret_cast<u32x4*>(orow + 8 * ci) = w;
     }
   }
 }
@@ -124,6 +146,15 @@ __global__ __launch_bounds__(256) void layernorm_f32_kernel(const float* __restr
   }
 }
 
+template <int NC>
+hipError_t launch_ln(const uint16_t* x, int64_t x_stride, const float* xcls, int tokens,
+                     uint16_t* out, int64_t rows, int d, const float* g, const float* b, float eps,
+                     hipStream_t s) {
+  hipLaunchKernelGGL(layernorm_bf16_kernel<NC>, dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s,
+                     x, x_stride, xcls, tokens, out, rows, d, g, b, eps);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, const float* xcls, int tokens,
@@ -131,11 +162,16 @@ hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, const float* x
                                  float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (xcls != nullptr && tokens < 1) return hipErrorInvalidValue;
-  const int64_t blocks = (rows + 3) / 4;
-  hipLaunchKernelGGL(layernorm_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(x), x_stride, xcls, tokens,
-                     static_cast<uint16_t*>(out), rows, d, g, b, eps);
-  return hipGetLastError();
+  if ((d & 7) != 0 || d > 8 * 32 * kMaxChunks) return hipErrorInvalidValue;
+  const uint16_t* xp = static_cast<const uint16_t*>(x);
+  uint16_t* op = static_cast<uint16_t*>(out);
+  switch ((d + 255) / 256) {
+    case 1: return launch_ln<1>(xp, x_stride, xcls, tokens, op, rows, d, g, b, eps, s);
+    case 2: return launch_ln<2>(xp, x_stride, xcls, tokens, op, rows, d, g, b, eps, s);
+    case 3: return launch_ln<3>(xp, x_stride, xcls, tokens, op, rows, d, g, b, eps, s);
+    case 4: return launch_ln<4>(xp, x_stride, xcls, tokens, op, rows, d, g, b, eps, s);
+    default: return launch_ln<kMaxChunks>(xp, x_stride, xcls, tokens, op, rows, d, g, b, eps, s);
+  }
 }
 
 hipError_t launch_layernorm_f32(const void* x, int64_t x_stride, void* out, int64_t rows, int d,

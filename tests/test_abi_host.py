@@ -163,3 +163,21 @@ def test_bf16_rounding_agrees_with_numpy_rne(lib):
     w["head_w"].reshape(-1)[special.size:special.size + 100] = rng.standard_normal(100) * 1e3
     buf = ffi.pack_weights(cfg, w, inputs.make_dn_table(cfg))
     np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W), inputs.bf16_round(w["head_w"]))
+
+
+def test_op_entry_points_validate_before_any_hip_call(lib):
+    """Shape and alignment checks of the single-kernel entry points return
+    INVALID_ARG without touching the (fake, never dereferenced) pointers."""
+    p16 = ctypes.c_void_p(1 << 20)
+    p8 = ctypes.c_void_p((1 << 20) + 8)
+    f = ctypes.c_float(1e-6)
+    ln = lib.elasto_op_layernorm
+    # bf16 LayerNorm: d and the stride must be multiples of 8, pointers 16-byte aligned
+    assert ln(1, p16, 12, None, 1, p16, 4, 12, p16, p16, f, None) == 1
+    assert ln(1, p16, 772, None, 1, p16, 4, 768, p16, p16, f, None) == 1
+    assert ln(1, p8, 768, None, 1, p16, 4, 768, p16, p16, f, None) == 1
+    assert ln(1, p16, 768, None, 1, p8, 4, 768, p16, p16, f, None) == 1
+    assert ln(1, p16, 768, None, 1, p16, 4, 4096, p16, p16, f, None) == 1   # d > 2048
+    assert ln(0, p16, 768, p16, 197, p16, 4, 768, p16, p16, f, None) == 1   # x_cls needs bf16
+    assert ln(1, p16, 768, p16, 0, p16, 4, 768, p16, p16, f, None) == 1     # tokens >= 1
+    assert lib.elasto_last_error()

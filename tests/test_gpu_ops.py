@@ -28,6 +28,7 @@ def _gpu():
 
 
 @pytest.mark.parametrize("dtype,rows,d", [(BF16, 1000, 768), (BF16, 197, 192), (BF16, 5, 384),
+                                          (BF16, 9, 2048), (BF16, 3, 8),
                                           (FP32, 68, 64), (FP32, 300, 200)])
 def test_layernorm(dtype, rows, d):
     rng = np.random.default_rng(rows + d)
