@@ -44,7 +44,8 @@ typedef enum {
   ELASTO_ERR_OUT_OF_MEMORY = 4, /* device or host allocation failed             */
   ELASTO_ERR_HIP = 5,           /* a HIP runtime call or kernel launch failed   */
   ELASTO_ERR_MODE_RANGE = 6,    /* mode index outside [0, num_modes)            */
-  ELASTO_ERR_BATCH_RANGE = 7    /* batch outside [1, max_batch]                 */
+  ELASTO_ERR_BATCH_RANGE = 7,   /* batch outside [1, max_batch]                 */
+  ELASTO_ERR_INFEASIBLE = 8     /* no DN meets the selection bounds             */
 } elasto_status_t;
 
 /* Arithmetic of the whole path.  BF16: matrices and activations in bf16,
@@ -154,6 +155,49 @@ elasto_status_t elasto_mode_info(elasto_handle_t h, int32_t k, double* flops_per
 /* Device bytes the handle holds: packed weights and activation scratch. */
 elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes,
                                    int64_t* scratch_bytes);
+
+/* ----------------------------------------------- DN selection (Eq. 11) */
+/* Look-up table of the DNs, one entry per mode: each DN is profiled once for
+ * its computational cost, latency, memory footprint and accuracy, and the
+ * table is consulted at run time (Section 5, system monitoring and network
+ * selection).  Arrays are host pointers of num_modes doubles; no entry may be
+ * NaN.  accuracy and power_w may be NULL (no such data). */
+typedef struct {
+  int32_t num_modes;
+  const double* flops;        /* cost of one forward, any fixed unit           */
+  const double* latency_ms;   /* time of one forward                           */
+  const double* memory_bytes; /* device memory the DN needs resident           */
+  const double* accuracy;     /* user-supplied (no trained weights here)       */
+  const double* power_w;      /* power at this cost, from a FLOPs-to-power table */
+} elasto_dn_lut_t;
+
+/* Eq. 11: among the modes with latency_ms <= max_latency_ms,
+ * memory_bytes <= max_memory_bytes, accuracy >= min_accuracy and, when
+ * power_w is given, power_w <= max_power_w, picks the one with the smallest
+ * flops; equal flops go to the lower mode index.  Pass +INFINITY (-INFINITY
+ * for min_accuracy) to leave a bound open; with accuracy == NULL min_accuracy
+ * must be -INFINITY.  *mode = -1 and ELASTO_ERR_INFEASIBLE when no mode meets
+ * the bounds; ELASTO_ERR_INVALID_ARG for a NULL table array, num_modes < 1,
+ * NaN entries or NaN bounds.  Host only: makes no HIP call. */
+elasto_status_t elasto_select_mode(const elasto_dn_lut_t* lut, double max_latency_ms,
+                                   double max_memory_bytes, double min_accuracy,
+                                   double max_power_w, int32_t* mode);
+
+/* Profiles every mode of the handle at the given batch and fills the cost
+ * columns of a selection table (host arrays of num_modes doubles):
+ *   latency_ms[k]   median device time of one forward in mode k over `iters`
+ *                   forwards after `warmup` untimed ones (HIP events on
+ *                   hip_stream; iters in [1, 1000]);
+ *   memory_bytes[k] bytes mode k needs resident at this batch: its active
+ *                   weight matrices, every fp32 vector parameter, and the
+ *                   activation buffers of this batch at the mode's widths;
+ *   flops[k]        FLOPs of one forward of `batch` images in mode k.
+ * images / logits as for elasto_forward.  Synchronises hip_stream, leaves
+ * the handle's mode as it was.  Creates and destroys its own events. */
+elasto_status_t elasto_profile_modes(elasto_handle_t h, const void* images, int32_t batch,
+                                     float* logits, int32_t warmup, int32_t iters,
+                                     void* hip_stream, double* latency_ms,
+                                     double* memory_bytes, double* flops);
 
 /* ------------------------------------------------- host-only layout helpers */
 /* These make no HIP call; they let a CPU-only caller check validation and the

@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for the elastic-ViT forward pass.
+"""fp64 CPU oracle for the elastic-ViT forward pass and the DN selection.
 
 TEST INFRASTRUCTURE ONLY: imported by tests/, __graft_entry__.smoke() and the
 CPU-baseline leg of bench.py, never by the product path.
@@ -6,7 +6,8 @@ CPU-baseline leg of bench.py, never by the product path.
 from .vit import (layer_norm, gelu, softmax_rows, patchify, attention, vit_forward,
                   canonical_params, active_sets, masks, elastic_forward_masked,
                   extract_dense, elastic_forward)
+from .select import select_dn
 
 __all__ = ["layer_norm", "gelu", "softmax_rows", "patchify", "attention", "vit_forward",
            "canonical_params", "active_sets", "masks", "elastic_forward_masked",
-           "extract_dense", "elastic_forward"]
+           "extract_dense", "elastic_forward", "select_dn"]

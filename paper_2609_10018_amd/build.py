@@ -20,7 +20,7 @@ LIB_DIR = os.path.join(HERE, "_lib")
 LIB_PATH = os.path.join(LIB_DIR, "libelasto.so")
 
 SOURCES = ["gemm_bf16.hip", "gemm_f32.hip", "attention.hip", "layernorm.hip", "api.cpp",
-           "layout.cpp"]
+           "layout.cpp", "select.cpp"]
 ARCH = "gfx950"
 
 

@@ -18,6 +18,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -189,6 +190,86 @@ elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes, int
   if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
   if (weight_bytes) *weight_bytes = h->wbytes;
   if (scratch_bytes) *scratch_bytes = h->sbytes;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_profile_modes(elasto_handle_t h, const void* images, int32_t batch,
+                                     float* logits, int32_t warmup, int32_t iters,
+                                     void* hip_stream, double* latency_ms, double* memory_bytes,
+                                     double* flops) {
+  if (!h || !images || !logits || !latency_ms || !memory_bytes || !flops)
+    return fail(ELASTO_ERR_INVALID_ARG, "NULL argument");
+  if (batch < 1 || batch > h->cfg.max_batch)
+    return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
+  if (warmup < 0 || iters < 1 || iters > 1000)
+    return fail(ELASTO_ERR_INVALID_ARG, "warmup must be >= 0 and iters in [1, 1000]");
+  if ((h->cfg.dtype == ELASTO_BF16 && !aligned(images, 16)) || !aligned(images, 4) ||
+      !aligned(logits, 4))
+    return fail(ELASTO_ERR_INVALID_ARG, "misaligned images / logits");
+  const elasto_config_t& c = h->cfg;
+  const Dims& d = h->dims;
+  const int L = c.depth;
+  const int64_t eb = c.dtype == ELASTO_BF16 ? 2 : 4, D = c.dim, rows = (int64_t)batch * d.T;
+  for (int k = 0; k < h->num_modes; ++k) {
+    const int32_t* nh = h->n_heads.data() + (size_t)k * L;
+    const int32_t* nm = h->n_mlp.data() + (size_t)k * L;
+    int64_t vec = 2 * D + (int64_t)d.T * D + 2 * D + c.num_classes;  // patch_b, cls, pos, norm, head_b
+    int64_t hmax = 0, mmax = 0;
+    for (int l = 0; l < L; ++l) {
+      vec += 2 * D + 3 * d.hd * nh[l] + D + 2 * D + nm[l] + D;  // ln1, bqkv, bo, ln2, b1, b2
+      hmax = nh[l] > hmax ? nh[l] : hmax;
+      mmax = nm[l] > mmax ? nm[l] : mmax;
+    }
+    int64_t act = 2 * rows * D * eb                       // residual stream, LN output
+                  + rows * 3 * d.hd * hmax * eb            // q/k/v
+                  + rows * d.hd * hmax * eb                // attention output
+                  + rows * mmax * eb                       // MLP hidden
+                  + (int64_t)batch * D * eb;               // final LN rows
+    if (c.dtype == ELASTO_BF16) act += (int64_t)batch * D * 4;  // fp32 class-token rows
+    memory_bytes[k] = (double)(mode_weight_bytes(c, nh, nm) + vec * 4 + act);
+    flops[k] = mode_flops(c, nh, nm) * batch;
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device) {
+    if (hipSetDevice(h->device) != hipSuccess) return fail(ELASTO_ERR_HIP, "cannot select device %d", h->device);
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  std::vector<hipEvent_t> ev(iters + 1, nullptr);
+  hipError_t e = hipSuccess;
+  elasto_status_t fst = ELASTO_OK;  // status of the forwards
+  for (auto& x : ev)
+    if (e == hipSuccess) e = hipEventCreate(&x);
+  const int saved = h->mode;
+  std::vector<double> ms(iters);
+  for (int k = 0; k < h->num_modes && e == hipSuccess && fst == ELASTO_OK; ++k) {
+    h->mode = k;
+    for (int i = 0; i < warmup && fst == ELASTO_OK; ++i)
+      fst = elasto_forward(h, images, batch, logits, hip_stream);
+    for (int i = 0; i < iters && e == hipSuccess && fst == ELASTO_OK; ++i) {
+      e = hipEventRecord(ev[i], s);
+      if (e == hipSuccess) fst = elasto_forward(h, images, batch, logits, hip_stream);
+      if (e == hipSuccess && fst == ELASTO_OK && i == iters - 1) e = hipEventRecord(ev[iters], s);
+    }
+    if (fst != ELASTO_OK) break;
+    if (e == hipSuccess) e = hipEventSynchronize(ev[iters]);
+    for (int i = 0; i < iters && e == hipSuccess; ++i) {
+      float t = 0.0f;
+      e = hipEventElapsedTime(&t, ev[i], ev[i + 1]);
+      ms[i] = t;
+    }
+    if (e == hipSuccess) {
+      std::vector<double> sorted(ms);
+      std::sort(sorted.begin(), sorted.end());
+      latency_ms[k] = iters % 2 ? sorted[iters / 2]
+                                : 0.5 * (sorted[iters / 2 - 1] + sorted[iters / 2]);
+    }
+  }
+  h->mode = saved;
+  if (fst != ELASTO_OK) (void)hipStreamSynchronize(s);  // drain before the events go
+  for (auto x : ev)
+    if (x) (void)hipEventDestroy(x);
+  if (fst != ELASTO_OK) return fst;  // the forward's own message stays
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "profiling failed: %s", hipGetErrorString(e));
   return ELASTO_OK;
 }
 

@@ -8,6 +8,7 @@ this module raises: there is no CPU fallback.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from typing import Dict, Optional
 
@@ -58,6 +59,12 @@ class Table(ctypes.Structure):
                 ("head_order", c_vp), ("mlp_order", c_vp)]
 
 
+class DNLut(ctypes.Structure):
+    _fields_ = [("num_modes", c_i32), ("flops", ctypes.POINTER(c_f64)),
+                ("latency_ms", ctypes.POINTER(c_f64)), ("memory_bytes", ctypes.POINTER(c_f64)),
+                ("accuracy", ctypes.POINTER(c_f64)), ("power_w", ctypes.POINTER(c_f64))]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -91,6 +98,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                              c_vp, c_i64, c_i32, c_i32, c_vp],
         "elasto_op_attention": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32,
                                 c_f32, c_vp],
+        "elasto_select_mode": [P(DNLut), c_f64, c_f64, c_f64, c_f64, P(c_i32)],
+        "elasto_profile_modes": [c_vp, c_vp, c_i32, c_vp, c_i32, c_i32, c_vp, P(c_f64), P(c_f64),
+                                 P(c_f64)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -216,6 +226,17 @@ class ElasticViT:
         check(self.lib.elasto_mode_info(self.h, int(k), ctypes.byref(f), ctypes.byref(b)))
         return f.value, b.value
 
+    def profile_modes(self, images, logits, warmup: int = 3, iters: int = 10, stream=None):
+        """Per-mode (latency_ms, memory_bytes, flops) arrays at images.shape[0]."""
+        n = self.num_modes
+        lat, mem, fl = (np.zeros(n, dtype=np.float64) for _ in range(3))
+        dp = ctypes.POINTER(c_f64)
+        check(self.lib.elasto_profile_modes(
+            self.h, images.data_ptr(), int(images.shape[0]), logits.data_ptr(), int(warmup),
+            int(iters), _stream_ptr(stream), lat.ctypes.data_as(dp), mem.ctypes.data_as(dp),
+            fl.ctypes.data_as(dp)))
+        return lat, mem, fl
+
     def memory_info(self):
         wb, sb = c_i64(), c_i64()
         check(self.lib.elasto_memory_info(self.h, ctypes.byref(wb), ctypes.byref(sb)))
@@ -262,6 +283,29 @@ def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int,
                                              _stream_ptr(stream)))
 
 
-__all__ = ["ElasticViT", "ElastoError", "load_library", "validate", "packed_bytes",
+def select_mode(flops, latency_ms, memory_bytes, accuracy=None, power_w=None,
+                max_latency_ms=math.inf, max_memory_bytes=math.inf, min_accuracy=-math.inf,
+                max_power_w=math.inf):
+    """Eq. 11 over a DN table (host only).  Returns the mode, or None when no
+    mode meets the bounds."""
+    cols = [np.ascontiguousarray(c, dtype=np.float64) if c is not None else None
+            for c in (flops, latency_ms, memory_bytes, accuracy, power_w)]
+    n = len(cols[0])
+    if any(c is not None and len(c) != n for c in cols):
+        raise ValueError("table columns differ in length")
+    dp = ctypes.POINTER(c_f64)
+    ptr = [c.ctypes.data_as(dp) if c is not None else None for c in cols]
+    lut = DNLut(n, *ptr)
+    k = c_i32(-1)
+    st = load_library().elasto_select_mode(ctypes.byref(lut), float(max_latency_ms),
+                                           float(max_memory_bytes), float(min_accuracy),
+                                           float(max_power_w), ctypes.byref(k))
+    if st == 8:
+        return None
+    check(st)
+    return k.value
+
+
+__all__ = ["ElasticViT", "select_mode", "ElastoError", "load_library", "validate", "packed_bytes",
            "packed_layout", "pack_weights", "op_layernorm", "op_linear", "op_attention",
            "KERNELS", "FP32", "BF16"]
