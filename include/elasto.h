@@ -101,13 +101,27 @@ typedef struct {
  * mlp_order[l]; prefixes of one order make the modes nested (Eq. 8).
  * Mode 0 conventionally is the widest.  ELASTO_ERR_BAD_TABLE unless:
  * depth == cfg.depth, num_modes >= 1, 1 <= n_heads <= heads,
- * 1 <= n_mlp <= mlp_hidden, and every order row is a permutation. */
+ * 1 <= n_mlp <= mlp_hidden, and every order row is a permutation.
+ *
+ * Embedding width (the compress stage also narrows the hidden size of the
+ * LayerNorm and patch-embedding layers, Section 4.1): mode k keeps the first
+ * n_embed[k] channels of embed_order, the same channels in every layer (the
+ * residual stream is shared by all blocks).  Patch embedding, class token and
+ * positions produce only those channels, every LayerNorm normalises over
+ * them (mean and variance over the n_embed[k] active channels), q/k/v and
+ * fc1 read only them, projection and fc2 write only them, and the classifier
+ * reads only them; head_dim and the attention scale stay those of the full
+ * model.  n_embed == NULL keeps all dim channels in every mode, embed_order ==
+ * NULL is the identity.  Needs 1 <= n_embed <= dim (a multiple of 8 on the
+ * BF16 path) and embed_order a permutation of dim. */
 typedef struct {
   int32_t num_modes, depth;
-  const int32_t* n_heads;    /* [num_modes][depth] */
-  const int32_t* n_mlp;      /* [num_modes][depth] */
-  const int32_t* head_order; /* [depth][heads] */
-  const int32_t* mlp_order;  /* [depth][mlp_hidden] */
+  const int32_t* n_heads;     /* [num_modes][depth] */
+  const int32_t* n_mlp;       /* [num_modes][depth] */
+  const int32_t* head_order;  /* [depth][heads] */
+  const int32_t* mlp_order;   /* [depth][mlp_hidden] */
+  const int32_t* n_embed;     /* [num_modes] or NULL */
+  const int32_t* embed_order; /* [dim] or NULL */
 } elasto_dn_table_t;
 
 /* ---------------------------------------------------------------- lifecycle */
@@ -159,7 +173,7 @@ elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes,
 /* ----------------------------------------------- DN selection (Eq. 11) */
 /* Look-up table of the DNs, one entry per mode: each DN is profiled once for
  * its computational cost, latency, memory footprint and accuracy, and the
- * table is consulted at run time (Section 5, system monitoring and network
+ * table is consulted at run time (Section 4.4, system monitoring and network
  * selection).  Arrays are host pointers of num_modes doubles; no entry may be
  * NaN.  accuracy and power_w may be NULL (no such data). */
 typedef struct {
@@ -205,7 +219,9 @@ elasto_status_t elasto_profile_modes(elasto_handle_t h, const void* images, int3
 
 elasto_status_t elasto_validate(const elasto_config_t* cfg, const elasto_dn_table_t* table);
 
-/* Tensor ids of the packed weight image. */
+/* Tensor ids of the packed weight image.  Every axis of length d (embedding
+ * channels) is stored in embed_order: packed channel j is canonical channel
+ * embed_order[j] (e.g. PATCH_W row j, POS column j, WQKV column j, WO row j). */
 typedef enum {
   ELASTO_T_PATCH_W = 0, /* [d][in_chans*P*P], matrix dtype                     */
   ELASTO_T_PATCH_B,     /* [d] fp32                                            */

@@ -3,11 +3,11 @@
 TEST INFRASTRUCTURE ONLY: imported by tests/, __graft_entry__.smoke() and the
 CPU-baseline leg of bench.py, never by the product path.
 """
-from .vit import (layer_norm, gelu, softmax_rows, patchify, attention, vit_forward,
-                  canonical_params, active_sets, masks, elastic_forward_masked,
-                  extract_dense, elastic_forward)
+from .vit import (layer_norm, layer_norm_masked, gelu, softmax_rows, patchify, attention,
+                  vit_forward, canonical_params, active_sets, active_embed, embed_mask, masks,
+                  elastic_forward_masked, extract_dense, elastic_forward)
 from .select import select_dn
 
-__all__ = ["layer_norm", "gelu", "softmax_rows", "patchify", "attention", "vit_forward",
+__all__ = ["layer_norm", "layer_norm_masked", "active_embed", "embed_mask", "gelu", "softmax_rows", "patchify", "attention", "vit_forward",
            "canonical_params", "active_sets", "masks", "elastic_forward_masked",
            "extract_dense", "elastic_forward", "select_dn"]

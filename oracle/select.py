@@ -3,7 +3,7 @@
 TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 CPU-baseline leg of ``bench.py`` may import or run anything in this package.
 
-Section 5 (system monitoring and network selection): every DN is profiled
+Section 4.4 (system monitoring and network selection): every DN is profiled
 once for its cost (FLOPs), latency, memory footprint and accuracy, and the
 values are kept as a look-up table.  At run time the device state gives an
 allowed latency L_d, available memory M_d, a minimum accuracy A_min and a

@@ -27,7 +27,10 @@ per-layer order.  Three formulations live here:
 Readings where the paper is silent (each is listed in the design notes):
 LayerNorm eps 1e-6 with biased variance; exact erf GELU; attention scale
 1/sqrt(d/H) with H the full head count in every mode; a pruned head removes
-its q/k/v output rows and its input columns of the output projection.
+its q/k/v output rows and its input columns of the output projection.  A
+narrower embedding (Section 4.1 also reduces the hidden size of the
+LayerNorm and patch-embedding layers) keeps one set of embedding channels in
+every layer, and each LayerNorm normalises over that set only.
 
 Parity status: pinned (see tests/test_oracle.py) by a textbook ViT built from
 torch CPU fp64 library ops (full width), brute-force matmul / softmax /
@@ -50,6 +53,16 @@ def layer_norm(x: np.ndarray, g: np.ndarray, b: np.ndarray, eps: float) -> np.nd
     mu = x.mean(axis=-1, keepdims=True)
     var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
     return (x - mu) / np.sqrt(var + eps) * g + b
+
+
+def layer_norm_masked(x: np.ndarray, g: np.ndarray, b: np.ndarray, eps: float,
+                      m: np.ndarray) -> np.ndarray:
+    """LayerNorm over the channels where the {0,1} mask m is 1 (mean and biased
+    variance over those channels only); masked-out channels give 0."""
+    n = m.sum()
+    mu = (x * m).sum(axis=-1, keepdims=True) / n
+    var = (((x - mu) * m) ** 2).sum(axis=-1, keepdims=True) / n
+    return ((x - mu) / np.sqrt(var + eps) * g + b) * m
 
 
 def gelu(z: np.ndarray) -> np.ndarray:
@@ -92,13 +105,21 @@ def attention(u: np.ndarray, qkv_w: np.ndarray, qkv_b: np.ndarray,
     return o.transpose(0, 2, 1, 3).reshape(B, T, h * head_dim)
 
 
-def vit_forward(p: Params, images: np.ndarray, head_dim: int, eps: float) -> np.ndarray:
+def vit_forward(p: Params, images: np.ndarray, head_dim: int, eps: float,
+                embed_mask: np.ndarray = None) -> np.ndarray:
     """F1: dense ViT forward in fp64.  Returns logits [B, num_classes].
 
     ``p["layers"]`` is a list of per-layer dicts; each layer may have its own
     head count (rows of qkv_w / (3*head_dim)) and MLP width (rows of fc1_w).
+    With ``embed_mask`` (a {0,1} vector over the d channels) every LayerNorm
+    normalises over the unmasked channels only (F2's form of a narrower
+    embedding); the masked weights themselves are the caller's.
     """
     f = lambda a: np.asarray(a, dtype=np.float64)
+    if embed_mask is None:
+        ln = layer_norm
+    else:
+        ln = lambda x, g, b, e: layer_norm_masked(x, g, b, e, embed_mask)
     x = patchify(f(images), int(f(p["patch_w"]).shape[-1]))
     d = f(p["patch_w"]).shape[0]
     e = x @ f(p["patch_w"]).reshape(d, -1).T + f(p["patch_b"])
@@ -106,13 +127,13 @@ def vit_forward(p: Params, images: np.ndarray, head_dim: int, eps: float) -> np.
     cls = np.broadcast_to(f(p["cls"]), (B, 1, d))
     x = np.concatenate([cls, e], axis=1) + f(p["pos"])
     for lp in p["layers"]:
-        u = layer_norm(x, f(lp["ln1_g"]), f(lp["ln1_b"]), eps)
+        u = ln(x, f(lp["ln1_g"]), f(lp["ln1_b"]), eps)
         o = attention(u, f(lp["qkv_w"]), f(lp["qkv_b"]), head_dim)
         x = x + (o @ f(lp["proj_w"]).T + f(lp["proj_b"]))
-        u = layer_norm(x, f(lp["ln2_g"]), f(lp["ln2_b"]), eps)
+        u = ln(x, f(lp["ln2_g"]), f(lp["ln2_b"]), eps)
         g = gelu(u @ f(lp["fc1_w"]).T + f(lp["fc1_b"]))
         x = x + (g @ f(lp["fc2_w"]).T + f(lp["fc2_b"]))
-    c = layer_norm(x[:, 0], f(p["norm_g"]), f(p["norm_b"]), eps)
+    c = ln(x[:, 0], f(p["norm_g"]), f(p["norm_b"]), eps)
     return c @ f(p["head_w"]).T + f(p["head_b"])
 
 
@@ -135,6 +156,23 @@ def active_sets(table, k: int, layer: int):
             np.asarray(table.mlp_order[layer][:m], dtype=np.int64))
 
 
+def active_embed(table, k: int, dim: int) -> np.ndarray:
+    """Active embedding channels of mode k, in order (all d when the table
+    narrows no embedding)."""
+    order = getattr(table, "embed_order", None)
+    n_embed = getattr(table, "n_embed", None)
+    order = np.arange(dim) if order is None else np.asarray(order, dtype=np.int64)
+    n = dim if n_embed is None else int(n_embed[k])
+    return order[:n]
+
+
+def embed_mask(table, k: int, dim: int) -> np.ndarray:
+    """{0,1} mask over the d embedding channels of mode k."""
+    m = np.zeros(dim)
+    m[active_embed(table, k, dim)] = 1.0
+    return m
+
+
 def masks(table, k: int, layer: int, dim: int, heads: int, mlp_hidden: int):
     """Binary masks of Eqs. 4 and 6 for one layer of mode k.
 
@@ -154,8 +192,26 @@ def masks(table, k: int, layer: int, dim: int, heads: int, mlp_hidden: int):
 
 def elastic_forward_masked(w: Dict[str, np.ndarray], cfg, table, k: int,
                            images: np.ndarray, mask_biases: bool = True) -> np.ndarray:
-    """F2: mode-k logits as M (.) W on the full-width model, then F1 (Eqs. 4, 6)."""
+    """F2: mode-k logits as M (.) W on the full-width model, then F1 (Eqs. 4, 6).
+
+    A narrower embedding masks every embedding channel outside the active set:
+    patch-embedding rows, class token, positions, the input columns of q/k/v
+    and fc1, the output rows of the projection and fc2 (with their biases),
+    the classifier's input columns, and the LayerNorm affine parameters; every
+    LayerNorm then normalises over the active channels only.  Masked channels
+    of the residual stream stay exactly zero.
+    """
     p = canonical_params(w, cfg.depth)
+    me = embed_mask(table, k, cfg.dim)
+    narrow = me.sum() < cfg.dim
+    if narrow:
+        p["patch_w"] = p["patch_w"] * me[:, None, None, None]
+        p["patch_b"] = p["patch_b"] * me
+        p["cls"] = p["cls"] * me
+        p["pos"] = p["pos"] * me[None, :]
+        p["norm_g"] = p["norm_g"] * me
+        p["norm_b"] = p["norm_b"] * me
+        p["head_w"] = p["head_w"] * me[None, :]
     for l, lp in enumerate(p["layers"]):
         mq, mo, m1, m2 = masks(table, k, l, cfg.dim, cfg.heads, cfg.mlp_hidden)
         lp["qkv_w"] = mq[:, None] * lp["qkv_w"]
@@ -165,23 +221,45 @@ def elastic_forward_masked(w: Dict[str, np.ndarray], cfg, table, k: int,
         if mask_biases:
             lp["qkv_b"] = mq * lp["qkv_b"]
             lp["fc1_b"] = m1 * lp["fc1_b"]
-    return vit_forward(p, images, cfg.dim // cfg.heads, cfg.ln_eps)
+        if narrow:
+            lp["qkv_w"] = lp["qkv_w"] * me[None, :]
+            lp["fc1_w"] = lp["fc1_w"] * me[None, :]
+            lp["proj_w"] = me[:, None] * lp["proj_w"]
+            lp["proj_b"] = me * lp["proj_b"]
+            lp["fc2_w"] = me[:, None] * lp["fc2_w"]
+            lp["fc2_b"] = me * lp["fc2_b"]
+            for key in ("ln1_g", "ln1_b", "ln2_g", "ln2_b"):
+                lp[key] = me * lp[key]
+    return vit_forward(p, images, cfg.dim // cfg.heads, cfg.ln_eps,
+                       embed_mask=me if narrow else None)
 
 
 def extract_dense(w: Dict[str, np.ndarray], cfg, table, k: int) -> Params:
     """F3: copy mode k's active sub-blocks, in order, into a smaller dense ViT."""
     p = canonical_params(w, cfg.depth)
     d, hd = cfg.dim, cfg.dim // cfg.heads
+    e = active_embed(table, k, d)
+    p["patch_w"] = p["patch_w"][e].copy()
+    p["patch_b"] = p["patch_b"][e].copy()
+    p["cls"] = p["cls"][e].copy()
+    p["pos"] = p["pos"][:, e].copy()
+    p["norm_g"] = p["norm_g"][e].copy()
+    p["norm_b"] = p["norm_b"][e].copy()
+    p["head_w"] = p["head_w"][:, e].copy()
     for l, lp in enumerate(p["layers"]):
         act_h, act_m = active_sets(table, k, l)
         chans = np.concatenate([np.arange(i * hd, (i + 1) * hd) for i in act_h])
         rows = np.concatenate([chans, d + chans, 2 * d + chans])
-        lp["qkv_w"] = lp["qkv_w"][rows].copy()
+        lp["qkv_w"] = lp["qkv_w"][rows][:, e].copy()
         lp["qkv_b"] = lp["qkv_b"][rows].copy()
-        lp["proj_w"] = lp["proj_w"][:, chans].copy()
-        lp["fc1_w"] = lp["fc1_w"][act_m].copy()
+        lp["proj_w"] = lp["proj_w"][e][:, chans].copy()
+        lp["proj_b"] = lp["proj_b"][e].copy()
+        lp["fc1_w"] = lp["fc1_w"][act_m][:, e].copy()
         lp["fc1_b"] = lp["fc1_b"][act_m].copy()
-        lp["fc2_w"] = lp["fc2_w"][:, act_m].copy()
+        lp["fc2_w"] = lp["fc2_w"][e][:, act_m].copy()
+        lp["fc2_b"] = lp["fc2_b"][e].copy()
+        for key in ("ln1_g", "ln1_b", "ln2_g", "ln2_b"):
+            lp[key] = lp[key][e].copy()
     return p
 
 

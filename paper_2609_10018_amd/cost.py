@@ -23,9 +23,15 @@ def layer_widths(table, k: int):
             np.asarray(table.n_mlp[k], dtype=np.int64))
 
 
+def embed_width(cfg: ModelConfig, table, k: int) -> int:
+    """Active embedding channels of mode k (all d when the table has none)."""
+    n = getattr(table, "n_embed", None)
+    return cfg.dim if n is None else int(n[k])
+
+
 def gemm_flops(cfg: ModelConfig, table, k: int) -> Dict[str, float]:
     """Per-image FLOPs of each contraction kernel class in mode k."""
-    T, d, hd, P = cfg.tokens, cfg.dim, cfg.head_dim, cfg.patch
+    T, d, hd = cfg.tokens, embed_width(cfg, table, k), cfg.head_dim
     h, m = layer_widths(table, k)
     return {
         "patch": 2.0 * cfg.num_patches * cfg.patch_k * d,
@@ -54,7 +60,7 @@ def layernorm_bytes_per_image(cfg: ModelConfig, out_bytes: int = 2) -> float:
 
 def active_weight_elems(cfg: ModelConfig, table, k: int) -> int:
     """Matrix elements a mode-k forward reads (biases and norms excluded)."""
-    d, hd, C = cfg.dim, cfg.head_dim, cfg.num_classes
+    d, hd, C = embed_width(cfg, table, k), cfg.head_dim, cfg.num_classes
     h, m = layer_widths(table, k)
     per_layer = 3 * hd * h * d + d * hd * h + m * d + d * m
     return int(d * cfg.patch_k + per_layer.sum() + C * d)

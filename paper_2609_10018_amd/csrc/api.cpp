@@ -34,6 +34,7 @@ struct elasto_handle_s {
   int device = 0;
   int num_modes = 0;
   std::vector<int32_t> n_heads, n_mlp;  // [num_modes][depth]
+  std::vector<int32_t> n_embed;         // [num_modes] active embedding channels
   int mode = 0;
   uint8_t* dw = nullptr;  // packed weights
   uint8_t* ds = nullptr;  // activation scratch
@@ -102,6 +103,10 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   const size_t nk = (size_t)table->num_modes * cfg->depth;
   h->n_heads.assign(table->n_heads, table->n_heads + nk);
   h->n_mlp.assign(table->n_mlp, table->n_mlp + nk);
+  if (table->n_embed)
+    h->n_embed.assign(table->n_embed, table->n_embed + table->num_modes);
+  else
+    h->n_embed.assign((size_t)table->num_modes, cfg->dim);
 
   std::vector<uint8_t> host;
   try {
@@ -181,8 +186,9 @@ elasto_status_t elasto_mode_info(elasto_handle_t h, int32_t k, double* flops_per
   if (k < 0 || k >= h->num_modes) return fail(ELASTO_ERR_MODE_RANGE, "mode %d outside [0, %d)", k, h->num_modes);
   const int32_t* nh = h->n_heads.data() + (size_t)k * h->cfg.depth;
   const int32_t* nm = h->n_mlp.data() + (size_t)k * h->cfg.depth;
-  if (flops_per_image) *flops_per_image = mode_flops(h->cfg, nh, nm);
-  if (active_weight_bytes) *active_weight_bytes = mode_weight_bytes(h->cfg, nh, nm);
+  const int de = h->n_embed[k];
+  if (flops_per_image) *flops_per_image = mode_flops(h->cfg, nh, nm, de);
+  if (active_weight_bytes) *active_weight_bytes = mode_weight_bytes(h->cfg, nh, nm, de);
   return ELASTO_OK;
 }
 
@@ -209,10 +215,11 @@ elasto_status_t elasto_profile_modes(elasto_handle_t h, const void* images, int3
   const elasto_config_t& c = h->cfg;
   const Dims& d = h->dims;
   const int L = c.depth;
-  const int64_t eb = c.dtype == ELASTO_BF16 ? 2 : 4, D = c.dim, rows = (int64_t)batch * d.T;
+  const int64_t eb = c.dtype == ELASTO_BF16 ? 2 : 4, rows = (int64_t)batch * d.T;
   for (int k = 0; k < h->num_modes; ++k) {
     const int32_t* nh = h->n_heads.data() + (size_t)k * L;
     const int32_t* nm = h->n_mlp.data() + (size_t)k * L;
+    const int64_t D = h->n_embed[k];
     int64_t vec = 2 * D + (int64_t)d.T * D + 2 * D + c.num_classes;  // patch_b, cls, pos, norm, head_b
     int64_t hmax = 0, mmax = 0;
     for (int l = 0; l < L; ++l) {
@@ -226,8 +233,8 @@ elasto_status_t elasto_profile_modes(elasto_handle_t h, const void* images, int3
                   + rows * mmax * eb                       // MLP hidden
                   + (int64_t)batch * D * eb;               // final LN rows
     if (c.dtype == ELASTO_BF16) act += (int64_t)batch * D * 4;  // fp32 class-token rows
-    memory_bytes[k] = (double)(mode_weight_bytes(c, nh, nm) + vec * 4 + act);
-    flops[k] = mode_flops(c, nh, nm) * batch;
+    memory_bytes[k] = (double)(mode_weight_bytes(c, nh, nm, (int)D) + vec * 4 + act);
+    flops[k] = mode_flops(c, nh, nm, (int)D) * batch;
   }
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != h->device) {
@@ -291,15 +298,17 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   const elasto_config_t& c = h->cfg;
   const Dims& d = h->dims;
   const int k = h->mode;
-  const int L = c.depth, D = c.dim, Mh = c.mlp_hidden;
+  // D: row stride of the residual stream; E: its active channels in mode k
+  // (LayerNorm outputs and the class-token rows are stored E wide).
+  const int L = c.depth, D = c.dim, E = h->n_embed[k], Mh = c.mlp_hidden;
   const int64_t rows = (int64_t)batch * d.T;
   auto gemm = bf ? launch_gemm_bf16 : launch_gemm_f32;
   auto attn = bf ? launch_attention_bf16 : launch_attention_f32;
   float* xcls = bf ? h->xcls : nullptr;
   // LayerNorm over all rows of the residual stream.
   auto ln = [&](const float* g, const float* b) {
-    return bf ? launch_layernorm_bf16(h->x, D, xcls, d.T, h->u, rows, D, g, b, c.ln_eps, s)
-              : launch_layernorm_f32(h->x, D, h->u, rows, D, g, b, c.ln_eps, s);
+    return bf ? launch_layernorm_bf16(h->x, D, xcls, d.T, h->u, rows, E, g, b, c.ln_eps, s)
+              : launch_layernorm_f32(h->x, D, h->u, rows, E, g, b, c.ln_eps, s);
   };
   const float scale = 1.0f / sqrtf((float)d.hd);
 
@@ -312,7 +321,7 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     a.ldc = D;
     a.bias = F(h, ELASTO_T_PATCH_B);
     a.M = rows;
-    a.N = D;
+    a.N = E;
     a.K = d.patch_k;
     a.img = images;
     a.img_size = c.img;
@@ -322,6 +331,7 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     a.tokens = d.T;
     a.cls = F(h, ELASTO_T_CLS);
     a.pos = F(h, ELASTO_T_POS);
+    a.ldpos = D;
     a.ccls = xcls;
     e = timed(h, ELASTO_K_PATCH, s, [&] { return gemm(Epi::Patch, a, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "patch embedding: %s", hipGetErrorString(e));
@@ -331,11 +341,11 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN1_G, l), F(h, ELASTO_T_LN1_B, l)); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs q;
-    q.A = h->u; q.lda = D;
+    q.A = h->u; q.lda = E;
     q.W = W(h, ELASTO_T_WQKV, l); q.ldw = D;
     q.C = h->qkv; q.ldc = 3 * D;
     q.bias = F(h, ELASTO_T_BQKV, l);
-    q.M = rows; q.N = 3 * d.hd * hh; q.K = D;
+    q.M = rows; q.N = 3 * d.hd * hh; q.K = E;
     e = timed(h, ELASTO_K_QKV, s, [&] { return gemm(Epi::Bias, q, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "qkv layer %d: %s", l, hipGetErrorString(e));
     AttnArgs at;
@@ -351,17 +361,17 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     pr.bias = F(h, ELASTO_T_BO, l);
     pr.ccls = xcls;
     pr.tokens = d.T;
-    pr.M = rows; pr.N = D; pr.K = d.hd * hh;
+    pr.M = rows; pr.N = E; pr.K = d.hd * hh;
     e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
     e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l)); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln2 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f1;
-    f1.A = h->u; f1.lda = D;
+    f1.A = h->u; f1.lda = E;
     f1.W = W(h, ELASTO_T_W1, l); f1.ldw = D;
     f1.C = h->g; f1.ldc = Mh;
     f1.bias = F(h, ELASTO_T_B1, l);
-    f1.M = rows; f1.N = mm; f1.K = D;
+    f1.M = rows; f1.N = mm; f1.K = E;
     e = timed(h, ELASTO_K_FC1, s, [&] { return gemm(Epi::BiasGelu, f1, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f2;
@@ -371,24 +381,24 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     f2.bias = F(h, ELASTO_T_B2, l);
     f2.ccls = xcls;
     f2.tokens = d.T;
-    f2.M = rows; f2.N = D; f2.K = mm;
+    f2.M = rows; f2.N = E; f2.K = mm;
     e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
   }
   // Final norm on the class-token rows only.
   e = timed(h, ELASTO_K_LN, s, [&] {
-    return bf ? launch_layernorm_bf16(xcls, D, xcls, 1, h->ucls, batch, D, F(h, ELASTO_T_NORM_G),
+    return bf ? launch_layernorm_bf16(xcls, E, xcls, 1, h->ucls, batch, E, F(h, ELASTO_T_NORM_G),
                                       F(h, ELASTO_T_NORM_B), c.ln_eps, s)
-              : launch_layernorm_f32(h->x, (int64_t)d.T * D, h->ucls, batch, D,
+              : launch_layernorm_f32(h->x, (int64_t)d.T * D, h->ucls, batch, E,
                                      F(h, ELASTO_T_NORM_G), F(h, ELASTO_T_NORM_B), c.ln_eps, s);
   });
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "final norm: %s", hipGetErrorString(e));
   GemmArgs hg;
-  hg.A = h->ucls; hg.lda = D;
+  hg.A = h->ucls; hg.lda = E;
   hg.W = W(h, ELASTO_T_HEAD_W); hg.ldw = D;
   hg.C = logits; hg.ldc = c.num_classes;
   hg.bias = F(h, ELASTO_T_HEAD_B);
-  hg.M = batch; hg.N = c.num_classes; hg.K = D;
+  hg.M = batch; hg.N = c.num_classes; hg.K = E;
   e = timed(h, ELASTO_K_HEAD, s, [&] { return gemm(Epi::BiasF32, hg, s); });
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "head: %s", hipGetErrorString(e));
   return ELASTO_OK;
@@ -439,7 +449,8 @@ elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, 
   const elasto_config_t& c = h->cfg;
   const Dims& d = h->dims;
   const double eb = c.dtype == ELASTO_BF16 ? 2.0 : 4.0;
-  const double B = batch, T = d.T, D = c.dim, hd = d.hd, Np = (double)d.grid * d.grid;
+  // D: active embedding channels of mode k.
+  const double B = batch, T = d.T, D = h->n_embed[k], hd = d.hd, Np = (double)d.grid * d.grid;
   const double Mr = B * T;
   double f = 0, by = 0;
   int n = 0;

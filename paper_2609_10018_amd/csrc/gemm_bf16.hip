@@ -51,6 +51,7 @@ struct Params {
   int img_size, patch, chans, grid, tokens;
   const float* cls;
   const float* pos;
+  int64_t ldpos;
   float* ccls;
   int row0;     // this launch covers rows [row0, M)
   int tiles_n;
@@ -345,7 +346,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         }
       } else {  // Patch: class rows (t == 0) take cls + pos[0] and drop the product
         const int t = row % p.tokens;
-        const float* pp = p.pos + (int64_t)t * p.N + col;
+        const float* pp = p.pos + (int64_t)t * p.ldpos + col;
         if (full) {
           const f32x4 p0 = *reinterpret_cast<const f32x4*>(pp);
           const f32x4 p1 = *reinterpret_cast<const f32x4*>(pp + 4);
@@ -468,6 +469,7 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.tokens = a.tokens;
   p.cls = a.cls;
   p.pos = a.pos;
+  p.ldpos = a.ldpos > 0 ? a.ldpos : a.N;
   p.ccls = a.ccls;
   switch (epi) {
     case Epi::Bias: return launch_epi<Epi::Bias>(p, s);

@@ -23,6 +23,7 @@ struct P32 {
   int img_size, patch, chans, grid, tokens;
   const float* cls;
   const float* pos;
+  int64_t ldpos;
 };
 
 template <Epi E>
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(P32 p) {
         *c = *c + (v + bv);
       } else {
         const int t = (int)(row % p.tokens);
-        *c = v + (t == 0 ? p.cls[col] : bv) + p.pos[(int64_t)t * p.N + col];
+        *c = v + (t == 0 ? p.cls[col] : bv) + p.pos[(int64_t)t * p.ldpos + col];
       }
     }
   }
@@ -136,6 +137,7 @@ hipError_t launch_gemm_f32(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.tokens = a.tokens;
   p.cls = a.cls;
   p.pos = a.pos;
+  p.ldpos = a.ldpos > 0 ? a.ldpos : a.N;
   switch (epi) {
     case Epi::Bias: return launch<Epi::Bias>(p, s);
     case Epi::BiasGelu: return launch<Epi::BiasGelu>(p, s);

@@ -36,6 +36,7 @@ struct GemmArgs {
   int img_size = 0, patch = 0, chans = 0, grid = 0, tokens = 0;
   const float* cls = nullptr;
   const float* pos = nullptr;
+  int64_t ldpos = 0;  // row stride of pos (elements); 0: N
   float* ccls = nullptr;
 };
 

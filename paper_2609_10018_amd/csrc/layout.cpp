@@ -7,6 +7,8 @@
 //   WO   column s*hd + c       = proj_w column head_order[s]*hd + c
 //   W1   row s                 = fc1_w row mlp_order[s]
 //   W2   column s              = fc2_w column mlp_order[s]
+// and every embedding axis (length d) in embed_order: packed channel j is
+// canonical channel embed_order[j] (identity when the table gives none).
 // Matrices are stored in the path's dtype (bf16 rounded to nearest even, or
 // fp32); biases, norms, class token and positions stay fp32.
 #include "layout.h"
@@ -114,7 +116,22 @@ bool check_table(const elasto_config_t* c, const elasto_dn_table_t* t) {
       if (h < 1 || h > c->heads) { set_error("n_heads[%d][%d] = %d outside [1, %d]", k, l, h, c->heads); return false; }
       if (m < 1 || m > c->mlp_hidden) { set_error("n_mlp[%d][%d] = %d outside [1, %d]", k, l, m, c->mlp_hidden); return false; }
     }
+  if (t->n_embed) {
+    for (int k = 0; k < t->num_modes; ++k) {
+      const int e = t->n_embed[k];
+      if (e < 1 || e > c->dim) { set_error("n_embed[%d] = %d outside [1, %d]", k, e, c->dim); return false; }
+      if (c->dtype == ELASTO_BF16 && e % 8 != 0) { set_error("n_embed[%d] = %d is not a multiple of 8 (bf16)", k, e); return false; }
+    }
+  }
   std::vector<char> seen;
+  if (t->embed_order) {
+    seen.assign(c->dim, 0);
+    for (int j = 0; j < c->dim; ++j) {
+      const int v = t->embed_order[j];
+      if (v < 0 || v >= c->dim || seen[v]) { set_error("embed_order is not a permutation"); return false; }
+      seen[v] = 1;
+    }
+  }
   for (int l = 0; l < t->depth; ++l) {
     seen.assign(c->heads, 0);
     for (int s = 0; s < c->heads; ++s) {
@@ -214,29 +231,36 @@ void pack(const elasto_config_t& c, const elasto_weights_t& w, const elasto_dn_t
   const Dims d = dims_of(c);
   const int64_t D = c.dim, M = c.mlp_hidden, C = c.num_classes, H = c.heads, hd = d.hd;
   const Writer wr{dst, c.dtype == ELASTO_BF16};
+  // ev[j]: canonical embedding channel stored at packed position j.
+  std::vector<int64_t> ev(D);
+  for (int64_t j = 0; j < D; ++j) ev[j] = t.embed_order ? t.embed_order[j] : j;
   auto g = [&](int id) { return L.get(id, 0).offset; };
-  for (int64_t i = 0; i < D * d.patch_k; ++i) wr.mat(g(ELASTO_T_PATCH_W), i, w.patch_w[i]);
-  for (int64_t i = 0; i < D; ++i) {
-    wr.vec(g(ELASTO_T_PATCH_B), i, w.patch_b[i]);
-    wr.vec(g(ELASTO_T_CLS), i, w.cls[i]);
-    wr.vec(g(ELASTO_T_NORM_G), i, w.norm_g[i]);
-    wr.vec(g(ELASTO_T_NORM_B), i, w.norm_b[i]);
+  for (int64_t j = 0; j < D; ++j) {
+    for (int64_t k = 0; k < d.patch_k; ++k)
+      wr.mat(g(ELASTO_T_PATCH_W), j * d.patch_k + k, w.patch_w[ev[j] * d.patch_k + k]);
+    wr.vec(g(ELASTO_T_PATCH_B), j, w.patch_b[ev[j]]);
+    wr.vec(g(ELASTO_T_CLS), j, w.cls[ev[j]]);
+    wr.vec(g(ELASTO_T_NORM_G), j, w.norm_g[ev[j]]);
+    wr.vec(g(ELASTO_T_NORM_B), j, w.norm_b[ev[j]]);
   }
-  for (int64_t i = 0; i < (int64_t)d.T * D; ++i) wr.vec(g(ELASTO_T_POS), i, w.pos[i]);
-  for (int64_t i = 0; i < C * D; ++i) wr.mat(g(ELASTO_T_HEAD_W), i, w.head_w[i]);
+  for (int64_t tk = 0; tk < d.T; ++tk)
+    for (int64_t j = 0; j < D; ++j) wr.vec(g(ELASTO_T_POS), tk * D + j, w.pos[tk * D + ev[j]]);
+  for (int64_t n = 0; n < C; ++n)
+    for (int64_t j = 0; j < D; ++j) wr.mat(g(ELASTO_T_HEAD_W), n * D + j, w.head_w[n * D + ev[j]]);
   for (int64_t i = 0; i < C; ++i) wr.vec(g(ELASTO_T_HEAD_B), i, w.head_b[i]);
 
   for (int l = 0; l < c.depth; ++l) {
     auto o = [&](int id) { return L.get(id, l).offset; };
     const int32_t* ho = t.head_order + (int64_t)l * H;
     const int32_t* mo = t.mlp_order + (int64_t)l * M;
-    for (int64_t i = 0; i < D; ++i) {
-      wr.vec(o(ELASTO_T_LN1_G), i, w.ln1_g[l * D + i]);
-      wr.vec(o(ELASTO_T_LN1_B), i, w.ln1_b[l * D + i]);
-      wr.vec(o(ELASTO_T_LN2_G), i, w.ln2_g[l * D + i]);
-      wr.vec(o(ELASTO_T_LN2_B), i, w.ln2_b[l * D + i]);
-      wr.vec(o(ELASTO_T_BO), i, w.proj_b[l * D + i]);
-      wr.vec(o(ELASTO_T_B2), i, w.fc2_b[l * D + i]);
+    for (int64_t j = 0; j < D; ++j) {
+      const int64_t i = ev[j];
+      wr.vec(o(ELASTO_T_LN1_G), j, w.ln1_g[l * D + i]);
+      wr.vec(o(ELASTO_T_LN1_B), j, w.ln1_b[l * D + i]);
+      wr.vec(o(ELASTO_T_LN2_G), j, w.ln2_g[l * D + i]);
+      wr.vec(o(ELASTO_T_LN2_B), j, w.ln2_b[l * D + i]);
+      wr.vec(o(ELASTO_T_BO), j, w.proj_b[l * D + i]);
+      wr.vec(o(ELASTO_T_B2), j, w.fc2_b[l * D + i]);
     }
     const float* qkv_w = w.qkv_w + (int64_t)l * 3 * D * D;
     const float* qkv_b = w.qkv_b + (int64_t)l * 3 * D;
@@ -245,42 +269,44 @@ void pack(const elasto_config_t& c, const elasto_weights_t& w, const elasto_dn_t
         for (int64_t c2 = 0; c2 < hd; ++c2) {
           const int64_t dst_row = s * 3 * hd + tq * hd + c2;
           const int64_t src_row = tq * D + (int64_t)ho[s] * hd + c2;
-          for (int64_t k = 0; k < D; ++k) wr.mat(o(ELASTO_T_WQKV), dst_row * D + k, qkv_w[src_row * D + k]);
+          for (int64_t j = 0; j < D; ++j)
+            wr.mat(o(ELASTO_T_WQKV), dst_row * D + j, qkv_w[src_row * D + ev[j]]);
           wr.vec(o(ELASTO_T_BQKV), dst_row, qkv_b[src_row]);
         }
     const float* proj_w = w.proj_w + (int64_t)l * D * D;
-    for (int64_t n = 0; n < D; ++n)
+    for (int64_t j = 0; j < D; ++j)
       for (int64_t s = 0; s < H; ++s)
         for (int64_t c2 = 0; c2 < hd; ++c2)
-          wr.mat(o(ELASTO_T_WO), n * D + s * hd + c2, proj_w[n * D + (int64_t)ho[s] * hd + c2]);
+          wr.mat(o(ELASTO_T_WO), j * D + s * hd + c2, proj_w[ev[j] * D + (int64_t)ho[s] * hd + c2]);
     const float* fc1_w = w.fc1_w + (int64_t)l * M * D;
     const float* fc1_b = w.fc1_b + (int64_t)l * M;
     for (int64_t s = 0; s < M; ++s) {
-      for (int64_t k = 0; k < D; ++k) wr.mat(o(ELASTO_T_W1), s * D + k, fc1_w[(int64_t)mo[s] * D + k]);
+      for (int64_t j = 0; j < D; ++j) wr.mat(o(ELASTO_T_W1), s * D + j, fc1_w[(int64_t)mo[s] * D + ev[j]]);
       wr.vec(o(ELASTO_T_B1), s, fc1_b[mo[s]]);
     }
     const float* fc2_w = w.fc2_w + (int64_t)l * D * M;
-    for (int64_t n = 0; n < D; ++n)
-      for (int64_t s = 0; s < M; ++s) wr.mat(o(ELASTO_T_W2), n * M + s, fc2_w[n * M + mo[s]]);
+    for (int64_t j = 0; j < D; ++j)
+      for (int64_t s = 0; s < M; ++s) wr.mat(o(ELASTO_T_W2), j * M + s, fc2_w[ev[j] * M + mo[s]]);
   }
 }
 
-double mode_flops(const elasto_config_t& c, const int32_t* nh, const int32_t* nm) {
+double mode_flops(const elasto_config_t& c, const int32_t* nh, const int32_t* nm, int embed) {
   const Dims d = dims_of(c);
-  const double T = d.T, D = c.dim, hd = d.hd, Np = (double)d.grid * d.grid;
-  double f = 2.0 * Np * d.patch_k * D + 2.0 * D * c.num_classes;
+  const double T = d.T, E = embed, hd = d.hd, Np = (double)d.grid * d.grid;
+  double f = 2.0 * Np * d.patch_k * E + 2.0 * E * c.num_classes;
   for (int l = 0; l < c.depth; ++l) {
     const double h = nh[l], m = nm[l];
-    f += 2.0 * T * (4.0 * hd * h * D + 2.0 * D * m) + 2.0 * 2.0 * T * T * hd * h;
+    f += 2.0 * T * (4.0 * hd * h * E + 2.0 * E * m) + 2.0 * 2.0 * T * T * hd * h;
   }
   return f;
 }
 
-int64_t mode_weight_bytes(const elasto_config_t& c, const int32_t* nh, const int32_t* nm) {
+int64_t mode_weight_bytes(const elasto_config_t& c, const int32_t* nh, const int32_t* nm,
+                          int embed) {
   const Dims d = dims_of(c);
-  const int64_t me = c.dtype == ELASTO_BF16 ? 2 : 4, D = c.dim, hd = d.hd;
-  int64_t e = D * d.patch_k + (int64_t)c.num_classes * D;
-  for (int l = 0; l < c.depth; ++l) e += 4 * hd * nh[l] * D + 2 * D * (int64_t)nm[l];
+  const int64_t me = c.dtype == ELASTO_BF16 ? 2 : 4, E = embed, hd = d.hd;
+  int64_t e = E * d.patch_k + (int64_t)c.num_classes * E;
+  for (int l = 0; l < c.depth; ++l) e += 4 * hd * nh[l] * E + 2 * E * (int64_t)nm[l];
   return e * me;
 }
 

@@ -46,9 +46,12 @@ void set_error(const char* fmt, ...);
 void clear_error();
 elasto_status_t fail(elasto_status_t st, const char* fmt, ...);
 
-// Per-image FLOPs of mode k (2 x MACs of every contraction).
-double mode_flops(const elasto_config_t& cfg, const int32_t* n_heads_k, const int32_t* n_mlp_k);
+// Per-image FLOPs of a mode (2 x MACs of every contraction) with per-layer
+// head / unit counts and embed active embedding channels.
+double mode_flops(const elasto_config_t& cfg, const int32_t* n_heads_k, const int32_t* n_mlp_k,
+                  int embed);
+// Bytes of the weight matrices the mode reads.
 int64_t mode_weight_bytes(const elasto_config_t& cfg, const int32_t* n_heads_k,
-                          const int32_t* n_mlp_k);
+                          const int32_t* n_mlp_k, int embed);
 
 }  // namespace elasto

@@ -1,4 +1,4 @@
-// DN selection of Eq. 11 (Section 5, system monitoring and network
+// DN selection of Eq. 11 (Section 4.4, system monitoring and network
 // selection): the cheapest DN, by its table cost, that meets the latency,
 // memory, accuracy and power bounds.  Host only.
 #include <math.h>

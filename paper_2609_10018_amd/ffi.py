@@ -56,7 +56,8 @@ class Weights(ctypes.Structure):
 
 class Table(ctypes.Structure):
     _fields_ = [("num_modes", c_i32), ("depth", c_i32), ("n_heads", c_vp), ("n_mlp", c_vp),
-                ("head_order", c_vp), ("mlp_order", c_vp)]
+                ("head_order", c_vp), ("mlp_order", c_vp), ("n_embed", c_vp),
+                ("embed_order", c_vp)]
 
 
 class DNLut(ctypes.Structure):
@@ -135,11 +136,17 @@ class _HostWeights:
 
 
 class _HostTable:
+    """Keeps int32 copies alive while the C struct points at them; the
+    embedding columns are optional (None: every mode keeps all channels,
+    identity order)."""
+
     def __init__(self, t: DNTable):
-        self.arrays = [np.ascontiguousarray(a, dtype=np.int32)
-                       for a in (t.n_heads, t.n_mlp, t.head_order, t.mlp_order)]
+        cols = (t.n_heads, t.n_mlp, t.head_order, t.mlp_order,
+                getattr(t, "n_embed", None), getattr(t, "embed_order", None))
+        self.arrays = [None if a is None else np.ascontiguousarray(a, dtype=np.int32)
+                       for a in cols]
         self.struct = Table(int(t.n_heads.shape[0]), int(t.n_heads.shape[1]),
-                            *[a.ctypes.data for a in self.arrays])
+                            *[None if a is None else a.ctypes.data for a in self.arrays])
 
 
 def validate(cfg: ModelConfig, table: DNTable, max_batch: int = 1) -> int:

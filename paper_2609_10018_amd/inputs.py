@@ -22,7 +22,7 @@ permutation stands in for it: it exercises the same permuted-prefix storage.
 from __future__ import annotations
 
 import dataclasses
-from typing import Dict, List
+from typing import Dict, List, Optional
 
 import numpy as np
 
@@ -79,14 +79,22 @@ CONFIGS: Dict[str, ModelConfig] = {
     "vit_ti": ModelConfig("vit_ti", 224, 16, 3, 192, 12, 3, 768, 1000, BF16, 64),
     "vit_s": ModelConfig("vit_s", 224, 16, 3, 384, 12, 6, 1536, 1000, BF16, 128),
     "vit_b": ModelConfig("vit_b", 224, 16, 3, 768, 12, 12, 3072, 1000, BF16, 256),
+    # Same shapes with modes that also narrow the embedding width.
+    "tiny_emb": ModelConfig("tiny_emb", 32, 8, 3, 64, 2, 2, 128, 10, FP32, 4),
+    "vit_ti_emb": ModelConfig("vit_ti_emb", 224, 16, 3, 192, 12, 3, 768, 1000, BF16, 32),
+    "vit_b_emb": ModelConfig("vit_b_emb", 224, 16, 3, 768, 12, 12, 3072, 1000, BF16, 256),
 }
 
-# Per-mode (heads, MLP hidden) caps; mode 0 is full width, larger k is smaller.
+# Per-mode (heads, MLP hidden[, embedding width]) caps; mode 0 is full width,
+# larger k is smaller.  Without a third entry every mode keeps all d channels.
 MODE_CAPS: Dict[str, List[tuple]] = {
     "tiny": [(2, 128), (1, 64)],
     "vit_ti": [(3, 768), (2, 576), (1, 384), (1, 192)],
     "vit_s": [(6, 1536), (5, 1152), (4, 768), (3, 384), (2, 230)],
     "vit_b": [(12, 3072), (9, 2304), (6, 1536), (3, 768), (2, 460)],
+    "tiny_emb": [(2, 128, 64), (2, 96, 48), (1, 64, 24)],
+    "vit_ti_emb": [(3, 768, 192), (2, 576, 144), (1, 384, 96), (1, 192, 64)],
+    "vit_b_emb": [(12, 3072, 768), (9, 2304, 576), (6, 1536, 384), (3, 768, 192)],
 }
 # Configs whose per-layer widths follow a per-layer keep ratio r_l ~ U[0.15, 1].
 LAYER_RATIO_CONFIGS = ("vit_s",)
@@ -166,6 +174,8 @@ class DNTable:
     n_mlp: np.ndarray        # int32 [num_modes, depth]
     head_order: np.ndarray   # int32 [depth, heads], a permutation per layer
     mlp_order: np.ndarray    # int32 [depth, mlp_hidden], a permutation per layer
+    n_embed: Optional[np.ndarray] = None      # int32 [num_modes]; None: all d channels
+    embed_order: Optional[np.ndarray] = None  # int32 [dim], shared by all layers; None: identity
 
     @property
     def num_modes(self) -> int:
@@ -182,7 +192,8 @@ def make_dn_table(cfg: ModelConfig, seed: int = ORDER_SEED) -> DNTable:
     n_heads = np.zeros((len(caps), L), dtype=np.int32)
     n_mlp = np.zeros((len(caps), L), dtype=np.int32)
     ratios = layer_ratios(cfg) if cfg.name in LAYER_RATIO_CONFIGS else None
-    for k, (hk, mk) in enumerate(caps):
+    for k, cap in enumerate(caps):
+        hk, mk = cap[0], cap[1]
         for l in range(L):
             if ratios is None or k == 0:
                 n_heads[k, l], n_mlp[k, l] = hk, mk
@@ -192,7 +203,9 @@ def make_dn_table(cfg: ModelConfig, seed: int = ORDER_SEED) -> DNTable:
     rng = np.random.default_rng(seed)
     head_order = np.stack([rng.permutation(cfg.heads) for _ in range(L)]).astype(np.int32)
     mlp_order = np.stack([rng.permutation(cfg.mlp_hidden) for _ in range(L)]).astype(np.int32)
-    return DNTable(n_heads, n_mlp, head_order, mlp_order)
+    embed_order = rng.permutation(cfg.dim).astype(np.int32)
+    n_embed = np.array([cap[2] if len(cap) > 2 else cfg.dim for cap in caps], dtype=np.int32)
+    return DNTable(n_heads, n_mlp, head_order, mlp_order, n_embed, embed_order)
 
 
 def mode_sequence(n: int, num_modes: int, seed: int = SEQUENCE_SEED) -> np.ndarray:

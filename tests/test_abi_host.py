@@ -32,7 +32,8 @@ def test_library_exports_every_declared_function(lib):
 
 
 def _table_copy(t):
-    return DNTable(t.n_heads.copy(), t.n_mlp.copy(), t.head_order.copy(), t.mlp_order.copy())
+    return DNTable(t.n_heads.copy(), t.n_mlp.copy(), t.head_order.copy(), t.mlp_order.copy(),
+                   t.n_embed.copy(), t.embed_order.copy())
 
 
 @pytest.mark.parametrize("name", list(CONFIGS))
@@ -53,6 +54,10 @@ def test_bad_tables_rejected(lib):
     t = _table_copy(base); t.mlp_order[0, 7] = cfg.mlp_hidden; bad.append(t)
     t = DNTable(base.n_heads[:, :5].copy(), base.n_mlp[:, :5].copy(), base.head_order[:5].copy(),
                 base.mlp_order[:5].copy()); bad.append(t)
+    t = _table_copy(base); t.n_embed[1] = 0; bad.append(t)
+    t = _table_copy(base); t.n_embed[1] = cfg.dim + 8; bad.append(t)
+    t = _table_copy(base); t.n_embed[2] = 100; bad.append(t)          # bf16: not a multiple of 8
+    t = _table_copy(base); t.embed_order[3] = t.embed_order[4]; bad.append(t)
     for t in bad:
         assert ffi.validate(cfg, t, 4) == 3, ffi.last_error()
         assert ffi.last_error()
@@ -105,7 +110,7 @@ def _view(buf, cfg, tensor, layer=0):
     return buf[off:off + rows * cols * 4].view(np.float32).reshape(rows, cols)
 
 
-@pytest.mark.parametrize("name", ["tiny", "vit_ti"])
+@pytest.mark.parametrize("name", ["tiny", "vit_ti", "vit_ti_emb"])
 def test_pack_equals_numpy_gather(lib, name):
     cfg = CONFIGS[name]
     w = inputs.make_weights(cfg)
@@ -113,27 +118,34 @@ def test_pack_equals_numpy_gather(lib, name):
     buf = ffi.pack_weights(cfg, w, t)
     sw = inputs.stored_weights(cfg, w)      # bf16-rounded matrices on the bf16 path
     d, hd, H = cfg.dim, cfg.head_dim, cfg.heads
-    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_PATCH_W), sw["patch_w"].reshape(d, -1))
-    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_POS), sw["pos"])
-    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W), sw["head_w"])
-    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_CLS)[0], sw["cls"])
+    ev = t.embed_order                      # packed embedding channel j = canonical ev[j]
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_PATCH_W), sw["patch_w"].reshape(d, -1)[ev])
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_POS), sw["pos"][:, ev])
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W), sw["head_w"][:, ev])
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_CLS)[0], sw["cls"][ev])
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_NORM_G)[0], sw["norm_g"][ev])
     for l in range(cfg.depth):
         ho, mo = t.head_order[l], t.mlp_order[l]
         rows = np.array([tq * d + ho[s] * hd + c for s in range(H) for tq in range(3)
                          for c in range(hd)])
-        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_WQKV, l), sw["qkv_w"][l][rows])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_WQKV, l), sw["qkv_w"][l][rows][:, ev])
         np.testing.assert_array_equal(_view(buf, cfg, ffi.T_BQKV, l)[0], sw["qkv_b"][l][rows])
         cols = np.array([ho[s] * hd + c for s in range(H) for c in range(hd)])
-        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_WO, l), sw["proj_w"][l][:, cols])
-        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W1, l), sw["fc1_w"][l][mo])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_WO, l), sw["proj_w"][l][ev][:, cols])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_BO, l)[0], sw["proj_b"][l][ev])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W1, l), sw["fc1_w"][l][mo][:, ev])
         np.testing.assert_array_equal(_view(buf, cfg, ffi.T_B1, l)[0], sw["fc1_b"][l][mo])
-        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W2, l), sw["fc2_w"][l][:, mo])
-        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_LN2_G, l)[0], sw["ln2_g"][l])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W2, l), sw["fc2_w"][l][ev][:, mo])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_B2, l)[0], sw["fc2_b"][l][ev])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_LN1_B, l)[0], sw["ln1_b"][l][ev])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_LN2_G, l)[0], sw["ln2_g"][l][ev])
 
 
-def test_packed_prefix_is_what_mode_k_reads(lib):
-    """The first n rows of WQKV / W1 are exactly mode k's active heads / units."""
-    cfg = CONFIGS["vit_ti"]
+@pytest.mark.parametrize("name", ["vit_ti", "vit_ti_emb"])
+def test_packed_prefix_is_what_mode_k_reads(lib, name):
+    """The first n rows of WQKV / W1 are exactly mode k's active heads / units,
+    and the first n_embed[k] embedding positions its active channels."""
+    cfg = CONFIGS[name]
     w = inputs.make_weights(cfg)
     t = inputs.make_dn_table(cfg)
     buf = ffi.pack_weights(cfg, w, t)
@@ -141,15 +153,22 @@ def test_packed_prefix_is_what_mode_k_reads(lib):
     import oracle
     for k in range(t.num_modes):
         p = oracle.extract_dense(sw, cfg, t, k)
+        E = int(t.n_embed[k])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_PATCH_W)[:E],
+                                      p["patch_w"].reshape(E, -1))
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_POS)[:, :E], p["pos"])
+        np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W)[:, :E], p["head_w"])
         for l in range(cfg.depth):
             h, m = int(t.n_heads[k, l]), int(t.n_mlp[k, l])
-            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W1, l)[:m], p["layers"][l]["fc1_w"])
-            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W2, l)[:, :m], p["layers"][l]["fc2_w"])
-            wo = _view(buf, cfg, ffi.T_WO, l)[:, :h * cfg.head_dim]
-            np.testing.assert_array_equal(wo, p["layers"][l]["proj_w"])
-            packed_q = _view(buf, cfg, ffi.T_WQKV, l)[:3 * cfg.head_dim * h]
-            pq = packed_q.reshape(h, 3, cfg.head_dim, cfg.dim).transpose(1, 0, 2, 3)
-            np.testing.assert_array_equal(pq.reshape(-1, cfg.dim), p["layers"][l]["qkv_w"])
+            lp = p["layers"][l]
+            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W1, l)[:m, :E], lp["fc1_w"])
+            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_W2, l)[:E, :m], lp["fc2_w"])
+            wo = _view(buf, cfg, ffi.T_WO, l)[:E, :h * cfg.head_dim]
+            np.testing.assert_array_equal(wo, lp["proj_w"])
+            packed_q = _view(buf, cfg, ffi.T_WQKV, l)[:3 * cfg.head_dim * h, :E]
+            pq = packed_q.reshape(h, 3, cfg.head_dim, E).transpose(1, 0, 2, 3)
+            np.testing.assert_array_equal(pq.reshape(-1, E), lp["qkv_w"])
+            np.testing.assert_array_equal(_view(buf, cfg, ffi.T_LN1_G, l)[0, :E], lp["ln1_g"])
 
 
 def test_bf16_rounding_agrees_with_numpy_rne(lib):
@@ -161,8 +180,10 @@ def test_bf16_rounding_agrees_with_numpy_rne(lib):
     w["head_w"] = w["head_w"].copy()
     w["head_w"].reshape(-1)[:special.size] = special
     w["head_w"].reshape(-1)[special.size:special.size + 100] = rng.standard_normal(100) * 1e3
-    buf = ffi.pack_weights(cfg, w, inputs.make_dn_table(cfg))
-    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W), inputs.bf16_round(w["head_w"]))
+    t = inputs.make_dn_table(cfg)
+    buf = ffi.pack_weights(cfg, w, t)
+    np.testing.assert_array_equal(_view(buf, cfg, ffi.T_HEAD_W),
+                                  inputs.bf16_round(w["head_w"])[:, t.embed_order])
 
 
 def test_op_entry_points_validate_before_any_hip_call(lib):

@@ -31,7 +31,7 @@ def test_param_count_matches_table3():
 def test_flops_monotone_and_equal_direct_count(name):
     cfg = CONFIGS[name]
     table = inputs.make_dn_table(cfg)
-    w = inputs.make_weights(cfg) if name != "vit_b" else None
+    w = inputs.make_weights(cfg) if name not in ("vit_b", "vit_b_emb") else None
     prev = None
     for k in range(table.num_modes):
         f = cost.flops_per_image(cfg, table, k)
@@ -42,7 +42,7 @@ def test_flops_monotone_and_equal_direct_count(name):
             continue
         p = oracle.extract_dense(w, cfg, table, k)
         T, N = cfg.tokens, cfg.num_patches
-        direct = 2 * N * p["patch_w"].reshape(cfg.dim, -1).size
+        direct = 2 * N * p["patch_w"].size
         for lp in p["layers"]:
             h = lp["qkv_w"].shape[0] // (3 * cfg.head_dim)
             direct += 2 * T * (lp["qkv_w"].size + lp["proj_w"].size +
@@ -71,6 +71,11 @@ def test_dn_tables_nested_and_in_range(name):
     for l in range(cfg.depth):
         assert sorted(t.head_order[l]) == list(range(cfg.heads))
         assert sorted(t.mlp_order[l]) == list(range(cfg.mlp_hidden))
+    assert sorted(t.embed_order) == list(range(cfg.dim))
+    assert t.n_embed.shape == (t.num_modes,) and t.n_embed[0] == cfg.dim
+    assert (np.diff(t.n_embed) <= 0).all() and (t.n_embed >= 1).all()
+    if cfg.dtype == inputs.BF16:
+        assert (t.n_embed % 8 == 0).all()
 
 
 def test_vit_s_layer_ratios_give_layer_dependent_widths():

@@ -85,6 +85,34 @@ def test_bf16_all_modes_match_oracle(name):
         assert tie >= TOP1_MIN
 
 
+def test_tiny_emb_fp32_all_modes():
+    """Modes that also narrow the embedding (64, 48, 24 channels), fp32."""
+    m = model("tiny_emb")
+    for k in range(m.table.num_modes):
+        got = m.run(k)
+        ref = oracle.elastic_forward(m.w, m.cfg, m.table, k, m.x)
+        err = rel_err(got, ref)
+        print(f"tiny_emb mode {k} (d_k {m.table.n_embed[k]}): rel err {err:.3e}")
+        assert err <= FP32_TOL
+
+
+@pytest.mark.parametrize("name", ["vit_ti_emb", "vit_b_emb"])
+def test_bf16_embed_modes_match_oracle(name):
+    m = model(name)
+    gold = golden(name)
+    n = gold.shape[1]
+    assert gold.shape == (m.table.num_modes, n, m.cfg.num_classes)
+    for k in range(m.table.num_modes):
+        got = m.run(k)[:n]
+        assert np.isfinite(got).all()
+        err = rel_err(got, gold[k])
+        raw, tie = top1_agreement(got, gold[k])
+        print(f"{name} mode {k} (d_k {m.table.n_embed[k]}): rel err {err:.3e}, "
+              f"top-1 raw {raw:.4f} tie-aware {tie:.4f}")
+        assert err <= BF16_TOL
+        assert tie >= TOP1_MIN
+
+
 def test_forward_is_deterministic_and_switch_copies_nothing():
     m = model("vit_s")
     a = m.run(2)
@@ -123,12 +151,28 @@ def _poison_outside(w, cfg, table, k):
         p["fc1_w"][l][off_m] = np.nan
         p["fc1_b"][l][off_m] = np.nan
         p["fc2_w"][l][:, off_m] = np.nan
+    # embedding channels the mode drops: every tensor with a d axis
+    off_e = np.setdiff1d(np.arange(d), oracle.active_embed(table, k, d))
+    if off_e.size:
+        p["patch_w"][off_e] = np.nan
+        for key in ("patch_b", "cls", "norm_g", "norm_b"):
+            p[key][off_e] = np.nan
+        p["pos"][:, off_e] = np.nan
+        p["head_w"][:, off_e] = np.nan
+        for key in ("ln1_g", "ln1_b", "ln2_g", "ln2_b", "proj_b", "fc2_b"):
+            p[key][:, off_e] = np.nan
+        p["qkv_w"][:, :, off_e] = np.nan
+        p["fc1_w"][:, :, off_e] = np.nan
+        p["proj_w"][:, off_e, :] = np.nan
+        p["fc2_w"][:, off_e, :] = np.nan
     return p
 
 
-@pytest.mark.parametrize("name,k", [("tiny", 1), ("vit_s", 3), ("vit_s", 4), ("vit_b", 4)])
+@pytest.mark.parametrize("name,k", [("tiny", 1), ("vit_s", 3), ("vit_s", 4), ("vit_b", 4),
+                                    ("tiny_emb", 2), ("vit_ti_emb", 2), ("vit_ti_emb", 3)])
 def test_prefix_read_nan_poison(name, k):
-    """Mode k never reads a weight outside its prefix, ragged tails included."""
+    """Mode k never reads a weight outside its prefix (heads, units and
+    embedding channels), ragged tails included."""
     clean = model(name)
     ref = clean.run(k)
     poisoned = Model(name, weights=_poison_outside(clean.w, clean.cfg, clean.table, k))
@@ -151,10 +195,12 @@ def test_error_paths_on_device():
     assert m.vit.get_mode() in range(m.table.num_modes)
 
 
-def test_mode_info_matches_cost_model():
+@pytest.mark.parametrize("name", ["vit_b", "vit_b_emb", "tiny_emb"])
+def test_mode_info_matches_cost_model(name):
     from paper_2609_10018_amd import cost
-    m = model("vit_b")
+    m = model(name)
     for k in range(m.table.num_modes):
         f, wbytes = m.vit.mode_info(k)
         assert f == pytest.approx(cost.flops_per_image(m.cfg, m.table, k), rel=1e-12)
-        assert wbytes == 2 * cost.active_weight_elems(m.cfg, m.table, k)
+        eb = 2 if m.cfg.dtype == inputs.BF16 else 4
+        assert wbytes == eb * cost.active_weight_elems(m.cfg, m.table, k)

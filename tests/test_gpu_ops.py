@@ -183,6 +183,9 @@ def _attention_ref(qkv, B, T, h, hd, scale):
     (BF16, 2, 17, 2, 64, 384),
     (BF16, 1, 240, 3, 64, 576),
     (BF16, 2, 1, 2, 64, 384),
+    # more (sequence, head) pairs than workgroups: each walks several pairs
+    (BF16, 100, 197, 3, 64, 576),
+    (BF16, 130, 33, 4, 64, 768),
     (FP32, 4, 17, 2, 32, 192),
     (FP32, 2, 197, 3, 64, 576),
 ])

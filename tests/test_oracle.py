@@ -15,7 +15,7 @@ import pytest
 import oracle
 from paper_2609_10018_amd import inputs
 from paper_2609_10018_amd.inputs import CONFIGS, DNTable, ModelConfig
-from textbook import loop_masked_weights, rel_err, torch_vit
+from textbook import loop_extract_embed, loop_masked_weights, rel_err, torch_vit
 
 MINI = ModelConfig("mini", 48, 8, 3, 96, 3, 3, 192, 7, inputs.FP32, 3)
 
@@ -247,3 +247,82 @@ def test_i4_locality(mini):
     a2 = oracle.elastic_forward_masked(w, MINI, table, k, x)
     b2 = oracle.elastic_forward_masked(w2, MINI, table, k, x)
     assert np.array_equal(a2, b2)
+
+
+# ------------------------------------------------- narrower embedding (E1-E4)
+
+def test_masked_layer_norm_is_layer_norm_of_the_active_channels():
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((5, 40)) * 3 + 1
+    g, b = rng.standard_normal(40), rng.standard_normal(40)
+    act = np.sort(rng.permutation(40)[:17])
+    m = np.zeros(40)
+    m[act] = 1.0
+    got = oracle.layer_norm_masked(x, g * m, b * m, 1e-6, m)
+    ref = oracle.layer_norm(x[:, act], g[act], b[act], 1e-6)
+    np.testing.assert_allclose(got[:, act], ref, rtol=1e-13, atol=1e-13)
+    assert np.all(got[:, np.setdiff1d(np.arange(40), act)] == 0.0)
+    full = oracle.layer_norm_masked(x, g, b, 1e-6, np.ones(40))
+    np.testing.assert_allclose(full, oracle.layer_norm(x, g, b, 1e-6), rtol=1e-13, atol=1e-13)
+
+
+def test_embed_modes_equal_textbook_on_extracted_channels():
+    """Every tiny_emb mode: the textbook ViT (F.layer_norm over the d_k
+    channels it is given) on weights copied channel by channel equals both the
+    mask form and the gather form."""
+    import dataclasses
+    cfg = CONFIGS["tiny_emb"]
+    w = inputs.make_weights(cfg)
+    x = inputs.make_images(cfg, cfg.batch)
+    table = inputs.make_dn_table(cfg)
+    assert list(table.n_embed) == [64, 48, 24]
+    for k in range(table.num_modes):
+        sub, E = loop_extract_embed(w, cfg, table, k)
+        ref = torch_vit(sub, x, dataclasses.replace(cfg, dim=E), head_dim=cfg.head_dim)
+        assert rel_err(oracle.elastic_forward(w, cfg, table, k, x), ref) < 1e-10, k
+        assert rel_err(oracle.elastic_forward_masked(w, cfg, table, k, x), ref) < 1e-10, k
+
+
+@pytest.mark.parametrize("name", ["vit_ti_emb", "vit_b_emb"])
+def test_c2_embed_mask_form_equals_gather_form(name):
+    cfg = CONFIGS[name]
+    w = inputs.make_weights(cfg)
+    table = inputs.make_dn_table(cfg)
+    x = inputs.make_images(cfg, 1)
+    for k in range(1, table.num_modes):
+        assert table.n_embed[k] < cfg.dim
+        f2 = oracle.elastic_forward_masked(w, cfg, table, k, x)
+        f13 = oracle.elastic_forward(w, cfg, table, k, x)
+        assert rel_err(f13, f2) < 1e-10, (name, k)
+
+
+def test_i4_embed_locality():
+    """Weights of the embedding channels a mode drops do not change its logits."""
+    cfg = CONFIGS["tiny_emb"]
+    w = inputs.make_weights(cfg)
+    x = inputs.make_images(cfg, 2)
+    table = inputs.make_dn_table(cfg)
+    k = 2
+    off = np.setdiff1d(np.arange(cfg.dim), oracle.active_embed(table, k, cfg.dim))
+    rng = np.random.default_rng(22)
+    w2 = {key: np.array(v, copy=True) for key, v in w.items()}
+    w2["patch_w"][off] = rng.standard_normal(w2["patch_w"][off].shape)
+    for key in ("patch_b", "cls", "norm_g", "norm_b"):
+        w2[key][off] = 7.0
+    w2["pos"][:, off] = -3.0
+    w2["head_w"][:, off] = 5.0
+    for key in ("ln1_g", "ln1_b", "ln2_g", "ln2_b", "proj_b", "fc2_b"):
+        w2[key][:, off] = 9.0
+    w2["qkv_w"][:, :, off] = 4.0
+    w2["fc1_w"][:, :, off] = -4.0
+    w2["proj_w"][:, off, :] = 2.0
+    w2["fc2_w"][:, off, :] = 2.0
+    a = oracle.elastic_forward(w, cfg, table, k, x)
+    b = oracle.elastic_forward(w2, cfg, table, k, x)
+    assert np.array_equal(a, b)
+    am = oracle.elastic_forward_masked(w, cfg, table, k, x)
+    bm = oracle.elastic_forward_masked(w2, cfg, table, k, x)
+    assert rel_err(bm, am) < 1e-12
+    # and they do change a mode that keeps every channel
+    assert not np.array_equal(oracle.elastic_forward(w, cfg, table, 0, x),
+                              oracle.elastic_forward(w2, cfg, table, 0, x))

@@ -14,9 +14,11 @@ def t64(a):
     return torch.as_tensor(np.asarray(a, dtype=np.float64))
 
 
-def torch_vit(w, images, cfg, layer_heads=None):
-    """Full-width (or per-layer ``layer_heads``) ViT over stacked canonical weights."""
-    d, P, hd, eps = cfg.dim, cfg.patch, cfg.dim // cfg.heads, cfg.ln_eps
+def torch_vit(w, images, cfg, layer_heads=None, head_dim=None):
+    """Full-width (or per-layer ``layer_heads``) ViT over stacked canonical
+    weights (or per-layer lists); ``head_dim`` defaults to dim / heads."""
+    d, P, eps = cfg.dim, cfg.patch, cfg.ln_eps
+    hd = head_dim or cfg.dim // cfg.heads
     with torch.no_grad():
         x = F.conv2d(t64(images), t64(w["patch_w"]), t64(w["patch_b"]), stride=P)
         B = x.shape[0]
@@ -69,3 +71,42 @@ def rel_err(got, ref):
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     return float(np.max(np.abs(got - ref)) / np.max(np.abs(ref)))
+
+
+def loop_extract_embed(w, cfg, table, k):
+    """Mode k as a smaller dense ViT, copied element by element: the active
+    embedding channels (embed_order prefix), heads and MLP units.  Returns
+    (weights with per-layer lists, active embedding width)."""
+    d, H, M = cfg.dim, cfg.heads, cfg.mlp_hidden
+    hd = d // H
+    e = [int(c) for c in table.embed_order[:table.n_embed[k]]]
+    E = len(e)
+    out = {
+        "patch_w": np.array([w["patch_w"][c] for c in e]),
+        "patch_b": np.array([w["patch_b"][c] for c in e]),
+        "cls": np.array([w["cls"][c] for c in e]),
+        "pos": np.array([[w["pos"][t][c] for c in e] for t in range(w["pos"].shape[0])]),
+        "norm_g": np.array([w["norm_g"][c] for c in e]),
+        "norm_b": np.array([w["norm_b"][c] for c in e]),
+        "head_w": np.array([[w["head_w"][n][c] for c in e] for n in range(w["head_w"].shape[0])]),
+        "head_b": np.array(w["head_b"]),
+    }
+    for key in ("ln1_g", "ln1_b", "qkv_w", "qkv_b", "proj_w", "proj_b", "ln2_g", "ln2_b",
+                "fc1_w", "fc1_b", "fc2_w", "fc2_b"):
+        out[key] = []
+    for l in range(cfg.depth):
+        heads = [int(i) for i in table.head_order[l][:table.n_heads[k][l]]]
+        units = [int(j) for j in table.mlp_order[l][:table.n_mlp[k][l]]]
+        for key in ("ln1_g", "ln1_b", "ln2_g", "ln2_b"):
+            out[key].append(np.array([w[key][l][c] for c in e]))
+        qrows = [t * d + i * hd + c2 for t in range(3) for i in heads for c2 in range(hd)]
+        out["qkv_w"].append(np.array([[w["qkv_w"][l][r][c] for c in e] for r in qrows]))
+        out["qkv_b"].append(np.array([w["qkv_b"][l][r] for r in qrows]))
+        pcols = [i * hd + c2 for i in heads for c2 in range(hd)]
+        out["proj_w"].append(np.array([[w["proj_w"][l][c][q] for q in pcols] for c in e]))
+        out["proj_b"].append(np.array([w["proj_b"][l][c] for c in e]))
+        out["fc1_w"].append(np.array([[w["fc1_w"][l][j][c] for c in e] for j in units]))
+        out["fc1_b"].append(np.array([w["fc1_b"][l][j] for j in units]))
+        out["fc2_w"].append(np.array([[w["fc2_w"][l][c][j] for j in units] for c in e]))
+        out["fc2_b"].append(np.array([w["fc2_b"][l][c] for c in e]))
+    return out, E
