@@ -67,7 +67,7 @@ def time_steps(torch, vit, mode, xd, logits, steps, stream):
     return per, evs[0].elapsed_time(evs[-1]), wall
 
 
-def cpu_baseline(cfg, table, w_stored, x_stored, budget_s=12.0, max_images=64):
+def cpu_baseline(cfg, table, w_stored, x_stored, budget_s=15.0, max_images=256):
     """fp64 oracle (mode 0) on consecutive images until the time budget is used."""
     import oracle
     try:
@@ -142,6 +142,8 @@ def main():
     ap.add_argument("--copy-probe", action="store_true",
                     help="end with three plain copies of 1 GiB (out = in * 1, fp32), the "
                          "calibration dispatches for HBM byte counters")
+    ap.add_argument("--no-embed", action="store_true",
+                    help="skip the modes that also narrow the embedding (ViT-B, d 768..192)")
     ap.add_argument("--work-out", type=str, default=None,
                     help="write the algorithmic work per kernel class (mode 0) to this JSON file")
     args = ap.parse_args()
@@ -254,6 +256,28 @@ def main():
         "per_mode": per_mode,
         "roofline": roof,
     }
+    if not args.no_embed and args.modes == "all":
+        # Supplementary: the same ViT-B/16 with modes that also narrow the
+        # embedding width (768, 576, 384, 192 channels), same batch and dtype.
+        ecfg = inputs.CONFIGS["vit_b_emb"]
+        etable = inputs.make_dn_table(ecfg)
+        evit = ffi.ElasticViT(ecfg, w, etable, B)
+        emb = []
+        for k in range(etable.num_modes):
+            evit.set_mode(k)
+            for _ in range(max(1, args.warmup)):
+                evit.forward(xd, logits, stream)
+            per, tot, _ = time_steps(torch, evit, k, xd, logits, args.steps, stream)
+            gflop = cost.flops_per_image(ecfg, etable, k) / 1e9
+            ips = B * 1e3 / (tot / args.steps)
+            emb.append({"mode": k, "heads": inputs.MODE_CAPS["vit_b_emb"][k][0],
+                        "mlp": inputs.MODE_CAPS["vit_b_emb"][k][1],
+                        "embed": int(etable.n_embed[k]), "gflop_per_image": round(gflop, 4),
+                        "images_per_s": ips, "median_ms": statistics.median(per),
+                        "mfu": ips * gflop * 1e9 / (BF16_PEAK_TFLOPS * 1e12)})
+            log(f"embed mode {k} (d {etable.n_embed[k]}): {ips:.0f} images/s")
+        evit.close()
+        result["per_mode_embed"] = emb
     # The cost columns of the run-time DN selection table (Eq. 11) as the
     # library measures them at this batch; the accuracy column is the user's
     # (there are no trained weights here to measure it on).

@@ -14,11 +14,11 @@ import oracle.vit as ov
 from paper_2609_10018_amd import inputs
 from paper_2609_10018_amd.inputs import CONFIGS
 from test_oracle import MINI, mini_table
-from textbook import loop_masked_weights, rel_err, torch_vit
+from textbook import loop_extract_embed, loop_masked_weights, rel_err, torch_vit
 
 _orig = {name: getattr(ov, name) for name in
          ("layer_norm", "gelu", "softmax_rows", "patchify", "attention", "active_sets",
-          "masks")}
+          "masks", "layer_norm_masked", "active_embed")}
 
 
 def _ln_no_beta(x, g, b, eps):
@@ -124,6 +124,37 @@ def _c2_err():
                for k in range(1, table.num_modes))
 
 
+def _ln_masked_full_stats(x, g, b, eps, m):
+    return _orig["layer_norm"](x, g, b, eps) * m      # statistics over all d channels
+
+
+def _active_embed_suffix(table, k, dim):
+    order = np.asarray(table.embed_order, dtype=np.int64)
+    return order[dim - int(table.n_embed[k]):]
+
+
+def _embed_err(form):
+    import dataclasses
+    cfg = CONFIGS["tiny_emb"]
+    w = inputs.make_weights(cfg)
+    x = inputs.make_images(cfg, 2)
+    table = inputs.make_dn_table(cfg)
+    errs = []
+    for k in range(1, table.num_modes):
+        sub, E = loop_extract_embed(w, cfg, table, k)
+        ref = torch_vit(sub, x, dataclasses.replace(cfg, dim=E), head_dim=cfg.head_dim)
+        errs.append(rel_err(form(w, cfg, table, k, x), ref))
+    return max(errs)
+
+
+def _embed_mask_form_err():
+    return _embed_err(oracle.elastic_forward_masked)
+
+
+def _embed_gather_form_err():
+    return _embed_err(oracle.elastic_forward)
+
+
 MUTANTS = [
     ("layer_norm", _ln_no_beta, _full_width_err),
     ("layer_norm", _ln_unbiased, _full_width_err),
@@ -135,6 +166,8 @@ MUTANTS = [
     ("softmax_rows", _softmax_cols, _full_width_err),
     ("active_sets", _active_suffix, _masked_mode_err),
     ("masks", _masks_modulo, _c2_err),
+    ("layer_norm_masked", _ln_masked_full_stats, _embed_mask_form_err),
+    ("active_embed", _active_embed_suffix, _embed_gather_form_err),
 ]
 
 
