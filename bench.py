@@ -281,10 +281,12 @@ def main():
     # The cost columns of the run-time DN selection table (Eq. 11) as the
     # library measures them at this batch; the accuracy column is the user's
     # (there are no trained weights here to measure it on).
-    lat, mem, fl = vit.profile_modes(xd, logits, warmup=2, iters=10, stream=stream)
-    result["dn_table"] = [{"mode": k, "latency_ms": float(lat[k]), "memory_bytes": float(mem[k]),
-                           "gflop": float(fl[k]) / 1e9} for k in range(len(lat))]
-    log("DN table measured")
+    if args.modes == "all":
+        lat, mem, fl = vit.profile_modes(xd, logits, warmup=2, iters=10, stream=stream)
+        result["dn_table"] = [{"mode": k, "latency_ms": float(lat[k]),
+                               "memory_bytes": float(mem[k]), "gflop": float(fl[k]) / 1e9}
+                              for k in range(len(lat))]
+        log("DN table measured")
     if not args.no_latency:
         result["latency"] = latency_regime(torch, ffi, inputs, cfg, w, table)
         log("latency regime done")
