@@ -150,6 +150,42 @@ def test_small_batches(name, batches):
                 np.testing.assert_array_equal(m.run(k, batch), got)
 
 
+def test_forward_captured_in_hip_graphs():
+    """The forward allocates, synchronises and memsets nothing, so one graph
+    per mode can be captured; every replay, with eager forwards in between,
+    equals the eager result."""
+    m = model("vit_ti")
+    batch = 8
+    s = torch.cuda.Stream()
+    logits = torch.empty((batch, m.cfg.num_classes), dtype=torch.float32, device="cuda")
+    xd = m.xd[:batch].contiguous()
+    eager = {}
+    with torch.cuda.stream(s):
+        for k in range(m.table.num_modes):
+            m.vit.set_mode(k)
+            m.vit.forward(xd, logits, s)
+            s.synchronize()
+            eager[k] = logits.clone()
+    graphs = {}
+    for k in range(m.table.num_modes):
+        g = torch.cuda.CUDAGraph()
+        m.vit.set_mode(k)
+        with torch.cuda.graph(g, stream=s):
+            m.vit.forward(xd, logits, s)
+        graphs[k] = g
+    torch.cuda.synchronize()
+    seq = inputs.mode_sequence(40, m.table.num_modes)
+    other = torch.empty_like(logits)
+    for i, k in enumerate(seq):
+        graphs[int(k)].replay()
+        torch.cuda.synchronize()
+        assert torch.equal(logits, eager[int(k)]), (i, int(k))
+        with torch.cuda.stream(s):            # eager work between replays
+            m.vit.set_mode(int((k + 1) % m.table.num_modes))
+            m.vit.forward(xd, other, s)
+        s.synchronize()
+
+
 def _poison_outside(w, cfg, table, k):
     """Copy of w with every weight outside mode k's active heads / units = NaN."""
     p = {key: np.array(v, copy=True) for key, v in w.items()}
