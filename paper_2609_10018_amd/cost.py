@@ -64,3 +64,28 @@ def active_weight_elems(cfg: ModelConfig, table, k: int) -> int:
     h, m = layer_widths(table, k)
     per_layer = 3 * hd * h * d + d * hd * h + m * d + d * m
     return int(d * cfg.patch_k + per_layer.sum() + C * d)
+
+
+def cnn_layer_macs(cfg, table, k: int):
+    """Per-image MACs of each convolution of an elastic bottleneck ResNet in
+    mode k, in forward order: (name, MACs)."""
+    out = []
+    hw = cfg.img // 2
+    out.append(("stem", hw * hw * cfg.stem * cfg.in_chans * 49))
+    hw //= 2
+    for i, b in enumerate(cfg.block_specs()):
+        w = int(table.n_width[k][i])
+        ho = hw // b["stride"]
+        out.append((f"b{i}_c1", hw * hw * w * b["c_in"]))
+        out.append((f"b{i}_c2", ho * ho * w * w * 9))
+        out.append((f"b{i}_c3", ho * ho * b["c_out"] * w))
+        if b["down"]:
+            out.append((f"b{i}_dn", ho * ho * b["c_out"] * b["c_in"]))
+        hw = ho
+    out.append(("fc", cfg.features * cfg.num_classes))
+    return out
+
+
+def cnn_macs(cfg, table, k: int) -> int:
+    """Per-image multiply-accumulates of every convolution and the classifier."""
+    return int(sum(m for _, m in cnn_layer_macs(cfg, table, k)))
