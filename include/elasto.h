@@ -339,6 +339,78 @@ elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_
                                     int32_t heads, int32_t head_dim, float scale,
                                     void* hip_stream);
 
+/* ======================================== elastic bottleneck ResNet (CNN) */
+/* The paper applies the same elastic transformation to CNNs (Eq. 7 masks
+ * whole convolution kernels; Table 2 reports ResNet-50 DNs).  This is the
+ * inference forward of a ResNet-50-style network (7x7 stride-2 stem + ReLU,
+ * 3x3 stride-2 max pool, bottleneck blocks of 1x1 reduce, 3x3 with the block
+ * stride and 1x1 expand, a 1x1 projection shortcut with the same stride on
+ * each stage's first block, ReLU after the sum, global average pooling,
+ * linear classifier), BF16 only: bf16 NHWC activations, MFMA convolutions
+ * (as GEMMs over explicit patch matrices), fp32 biases and logits.  Batch
+ * norm at inference is a per-channel affine map: the caller folds it into
+ * each convolution's weights and bias.
+ *
+ * A DN mode keeps, in each bottleneck, the first n_width[k][b] filters of
+ * the 1x1 reduce (in order1) and of the 3x3 (in order2); a pruned filter
+ * also removes the input channels that read it.  The weights are stored in
+ * those orders so a mode reads prefixes (nested DNs, Eq. 8). */
+typedef struct elasto_cnn_s* elasto_cnn_t;
+
+/* Shape.  Blocks: blocks[s] bottlenecks in stage s, inner width widths[s],
+ * output channels widths[s] * expansion; stage s > 0 starts with stride 2.
+ * Needs img % 32 == 0, stem, widths[] and expansion * widths[] multiples of
+ * 8, 1 <= num_stages <= 8, in_chans >= 1, dtype == ELASTO_BF16. */
+typedef struct {
+  int32_t img, in_chans, stem, num_stages;
+  int32_t widths[8], blocks[8];
+  int32_t expansion, num_classes, max_batch, dtype;
+} elasto_cnn_config_t;
+
+/* HOST pointers to fp32 tensors in PyTorch order, in this sequence:
+ * stem_w [stem][in_chans][7][7], stem_b; then per block b (stage-major):
+ * c1_w [w][c_in][1][1], c1_b, c2_w [w][w][3][3], c2_b, c3_w [c_out][w][1][1],
+ * c3_b, and on each stage's first block dn_w [c_out][c_in][1][1], dn_b;
+ * then fc_w [classes][features], fc_b.  num_tensors must match. */
+typedef struct {
+  int32_t num_tensors;
+  const float* const* tensors;
+} elasto_cnn_weights_t;
+
+/* n_width [num_modes][num_blocks], each a multiple of 8 in [8, width];
+ * order1 / order2: the blocks' filter orders concatenated (block b holds a
+ * permutation of its width).  ELASTO_ERR_BAD_TABLE otherwise. */
+typedef struct {
+  int32_t num_modes, num_blocks;
+  const int32_t* n_width;
+  const int32_t* order1;
+  const int32_t* order2;
+} elasto_cnn_table_t;
+
+/* Host-only validation (no HIP call). */
+elasto_status_t elasto_cnn_validate(const elasto_cnn_config_t* cfg, const elasto_cnn_table_t* t);
+
+/* As elasto_create: validates, packs (bf16 filters with the input channels
+ * of each 3x3 ordered channel-major, c * 9 + tap, so a narrower mode's
+ * channels are a prefix of every filter row), one weight and one scratch
+ * allocation sized for max_batch, mode 0 selected. */
+elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_cnn_weights_t* w,
+                                  const elasto_cnn_table_t* table, elasto_cnn_t* out);
+elasto_status_t elasto_cnn_destroy(elasto_cnn_t h);
+elasto_status_t elasto_cnn_set_mode(elasto_cnn_t h, int32_t k);  /* O(1) host store */
+elasto_status_t elasto_cnn_get_mode(elasto_cnn_t h, int32_t* k);
+
+/* One forward in the current mode on hip_stream: images bf16 NCHW
+ * [batch][in_chans][img][img] (device, 16-byte aligned), logits fp32
+ * [batch][num_classes] (device).  Allocates nothing, never synchronises. */
+elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t batch,
+                                   float* logits, void* hip_stream);
+
+/* Multiply-accumulates per image of mode k (convolutions and classifier) and
+ * bytes of the filters and classifier the mode reads. */
+elasto_status_t elasto_cnn_mode_info(elasto_cnn_t h, int32_t k, double* macs_per_image,
+                                     int64_t* active_weight_bytes);
+
 #ifdef __cplusplus
 }
 #endif

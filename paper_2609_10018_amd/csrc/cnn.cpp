@@ -1,0 +1,418 @@
+// C ABI of the elastic bottleneck-ResNet path: validation, packing into the
+// prefix layout, buffers, and the forward as a sequence of launches.
+//
+// One forward in mode k (NHWC bf16 activations; n = n_width[k][b]):
+//   stem: patch matrix of the NCHW images (7x7, stride 2) -> GEMM + ReLU
+//   3x3 stride-2 max pool                                       -> cur
+//   per bottleneck b:
+//     1x1 reduce: GEMM over cur, N = n (prefix of order1) + ReLU -> t1
+//     3x3: patch matrix of t1's first n channels (k = c*9 + tap), GEMM with
+//          K = 9n (prefix of each packed filter row), N = n (order2) + ReLU -> t2
+//     shortcut: cur, or a 1x1 (strided) projection GEMM        -> other
+//     1x1 expand: GEMM over t2, K = n, + shortcut, ReLU, in place into the
+//          shortcut buffer (which becomes cur)
+//   global average pool -> classifier GEMM (fp32 logits)
+#include <hip/hip_runtime.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <vector>
+
+#include "kernels.h"
+#include "layout.h"
+
+using namespace elasto;
+
+namespace {
+
+struct BlockSpec {
+  int c_in, width, c_out, stride, hw_in;
+  bool down;
+};
+
+struct BlockOff {
+  int64_t c1w, c1b, c2w, c2b, c3w, c3b, dnw, dnb;
+};
+
+std::vector<BlockSpec> block_specs(const elasto_cnn_config_t& c) {
+  std::vector<BlockSpec> out;
+  int c_in = c.stem, hw = c.img / 4;
+  for (int s = 0; s < c.num_stages; ++s)
+    for (int b = 0; b < c.blocks[s]; ++b) {
+      BlockSpec k;
+      k.c_in = c_in;
+      k.width = c.widths[s];
+      k.c_out = c.widths[s] * c.expansion;
+      k.stride = (b == 0 && s > 0) ? 2 : 1;
+      k.hw_in = hw;
+      k.down = b == 0;
+      out.push_back(k);
+      hw /= k.stride;
+      c_in = k.c_out;
+    }
+  return out;
+}
+
+int64_t al256(int64_t v) { return (v + 255) / 256 * 256; }
+
+bool check_cnn_config(const elasto_cnn_config_t* c) {
+  if (!c) { set_error("config is NULL"); return false; }
+  if (c->dtype != ELASTO_BF16) { set_error("the CNN path is bf16 only"); return false; }
+  if (c->img < 32 || c->img % 32 != 0) { set_error("img must be a positive multiple of 32"); return false; }
+  if (c->in_chans < 1 || c->in_chans > 64) { set_error("in_chans outside [1, 64]"); return false; }
+  if (c->stem < 8 || c->stem % 8 != 0) { set_error("stem channels must be a multiple of 8"); return false; }
+  if (c->num_stages < 1 || c->num_stages > 8) { set_error("num_stages outside [1, 8]"); return false; }
+  if (c->expansion < 1 || c->num_classes < 1 || c->max_batch < 1) { set_error("bad size"); return false; }
+  if ((c->img >> (c->num_stages + 1)) < 1) { set_error("too many stages for img"); return false; }
+  for (int s = 0; s < c->num_stages; ++s) {
+    if (c->widths[s] < 8 || c->widths[s] % 8 != 0) { set_error("widths must be multiples of 8"); return false; }
+    if (c->blocks[s] < 1) { set_error("every stage needs a block"); return false; }
+  }
+  return true;
+}
+
+bool check_cnn_table(const elasto_cnn_config_t* c, const elasto_cnn_table_t* t) {
+  if (!t) { set_error("table is NULL"); return false; }
+  const std::vector<BlockSpec> bs = block_specs(*c);
+  if (t->num_blocks != (int)bs.size()) { set_error("table has %d blocks, the network %d", t->num_blocks, (int)bs.size()); return false; }
+  if (t->num_modes < 1 || t->num_modes > 4096) { set_error("num_modes outside [1, 4096]"); return false; }
+  if (!t->n_width || !t->order1 || !t->order2) { set_error("table has a NULL array"); return false; }
+  for (int k = 0; k < t->num_modes; ++k)
+    for (size_t b = 0; b < bs.size(); ++b) {
+      const int n = t->n_width[(size_t)k * bs.size() + b];
+      if (n < 8 || n > bs[b].width || n % 8 != 0) {
+        set_error("n_width[%d][%d] = %d not a multiple of 8 in [8, %d]", k, (int)b, n, bs[b].width);
+        return false;
+      }
+    }
+  int64_t off = 0;
+  std::vector<char> seen;
+  for (size_t b = 0; b < bs.size(); ++b) {
+    for (const int32_t* ord : {t->order1, t->order2}) {
+      seen.assign(bs[b].width, 0);
+      for (int j = 0; j < bs[b].width; ++j) {
+        const int v = ord[off + j];
+        if (v < 0 || v >= bs[b].width || seen[v]) { set_error("block %d filter order is not a permutation", (int)b); return false; }
+        seen[v] = 1;
+      }
+    }
+    off += bs[b].width;
+  }
+  return true;
+}
+
+int num_tensors(const std::vector<BlockSpec>& bs) {
+  int n = 4;  // stem w, b; fc w, b
+  for (const BlockSpec& b : bs) n += b.down ? 8 : 6;
+  return n;
+}
+
+}  // namespace
+
+struct elasto_cnn_s {
+  elasto_cnn_config_t cfg;
+  std::vector<BlockSpec> blocks;
+  int num_modes = 0;
+  std::vector<int32_t> n_width;  // [num_modes][blocks]
+  int mode = 0, device = 0;
+  uint8_t* dw = nullptr;
+  uint8_t* ds = nullptr;
+  int64_t wbytes = 0, sbytes = 0;
+  int stem_kpad = 0;
+  int64_t stem_w = 0, stem_b = 0, fc_w = 0, fc_b = 0;
+  std::vector<BlockOff> boff;
+  void *col = nullptr, *stem_out = nullptr, *x = nullptr, *d = nullptr, *t1 = nullptr,
+       *t2 = nullptr, *feat = nullptr;
+};
+
+extern "C" {
+
+elasto_status_t elasto_cnn_validate(const elasto_cnn_config_t* cfg, const elasto_cnn_table_t* t) {
+  if (!check_cnn_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
+  if (!check_cnn_table(cfg, t)) return ELASTO_ERR_BAD_TABLE;
+  clear_error();
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_cnn_weights_t* w,
+                                  const elasto_cnn_table_t* table, elasto_cnn_t* out) {
+  if (!out) return fail(ELASTO_ERR_INVALID_ARG, "out is NULL");
+  if (!check_cnn_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
+  if (!check_cnn_table(cfg, table)) return ELASTO_ERR_BAD_TABLE;
+  const std::vector<BlockSpec> bs = block_specs(*cfg);
+  if (!w || !w->tensors || w->num_tensors != num_tensors(bs))
+    return fail(ELASTO_ERR_INVALID_ARG, "expected %d weight tensors", num_tensors(bs));
+  for (int i = 0; i < w->num_tensors; ++i)
+    if (!w->tensors[i]) return fail(ELASTO_ERR_INVALID_ARG, "weight tensor %d is NULL", i);
+
+  elasto_cnn_s* h = new (std::nothrow) elasto_cnn_s();
+  if (!h) return fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
+  h->cfg = *cfg;
+  h->blocks = bs;
+  h->num_modes = table->num_modes;
+  h->n_width.assign(table->n_width, table->n_width + (size_t)table->num_modes * bs.size());
+
+  // Packed layout (offsets in bytes, 256-aligned): bf16 filters, fp32 biases.
+  const int C = cfg->in_chans;
+  h->stem_kpad = (C * 49 + 7) / 8 * 8;
+  int64_t off = 0;
+  auto put = [&](int64_t bytes) { const int64_t o = off; off = al256(off + bytes); return o; };
+  h->stem_w = put((int64_t)cfg->stem * h->stem_kpad * 2);
+  h->stem_b = put((int64_t)cfg->stem * 4);
+  for (const BlockSpec& b : bs) {
+    BlockOff o{};
+    o.c1w = put((int64_t)b.width * b.c_in * 2);
+    o.c1b = put((int64_t)b.width * 4);
+    o.c2w = put((int64_t)b.width * b.width * 9 * 2);
+    o.c2b = put((int64_t)b.width * 4);
+    o.c3w = put((int64_t)b.c_out * b.width * 2);
+    o.c3b = put((int64_t)b.c_out * 4);
+    if (b.down) {
+      o.dnw = put((int64_t)b.c_out * b.c_in * 2);
+      o.dnb = put((int64_t)b.c_out * 4);
+    }
+    h->boff.push_back(o);
+  }
+  const int F = bs.back().c_out;
+  h->fc_w = put((int64_t)cfg->num_classes * F * 2);
+  h->fc_b = put((int64_t)cfg->num_classes * 4);
+  h->wbytes = off;
+
+  std::vector<uint8_t> host;
+  try {
+    host.assign((size_t)h->wbytes, 0);
+  } catch (...) {
+    delete h;
+    return fail(ELASTO_ERR_OUT_OF_MEMORY, "host staging allocation failed");
+  }
+  auto mat = [&](int64_t o, int64_t i, float v) {
+    const uint16_t b16 = f32_to_bf16_rne(v);
+    memcpy(host.data() + o + i * 2, &b16, 2);
+  };
+  auto vec = [&](int64_t o, int64_t i, float v) { memcpy(host.data() + o + i * 4, &v, 4); };
+  int ti = 0;
+  const float* const* T = w->tensors;
+  {
+    const float* sw = T[ti++];
+    const float* sb = T[ti++];
+    for (int co = 0; co < cfg->stem; ++co) {
+      for (int k = 0; k < C * 49; ++k) mat(h->stem_w, (int64_t)co * h->stem_kpad + k, sw[(int64_t)co * C * 49 + k]);
+      vec(h->stem_b, co, sb[co]);
+    }
+  }
+  int64_t ooff = 0;
+  for (size_t bi = 0; bi < bs.size(); ++bi) {
+    const BlockSpec& b = bs[bi];
+    const BlockOff& o = h->boff[bi];
+    const int32_t* o1 = table->order1 + ooff;
+    const int32_t* o2 = table->order2 + ooff;
+    ooff += b.width;
+    const float *c1w = T[ti], *c1b = T[ti + 1], *c2w = T[ti + 2], *c2b = T[ti + 3],
+                *c3w = T[ti + 4], *c3b = T[ti + 5];
+    ti += 6;
+    for (int j = 0; j < b.width; ++j) {  // reduce: filter j = order1[j]
+      for (int c = 0; c < b.c_in; ++c) mat(o.c1w, (int64_t)j * b.c_in + c, c1w[(int64_t)o1[j] * b.c_in + c]);
+      vec(o.c1b, j, c1b[o1[j]]);
+    }
+    for (int j = 0; j < b.width; ++j) {  // 3x3: filter order2[j], input channel order1[i]
+      for (int i = 0; i < b.width; ++i)
+        for (int t = 0; t < 9; ++t)
+          mat(o.c2w, ((int64_t)j * b.width + i) * 9 + t,
+              c2w[(((int64_t)o2[j] * b.width) + o1[i]) * 9 + t]);
+      vec(o.c2b, j, c2b[o2[j]]);
+    }
+    for (int co = 0; co < b.c_out; ++co) {  // expand: input channel order2[i]
+      for (int i = 0; i < b.width; ++i) mat(o.c3w, (int64_t)co * b.width + i, c3w[(int64_t)co * b.width + o2[i]]);
+      vec(o.c3b, co, c3b[co]);
+    }
+    if (b.down) {
+      const float *dw = T[ti], *db = T[ti + 1];
+      ti += 2;
+      for (int64_t i = 0; i < (int64_t)b.c_out * b.c_in; ++i) mat(o.dnw, i, dw[i]);
+      for (int co = 0; co < b.c_out; ++co) vec(o.dnb, co, db[co]);
+    }
+  }
+  {
+    const float* fw = T[ti++];
+    const float* fb = T[ti++];
+    for (int64_t i = 0; i < (int64_t)cfg->num_classes * F; ++i) mat(h->fc_w, i, fw[i]);
+    for (int n = 0; n < cfg->num_classes; ++n) vec(h->fc_b, n, fb[n]);
+  }
+
+  // Scratch for max_batch images.
+  const int64_t B = cfg->max_batch, hs = cfg->img / 2;
+  int64_t col = B * hs * hs * h->stem_kpad, io = B * (hs / 2) * (hs / 2) * cfg->stem, t1 = 0, t2 = 0;
+  for (const BlockSpec& b : bs) {
+    const int64_t hi = b.hw_in, ho = b.hw_in / b.stride;
+    col = std::max(col, B * ho * ho * 9 * b.width);
+    if (b.down && b.stride > 1) col = std::max(col, B * ho * ho * b.c_in);
+    io = std::max(io, B * ho * ho * b.c_out);
+    t1 = std::max(t1, B * hi * hi * b.width);
+    t2 = std::max(t2, B * ho * ho * b.width);
+  }
+  const int64_t sz_col = al256(col * 2), sz_stem = al256(B * hs * hs * cfg->stem * 2),
+                sz_io = al256(io * 2), sz_t1 = al256(t1 * 2), sz_t2 = al256(t2 * 2),
+                sz_feat = al256(B * F * 2);
+  h->sbytes = sz_col + sz_stem + 2 * sz_io + sz_t1 + sz_t2 + sz_feat;
+
+  hipError_t e = hipGetDevice(&h->device);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->dw), (size_t)h->wbytes);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->ds), (size_t)h->sbytes);
+  if (e == hipSuccess) e = hipMemcpy(h->dw, host.data(), (size_t)h->wbytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    const elasto_status_t st = (e == hipErrorOutOfMemory) ? ELASTO_ERR_OUT_OF_MEMORY : ELASTO_ERR_HIP;
+    if (h->dw) (void)hipFree(h->dw);
+    if (h->ds) (void)hipFree(h->ds);
+    delete h;
+    (void)hipGetLastError();
+    return fail(st, "cnn create: %s", hipGetErrorString(e));
+  }
+  uint8_t* p = h->ds;
+  h->col = p; p += sz_col;
+  h->stem_out = p; p += sz_stem;
+  h->x = p; p += sz_io;
+  h->d = p; p += sz_io;
+  h->t1 = p; p += sz_t1;
+  h->t2 = p; p += sz_t2;
+  h->feat = p;
+  *out = h;
+  clear_error();
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_cnn_destroy(elasto_cnn_t h) {
+  if (!h) return ELASTO_OK;
+  hipError_t e1 = hipSuccess, e2 = hipSuccess;
+  if (h->dw) e1 = hipFree(h->dw);
+  if (h->ds) e2 = hipFree(h->ds);
+  delete h;
+  if (e1 != hipSuccess || e2 != hipSuccess)
+    return fail(ELASTO_ERR_HIP, "cnn destroy: %s", hipGetErrorString(e1 != hipSuccess ? e1 : e2));
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_cnn_set_mode(elasto_cnn_t h, int32_t k) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (k < 0 || k >= h->num_modes) return fail(ELASTO_ERR_MODE_RANGE, "mode %d outside [0, %d)", k, h->num_modes);
+  h->mode = k;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_cnn_get_mode(elasto_cnn_t h, int32_t* k) {
+  if (!h || !k) return fail(ELASTO_ERR_INVALID_ARG, "NULL argument");
+  *k = h->mode;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_cnn_mode_info(elasto_cnn_t h, int32_t k, double* macs_per_image,
+                                     int64_t* active_weight_bytes) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (k < 0 || k >= h->num_modes) return fail(ELASTO_ERR_MODE_RANGE, "mode %d outside [0, %d)", k, h->num_modes);
+  const elasto_cnn_config_t& c = h->cfg;
+  const int64_t hs = c.img / 2;
+  double macs = (double)hs * hs * c.stem * c.in_chans * 49;
+  int64_t wb = (int64_t)c.stem * c.in_chans * 49;
+  for (size_t b = 0; b < h->blocks.size(); ++b) {
+    const BlockSpec& s = h->blocks[b];
+    const int64_t n = h->n_width[(size_t)k * h->blocks.size() + b];
+    const double hi = s.hw_in, ho = s.hw_in / s.stride;
+    macs += hi * hi * n * s.c_in + ho * ho * n * n * 9 + ho * ho * s.c_out * n;
+    wb += n * s.c_in + n * n * 9 + (int64_t)s.c_out * n;
+    if (s.down) {
+      macs += ho * ho * s.c_out * s.c_in;
+      wb += (int64_t)s.c_out * s.c_in;
+    }
+  }
+  macs += (double)h->blocks.back().c_out * c.num_classes;
+  wb += (int64_t)h->blocks.back().c_out * c.num_classes;
+  if (macs_per_image) *macs_per_image = macs;
+  if (active_weight_bytes) *active_weight_bytes = wb * 2;
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t batch,
+                                   float* logits, void* hip_stream) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (!images || !logits) return fail(ELASTO_ERR_INVALID_ARG, "images / logits is NULL");
+  if (batch < 1 || batch > h->cfg.max_batch)
+    return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
+  if ((reinterpret_cast<uintptr_t>(images) & 15) != 0 || (reinterpret_cast<uintptr_t>(logits) & 3) != 0)
+    return fail(ELASTO_ERR_INVALID_ARG, "misaligned images / logits");
+  int cur_dev = -1;
+  if (hipGetDevice(&cur_dev) != hipSuccess || cur_dev != h->device) {
+    if (hipSetDevice(h->device) != hipSuccess) return fail(ELASTO_ERR_HIP, "cannot select device %d", h->device);
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const elasto_cnn_config_t& c = h->cfg;
+  const int k = h->mode;
+  const int64_t B = batch;
+  auto Wp = [&](int64_t o) { return static_cast<const void*>(h->dw + o); };
+  auto Fp = [&](int64_t o) { return reinterpret_cast<const float*>(h->dw + o); };
+  auto gemm = [&](Epi epi, const void* A, int64_t lda, int64_t wo, int64_t ldw, void* C, int64_t ldc,
+                  int64_t bo, int64_t M, int N, int K, bool relu) {
+    GemmArgs a;
+    a.A = A; a.lda = lda;
+    a.W = Wp(wo); a.ldw = ldw;
+    a.C = C; a.ldc = ldc;
+    a.bias = Fp(bo);
+    a.M = M; a.N = N; a.K = K;
+    a.relu = relu;
+    return launch_gemm_bf16(epi, a, s);
+  };
+  hipError_t e;
+#define ELASTO_TRY(call, what)                                                       \
+  do {                                                                              \
+    e = (call);                                                                     \
+    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "%s: %s", what, hipGetErrorString(e)); \
+  } while (0)
+
+  const int hs = c.img / 2;
+  ELASTO_TRY(launch_im2col_nchw(images, batch, c.in_chans, c.img, c.img, 7, 7, 2, 3, h->stem_kpad,
+                                h->col, s), "stem patches");
+  ELASTO_TRY(gemm(Epi::Bias, h->col, h->stem_kpad, h->stem_w, h->stem_kpad, h->stem_out, c.stem,
+                  h->stem_b, B * hs * hs, c.stem, h->stem_kpad, true), "stem");
+  ELASTO_TRY(launch_max_pool_3x3_s2(h->stem_out, batch, hs, hs, c.stem, h->x, s), "max pool");
+  void* cur = h->x;
+  void* other = h->d;
+  for (size_t bi = 0; bi < h->blocks.size(); ++bi) {
+    const BlockSpec& b = h->blocks[bi];
+    const BlockOff& o = h->boff[bi];
+    const int n = h->n_width[(size_t)k * h->blocks.size() + bi];
+    const int hi = b.hw_in, ho = b.hw_in / b.stride;
+    const int64_t mi = B * hi * hi, mo = B * ho * ho;
+    ELASTO_TRY(gemm(Epi::Bias, cur, b.c_in, o.c1w, b.c_in, h->t1, b.width, o.c1b, mi, n, b.c_in, true),
+               "1x1 reduce");
+    ELASTO_TRY(launch_im2col_nhwc(h->t1, batch, hi, hi, b.width, n, 3, 3, b.stride, 1, h->col, s),
+               "3x3 patches");
+    ELASTO_TRY(gemm(Epi::Bias, h->col, 9 * n, o.c2w, 9 * b.width, h->t2, b.width, o.c2b, mo, n, 9 * n,
+                    true), "3x3");
+    void* shortcut = cur;
+    if (b.down) {
+      const void* src = cur;
+      if (b.stride > 1) {
+        ELASTO_TRY(launch_im2col_nhwc(cur, batch, hi, hi, b.c_in, b.c_in, 1, 1, b.stride, 0, h->col, s),
+                   "projection rows");
+        src = h->col;
+      }
+      ELASTO_TRY(gemm(Epi::Bias, src, b.c_in, o.dnw, b.c_in, other, b.c_out, o.dnb, mo, b.c_out,
+                      b.c_in, false), "projection");
+      shortcut = other;
+    }
+    ELASTO_TRY(gemm(Epi::BiasResid, h->t2, b.width, o.c3w, b.width, shortcut, b.c_out, o.c3b, mo,
+                    b.c_out, n, true), "1x1 expand");
+    if (b.down) {
+      other = cur;
+      cur = shortcut;
+    }
+  }
+  const BlockSpec& last = h->blocks.back();
+  const int hf = last.hw_in / last.stride;
+  ELASTO_TRY(launch_avg_pool(cur, batch, hf * hf, last.c_out, h->feat, s), "average pool");
+  ELASTO_TRY(gemm(Epi::BiasF32, h->feat, last.c_out, h->fc_w, last.c_out, logits, c.num_classes,
+                  h->fc_b, B, c.num_classes, last.c_out, false), "classifier");
+#undef ELASTO_TRY
+  return ELASTO_OK;
+}
+
+}  // extern "C"

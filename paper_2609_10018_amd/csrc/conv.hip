@@ -1,0 +1,193 @@
+// Data-movement kernels of the elastic bottleneck-ResNet path (Section 4.1's
+// CNN backbone, Table 2); the convolutions themselves run as bf16 MFMA GEMMs
+// (gemm_bf16.hip) over these operands.  Activations are NHWC bf16.
+//
+// * im2col_nhwc: [N,H,W,Cs] -> rows (n, oh, ow) x columns k = c*T + tap for
+//   the first Ca channels (T = KH*KW taps, zero padding).  Channel-major
+//   columns make the first Ca input channels of a filter a prefix of its row,
+//   which is what a narrower mode reads (Eq. 7).  One thread per (row, 8
+//   channels): T 16-byte reads, T 16-byte writes.
+// * im2col_nchw: the stem's rows from NCHW images (any channel count), row
+//   length padded with zeros to a multiple of 8.
+// * max_pool_3x3_s2: 3x3 window, stride 2, padding 1, NHWC, 8 channels per
+//   thread.
+// * avg_pool: mean over all pixels of each image, fp32 sums, bf16 out.
+#include "common.h"
+#include "kernels.h"
+
+namespace elasto {
+namespace {
+
+inline unsigned grid_for(int64_t n, int block) { return (unsigned)((n + block - 1) / block); }
+
+template <int KH, int KW>
+__global__ __launch_bounds__(256) void im2col_nhwc_kernel(const uint16_t* __restrict__ x, int H,
+                                                          int W, int Cs, int Ca, int stride,
+                                                          int pad, int Ho, int Wo, int64_t rows,
+                                                          uint16_t* __restrict__ out) {
+  constexpr int T = KH * KW;
+  const int c8n = Ca / 8;
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= rows * c8n) return;
+  const int64_t m = id / c8n;
+  const int c8 = (int)(id - m * c8n);
+  const int64_t n = m / ((int64_t)Ho * Wo);
+  const int r = (int)(m - n * Ho * Wo), oh = r / Wo, ow = r - oh * Wo;
+  u32x4 v[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int ih = oh * stride - pad + t / KW, iw = ow * stride - pad + t % KW;
+    if (ih >= 0 && ih < H && iw >= 0 && iw < W)
+      v[t] = *reinterpret_cast<const u32x4*>(x + ((n * H + ih) * W + iw) * (int64_t)Cs + c8 * 8);
+    else
+      v[t] = u32x4{0u, 0u, 0u, 0u};
+  }
+  // Output element q of this thread's run (q = c*T + t) is channel c of tap t.
+  uint16_t* o = out + m * (int64_t)(Ca * T) + (int64_t)c8 * 8 * T;
+#pragma unroll
+  for (int j = 0; j < T; ++j) {
+    u32x4 w;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int q0 = 8 * j + 2 * h, q1 = q0 + 1;
+      const uint32_t e0 = (v[q0 % T][(q0 / T) >> 1] >> (16 * ((q0 / T) & 1))) & 0xffffu;
+      const uint32_t e1 = (v[q1 % T][(q1 / T) >> 1] >> (16 * ((q1 / T) & 1))) & 0xffffu;
+      w[h] = e0 | (e1 << 16);
+    }
+    *reinterpret_cast<u32x4*>(o + 8 * j) = w;
+  }
+}
+
+__global__ __launch_bounds__(256) void im2col_nchw_kernel(const uint16_t* __restrict__ img, int C,
+                                                          int H, int W, int KH, int KW,
+                                                          int stride, int pad, int Ho, int Wo,
+                                                          int64_t rows, int kpad,
+                                                          uint16_t* __restrict__ out) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= rows) return;
+  const int64_t n = m / ((int64_t)Ho * Wo);
+  const int r = (int)(m - n * Ho * Wo), oh = r / Wo, ow = r - oh * Wo;
+  uint16_t* o = out + m * (int64_t)kpad;
+  int k = 0;
+  for (int c = 0; c < C; ++c)
+    for (int i = 0; i < KH; ++i)
+      for (int j = 0; j < KW; ++j, ++k) {
+        const int ih = oh * stride - pad + i, iw = ow * stride - pad + j;
+        o[k] = (ih >= 0 && ih < H && iw >= 0 && iw < W)
+                   ? img[((n * C + c) * H + ih) * (int64_t)W + iw]
+                   : (uint16_t)0;
+      }
+  for (; k < kpad; ++k) o[k] = 0;
+}
+
+__global__ __launch_bounds__(256) void max_pool_kernel(const uint16_t* __restrict__ x, int H, int W,
+                                                       int C, int Ho, int Wo, int64_t outs,
+                                                       uint16_t* __restrict__ y) {
+  const int c8n = C / 8;
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= outs * c8n) return;
+  const int64_t m = id / c8n;
+  const int c8 = (int)(id - m * c8n);
+  const int64_t n = m / ((int64_t)Ho * Wo);
+  const int r = (int)(m - n * Ho * Wo), oh = r / Wo, ow = r - oh * Wo;
+  float mx[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) mx[e] = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 3; ++i)
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const int ih = 2 * oh - 1 + i, iw = 2 * ow - 1 + j;
+      if (ih < 0 || ih >= H || iw < 0 || iw >= W) continue;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(x + ((n * H + ih) * W + iw) * (int64_t)C +
+                                                      c8 * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        mx[e] = fmaxf(mx[e], __uint_as_float((e & 1) ? (v[e >> 1] & 0xffff0000u)
+                                                      : (v[e >> 1] << 16)));
+    }
+  u32x4 w;
+#pragma unroll
+  for (int h = 0; h < 4; ++h)
+    w[h] = (uint32_t)f32_to_bf16(mx[2 * h]) | ((uint32_t)f32_to_bf16(mx[2 * h + 1]) << 16);
+  *reinterpret_cast<u32x4*>(y + m * (int64_t)C + c8 * 8) = w;
+}
+
+__global__ __launch_bounds__(256) void avg_pool_kernel(const uint16_t* __restrict__ x, int HW,
+                                                       int C, int batch,
+                                                       uint16_t* __restrict__ y) {
+  const int c8n = C / 8;
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= (int64_t)batch * c8n) return;
+  const int n = (int)(id / c8n), c8 = (int)(id - (int64_t)n * c8n);
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const uint16_t* p = x + (int64_t)n * HW * C + c8 * 8;
+  for (int i = 0; i < HW; ++i) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p + (int64_t)i * C);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      s[e] += __uint_as_float((e & 1) ? (v[e >> 1] & 0xffff0000u) : (v[e >> 1] << 16));
+  }
+  const float inv = 1.0f / (float)HW;
+  u32x4 w;
+#pragma unroll
+  for (int h = 0; h < 4; ++h)
+    w[h] = (uint32_t)f32_to_bf16(s[2 * h] * inv) | ((uint32_t)f32_to_bf16(s[2 * h + 1] * inv) << 16);
+  *reinterpret_cast<u32x4*>(y + (int64_t)n * C + c8 * 8) = w;
+}
+
+}  // namespace
+
+hipError_t launch_im2col_nhwc(const void* x, int batch, int H, int W, int Cs, int Ca, int KH,
+                              int KW, int stride, int pad, void* out, hipStream_t s) {
+  if ((Ca & 7) != 0 || (Cs & 7) != 0 || Ca > Cs) return hipErrorInvalidValue;
+  const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
+  const int64_t rows = (int64_t)batch * Ho * Wo, work = rows * (Ca / 8);
+  if (work <= 0) return hipSuccess;
+  const auto* xp = static_cast<const uint16_t*>(x);
+  auto* op = static_cast<uint16_t*>(out);
+  if (KH == 3 && KW == 3)
+    hipLaunchKernelGGL((im2col_nhwc_kernel<3, 3>), dim3(grid_for(work, 256)), dim3(256), 0, s, xp,
+                       H, W, Cs, Ca, stride, pad, Ho, Wo, rows, op);
+  else if (KH == 1 && KW == 1)
+    hipLaunchKernelGGL((im2col_nhwc_kernel<1, 1>), dim3(grid_for(work, 256)), dim3(256), 0, s, xp,
+                       H, W, Cs, Ca, stride, pad, Ho, Wo, rows, op);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, int KH, int KW,
+                              int stride, int pad, int kpad, void* out, hipStream_t s) {
+  const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
+  const int64_t rows = (int64_t)batch * Ho * Wo;
+  if (rows <= 0) return hipSuccess;
+  if (kpad < C * KH * KW) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(im2col_nchw_kernel, dim3(grid_for(rows, 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(img), C, H, W, KH, KW, stride, pad, Ho, Wo, rows,
+                     kpad, static_cast<uint16_t*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_max_pool_3x3_s2(const void* x, int batch, int H, int W, int C, void* y,
+                                  hipStream_t s) {
+  if ((C & 7) != 0) return hipErrorInvalidValue;
+  const int Ho = (H - 1) / 2 + 1, Wo = (W - 1) / 2 + 1;
+  const int64_t outs = (int64_t)batch * Ho * Wo, work = outs * (C / 8);
+  if (work <= 0) return hipSuccess;
+  hipLaunchKernelGGL(max_pool_kernel, dim3(grid_for(work, 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(x), H, W, C, Ho, Wo, outs,
+                     static_cast<uint16_t*>(y));
+  return hipGetLastError();
+}
+
+hipError_t launch_avg_pool(const void* x, int batch, int HW, int C, void* y, hipStream_t s) {
+  if ((C & 7) != 0) return hipErrorInvalidValue;
+  const int64_t work = (int64_t)batch * (C / 8);
+  if (work <= 0) return hipSuccess;
+  hipLaunchKernelGGL(avg_pool_kernel, dim3(grid_for(work, 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(x), HW, C, batch, static_cast<uint16_t*>(y));
+  return hipGetLastError();
+}
+
+}  // namespace elasto

@@ -56,6 +56,7 @@ struct Params {
   int row0;     // this launch covers rows [row0, M)
   int tiles_n;
   int group_m;  // row panels per rasterisation group
+  int relu;     // Bias / BiasResid: clamp the bf16 result at 0 (convolution blocks)
 };
 
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
@@ -371,6 +372,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           continue;
         }
       }
+      if constexpr (E == Epi::Bias || E == Epi::BiasResid) {
+        if (p.relu) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.0f);
+        }
+      }
       if (full) {
         u32x4 w;
 #pragma unroll
@@ -471,6 +478,7 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.pos = a.pos;
   p.ldpos = a.ldpos > 0 ? a.ldpos : a.N;
   p.ccls = a.ccls;
+  p.relu = a.relu ? 1 : 0;
   switch (epi) {
     case Epi::Bias: return launch_epi<Epi::Bias>(p, s);
     case Epi::BiasGelu: return launch_epi<Epi::BiasGelu>(p, s);

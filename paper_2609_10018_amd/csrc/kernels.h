@@ -38,6 +38,7 @@ struct GemmArgs {
   const float* pos = nullptr;
   int64_t ldpos = 0;  // row stride of pos (elements); 0: N
   float* ccls = nullptr;
+  bool relu = false;  // bf16 Bias / BiasResid epilogues: max(result, 0)
 };
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
@@ -67,5 +68,14 @@ hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
 // Largest token count the bf16 attention kernel supports (K and V^T of one
 // head are staged whole in LDS).
 constexpr int kAttnMaxTokens = 240;
+
+// Elastic bottleneck-ResNet data movement (conv.hip).  NHWC bf16.
+hipError_t launch_im2col_nhwc(const void* x, int batch, int H, int W, int Cs, int Ca, int KH,
+                              int KW, int stride, int pad, void* out, hipStream_t s);
+hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, int KH, int KW,
+                              int stride, int pad, int kpad, void* out, hipStream_t s);
+hipError_t launch_max_pool_3x3_s2(const void* x, int batch, int H, int W, int C, void* y,
+                                  hipStream_t s);
+hipError_t launch_avg_pool(const void* x, int batch, int HW, int C, void* y, hipStream_t s);
 
 }  // namespace elasto

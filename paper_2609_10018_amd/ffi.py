@@ -66,6 +66,21 @@ class DNLut(ctypes.Structure):
                 ("accuracy", ctypes.POINTER(c_f64)), ("power_w", ctypes.POINTER(c_f64))]
 
 
+class CNNConfig(ctypes.Structure):
+    _fields_ = [("img", c_i32), ("in_chans", c_i32), ("stem", c_i32), ("num_stages", c_i32),
+                ("widths", c_i32 * 8), ("blocks", c_i32 * 8), ("expansion", c_i32),
+                ("num_classes", c_i32), ("max_batch", c_i32), ("dtype", c_i32)]
+
+
+class CNNWeights(ctypes.Structure):
+    _fields_ = [("num_tensors", c_i32), ("tensors", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class CNNTableC(ctypes.Structure):
+    _fields_ = [("num_modes", c_i32), ("num_blocks", c_i32), ("n_width", c_vp),
+                ("order1", c_vp), ("order2", c_vp)]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -102,6 +117,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "elasto_select_mode": [P(DNLut), c_f64, c_f64, c_f64, c_f64, P(c_i32)],
         "elasto_profile_modes": [c_vp, c_vp, c_i32, c_vp, c_i32, c_i32, c_vp, P(c_f64), P(c_f64),
                                  P(c_f64)],
+        "elasto_cnn_validate": [P(CNNConfig), P(CNNTableC)],
+        "elasto_cnn_create": [P(CNNConfig), P(CNNWeights), P(CNNTableC), P(c_vp)],
+        "elasto_cnn_destroy": [c_vp],
+        "elasto_cnn_set_mode": [c_vp, c_i32],
+        "elasto_cnn_get_mode": [c_vp, P(c_i32)],
+        "elasto_cnn_forward": [c_vp, c_vp, c_i32, c_vp, c_vp],
+        "elasto_cnn_mode_info": [c_vp, c_i32, P(c_f64), P(c_i64)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -290,6 +312,78 @@ def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int,
                                              _stream_ptr(stream)))
 
 
+class _HostCNN:
+    """Keeps the host arrays alive while the C structs point at them."""
+
+    def __init__(self, cfg, w, table, max_batch: int):
+        from .inputs_cnn import conv_shapes
+        self.cfg = CNNConfig()
+        self.cfg.img, self.cfg.in_chans, self.cfg.stem = cfg.img, cfg.in_chans, cfg.stem
+        self.cfg.num_stages = len(cfg.widths)
+        for i, (wd, nb) in enumerate(zip(cfg.widths, cfg.blocks)):
+            self.cfg.widths[i], self.cfg.blocks[i] = wd, nb
+        self.cfg.expansion, self.cfg.num_classes = cfg.expansion, cfg.num_classes
+        self.cfg.max_batch, self.cfg.dtype = max_batch, cfg.dtype
+        self.tensors = [] if w is None else [
+            np.ascontiguousarray(w[key], dtype=np.float32) for key in conv_shapes(cfg)]
+        self.ptrs = (ctypes.c_void_p * max(1, len(self.tensors)))(
+            *[t.ctypes.data for t in self.tensors])
+        self.weights = CNNWeights(len(self.tensors), self.ptrs)
+        self.n_width = np.ascontiguousarray(table.n_width, dtype=np.int32)
+        self.order1 = np.ascontiguousarray(np.concatenate(table.order1), dtype=np.int32)
+        self.order2 = np.ascontiguousarray(np.concatenate(table.order2), dtype=np.int32)
+        self.table = CNNTableC(int(self.n_width.shape[0]), int(self.n_width.shape[1]),
+                               self.n_width.ctypes.data, self.order1.ctypes.data,
+                               self.order2.ctypes.data)
+
+
+def cnn_validate(cfg, table, max_batch: int = 1) -> int:
+    hc = _HostCNN(cfg, None, table, max_batch)
+    return load_library().elasto_cnn_validate(ctypes.byref(hc.cfg), ctypes.byref(hc.table))
+
+
+class ElasticResNet:
+    """One elastic bottleneck-ResNet handle (bf16, NHWC on the device)."""
+
+    def __init__(self, cfg, w, table, max_batch: int):
+        self.lib = load_library()
+        self.cfg = cfg
+        self.num_modes = int(table.n_width.shape[0])
+        hc = _HostCNN(cfg, w, table, max_batch)
+        h = c_vp()
+        check(self.lib.elasto_cnn_create(ctypes.byref(hc.cfg), ctypes.byref(hc.weights),
+                                         ctypes.byref(hc.table), ctypes.byref(h)))
+        self.h = h
+
+    def close(self) -> None:
+        if getattr(self, "h", None) is not None and self.h.value:
+            check(self.lib.elasto_cnn_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_mode(self, k: int) -> None:
+        check(self.lib.elasto_cnn_set_mode(self.h, int(k)))
+
+    def get_mode(self) -> int:
+        k = c_i32()
+        check(self.lib.elasto_cnn_get_mode(self.h, ctypes.byref(k)))
+        return k.value
+
+    def forward(self, images, logits, stream=None) -> None:
+        check(self.lib.elasto_cnn_forward(self.h, images.data_ptr(), int(images.shape[0]),
+                                          logits.data_ptr(), _stream_ptr(stream)))
+
+    def mode_info(self, k: int):
+        f, b = c_f64(), c_i64()
+        check(self.lib.elasto_cnn_mode_info(self.h, int(k), ctypes.byref(f), ctypes.byref(b)))
+        return f.value, b.value
+
+
 def select_mode(flops, latency_ms, memory_bytes, accuracy=None, power_w=None,
                 max_latency_ms=math.inf, max_memory_bytes=math.inf, min_accuracy=-math.inf,
                 max_power_w=math.inf):
@@ -313,6 +407,6 @@ def select_mode(flops, latency_ms, memory_bytes, accuracy=None, power_w=None,
     return k.value
 
 
-__all__ = ["ElasticViT", "select_mode", "ElastoError", "load_library", "validate", "packed_bytes",
+__all__ = ["ElasticViT", "ElasticResNet", "cnn_validate", "select_mode", "ElastoError", "load_library", "validate", "packed_bytes",
            "packed_layout", "pack_weights", "op_layernorm", "op_linear", "op_attention",
            "KERNELS", "FP32", "BF16"]

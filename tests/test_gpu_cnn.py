@@ -1,0 +1,140 @@
+"""Parity of the elastic ResNet forward (through the C ABI) with the fp64
+oracle: every DN mode of both ResNet configs, small batches, the prefix-read
+(NaN-poison) test and repeated calls."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import resnet as orn
+from paper_2609_10018_amd import ffi, inputs
+from paper_2609_10018_amd.inputs_cnn import (CNN_CONFIGS, make_cnn_images, make_cnn_table,
+                                             make_cnn_weights, stored_cnn_weights)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from gpu_util import rel_err, top1_agreement  # noqa: E402
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+BF16_TOL = 2e-2
+# The image-dependent part of the logits (logits minus their batch mean) is
+# only 4-20% of their magnitude on these random networks (white-noise images
+# through random filters): bf16 rounding of the common part (2^-9 relative)
+# is then up to ~5% of it.  It is still checked on its own scale, at 0.1,
+# which a mix-up of images or channels would exceed many times over.
+CENTERED_TOL = 1e-1
+
+
+def centered_err(got, ref):
+    g = np.asarray(got, np.float64) - np.asarray(got, np.float64).mean(axis=0)
+    r = np.asarray(ref, np.float64) - np.asarray(ref, np.float64).mean(axis=0)
+    return rel_err(g, r)
+
+
+class Net:
+    def __init__(self, name, weights=None, max_batch=None):
+        self.cfg = CNN_CONFIGS[name]
+        self.w = weights if weights is not None else make_cnn_weights(self.cfg)
+        self.table = make_cnn_table(self.cfg)
+        self.max_batch = max_batch or self.cfg.batch
+        self.net = ffi.ElasticResNet(self.cfg, self.w, self.table, self.max_batch)
+        self.x = make_cnn_images(self.cfg, self.max_batch)
+        self.xd = torch.from_numpy(self.x).to(torch.bfloat16).cuda().contiguous()
+
+    def run(self, k, batch=None):
+        batch = batch or self.max_batch
+        self.net.set_mode(k)
+        logits = torch.empty((batch, self.cfg.num_classes), dtype=torch.float32, device="cuda")
+        self.net.forward(self.xd[:batch], logits)
+        torch.cuda.synchronize()
+        return logits.cpu().numpy()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ffi.load_library()
+
+
+_nets = {}
+
+
+def net(name):
+    if name not in _nets:
+        _nets[name] = Net(name)
+    return _nets[name]
+
+
+def test_resnet_small_all_modes_match_oracle():
+    n = net("resnet_small")
+    w = stored_cnn_weights(n.cfg, n.w)
+    x = inputs.bf16_round(n.x)
+    for k in range(n.table.num_modes):
+        got = n.run(k)
+        ref = orn.elastic_forward(w, n.cfg, n.table, k, x)
+        err, cerr = rel_err(got, ref), centered_err(got, ref)
+        print(f"resnet_small mode {k}: rel err {err:.3e}, centered {cerr:.3e}")
+        assert np.isfinite(got).all()
+        assert err <= BF16_TOL and cerr <= CENTERED_TOL
+
+
+def test_resnet50_all_modes_match_golden():
+    n = net("resnet50")
+    gold = np.load(os.path.join(GOLDEN, "logits_resnet50.npz"))["logits"]
+    m = gold.shape[1]
+    for k in range(n.table.num_modes):
+        got = n.run(k)[:m]
+        err, cerr = rel_err(got, gold[k]), centered_err(got, gold[k])
+        raw, tie = top1_agreement(got, gold[k])
+        print(f"resnet50 mode {k}: rel err {err:.3e}, centered {cerr:.3e}, top-1 {raw:.3f}/{tie:.3f}")
+        assert np.isfinite(got).all()
+        assert err <= BF16_TOL and cerr <= CENTERED_TOL
+        assert tie >= 0.995
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+def test_resnet50_small_batches(batch):
+    n = net("resnet50")
+    gold = np.load(os.path.join(GOLDEN, "logits_resnet50.npz"))["logits"]
+    for k in (0, 5):
+        got = n.run(k, batch)
+        assert rel_err(got, gold[k][:batch]) <= BF16_TOL
+        np.testing.assert_array_equal(n.run(k, batch), got)
+
+
+def test_cnn_mode_info_matches_cost_model():
+    from paper_2609_10018_amd import cost
+    n = net("resnet50")
+    for k in range(n.table.num_modes):
+        macs, wbytes = n.net.mode_info(k)
+        assert macs == cost.cnn_macs(n.cfg, n.table, k)
+
+
+def _poison_inactive(w, cfg, table, k):
+    """Copy of w with every pruned filter of mode k (and the kernels reading
+    its channel) = NaN."""
+    p = {key: np.array(v, copy=True) for key, v in w.items()}
+    for i, spec in enumerate(cfg.block_specs()):
+        a1, a2 = orn.active_filters(table, k, i)
+        off1 = np.setdiff1d(np.arange(spec["width"]), a1)
+        off2 = np.setdiff1d(np.arange(spec["width"]), a2)
+        p[f"b{i}_c1_w"][off1] = np.nan
+        p[f"b{i}_c1_b"][off1] = np.nan
+        p[f"b{i}_c2_w"][:, off1] = np.nan
+        p[f"b{i}_c2_w"][off2] = np.nan
+        p[f"b{i}_c2_b"][off2] = np.nan
+        p[f"b{i}_c3_w"][:, off2] = np.nan
+    return p
+
+
+@pytest.mark.parametrize("name,k", [("resnet_small", 3), ("resnet50", 5)])
+def test_cnn_prefix_read_nan_poison(name, k):
+    clean = net(name)
+    ref = clean.run(k, 4)
+    poisoned = Net(name, weights=_poison_inactive(clean.w, clean.cfg, clean.table, k), max_batch=4)
+    got = poisoned.run(k)
+    poisoned.net.close()
+    assert np.isfinite(got).all()
+    np.testing.assert_array_equal(got, ref)
