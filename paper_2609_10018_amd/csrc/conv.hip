@@ -7,8 +7,9 @@
 //   columns make the first Ca input channels of a filter a prefix of its row,
 //   which is what a narrower mode reads (Eq. 7).  One thread per (row, 8
 //   channels): T 16-byte reads, T 16-byte writes.
-// * im2col_nchw: the stem's rows from NCHW images (any channel count), row
-//   length padded with zeros to a multiple of 8.
+// * im2col_nchw: the stem's 7x7 rows from NCHW images (any channel count),
+//   row length padded with zeros to a multiple of 8; one thread per 8
+//   columns (one 16-byte store).
 // * max_pool_3x3_s2: 3x3 window, stride 2, padding 1, NHWC, 8 channels per
 //   thread.
 // * avg_pool: mean over all pixels of each image, fp32 sums, bf16 out.
@@ -58,26 +59,31 @@ __global__ __launch_bounds__(256) void im2col_nhwc_kernel(const uint16_t* __rest
   }
 }
 
+// One thread per (row, 8 consecutive columns): columns k = c*KH*KW + tap.
+template <int KH, int KW>
 __global__ __launch_bounds__(256) void im2col_nchw_kernel(const uint16_t* __restrict__ img, int C,
-                                                          int H, int W, int KH, int KW,
-                                                          int stride, int pad, int Ho, int Wo,
-                                                          int64_t rows, int kpad,
+                                                          int H, int W, int stride, int pad,
+                                                          int Ho, int Wo, int64_t rows, int kpad,
                                                           uint16_t* __restrict__ out) {
-  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= rows) return;
+  constexpr int T = KH * KW;
+  const int chunks = kpad / 8;
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= rows * chunks) return;
+  const int64_t m = id / chunks;
+  const int j = (int)(id - m * chunks);
   const int64_t n = m / ((int64_t)Ho * Wo);
   const int r = (int)(m - n * Ho * Wo), oh = r / Wo, ow = r - oh * Wo;
-  uint16_t* o = out + m * (int64_t)kpad;
-  int k = 0;
-  for (int c = 0; c < C; ++c)
-    for (int i = 0; i < KH; ++i)
-      for (int j = 0; j < KW; ++j, ++k) {
-        const int ih = oh * stride - pad + i, iw = ow * stride - pad + j;
-        o[k] = (ih >= 0 && ih < H && iw >= 0 && iw < W)
-                   ? img[((n * C + c) * H + ih) * (int64_t)W + iw]
-                   : (uint16_t)0;
-      }
-  for (; k < kpad; ++k) o[k] = 0;
+  uint32_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int k = 8 * j + e, c = k / T, t = k - c * T, i = t / KW, jj = t - i * KW;
+    const int ih = oh * stride - pad + i, iw = ow * stride - pad + jj;
+    h[e] = (c < C && ih >= 0 && ih < H && iw >= 0 && iw < W)
+               ? img[((n * C + c) * H + ih) * (int64_t)W + iw]
+               : 0u;
+  }
+  *reinterpret_cast<u32x4*>(out + m * (int64_t)kpad + 8 * j) =
+      u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
 }
 
 __global__ __launch_bounds__(256) void max_pool_kernel(const uint16_t* __restrict__ x, int H, int W,
@@ -162,10 +168,11 @@ hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, i
   const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
   const int64_t rows = (int64_t)batch * Ho * Wo;
   if (rows <= 0) return hipSuccess;
-  if (kpad < C * KH * KW) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(im2col_nchw_kernel, dim3(grid_for(rows, 256)), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(img), C, H, W, KH, KW, stride, pad, Ho, Wo, rows,
-                     kpad, static_cast<uint16_t*>(out));
+  if (kpad < C * KH * KW || kpad % 8 != 0 || KH != 7 || KW != 7) return hipErrorInvalidValue;
+  const int64_t work = rows * (kpad / 8);
+  hipLaunchKernelGGL((im2col_nchw_kernel<7, 7>), dim3(grid_for(work, 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(img), C, H, W, stride, pad, Ho, Wo, rows, kpad,
+                     static_cast<uint16_t*>(out));
   return hipGetLastError();
 }
 

@@ -424,10 +424,13 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
   constexpr double kRel128x256 = 0.6;
   auto rounds = [](int64_t tiles) { return (double)((tiles + kCUs - 1) / kCUs); };
   struct Cfg { int bm, bn; double rel; };
-  const Cfg cfgs[3] = {{256, 256, 1.0}, {256, 128, 0.62}, {128, 128, 0.36}};
+  // 256x64 (four waves stacked along M) only for outputs at most 64 wide,
+  // where wider tiles would leave half their columns idle.
+  const Cfg cfgs[4] = {{256, 256, 1.0}, {256, 128, 0.62}, {128, 128, 0.36}, {256, 64, 0.3}};
+  const int ncfg = p.N <= 64 ? 4 : 3;
   int best = 0;
   double best_t = 1e300;
-  for (int i = 0; i < 3; ++i) {
+  for (int i = 0; i < ncfg; ++i) {
     const int64_t tiles = ((p.M + cfgs[i].bm - 1) / cfgs[i].bm) * ((p.N + cfgs[i].bn - 1) / cfgs[i].bn);
     const double t = rounds(tiles) * cfgs[i].rel;
     if (t < best_t - 1e-9) { best_t = t; best = i; }
@@ -448,7 +451,8 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
   switch (best) {
     case 0: return launch_cfg<256, 256, 2, 4, E>(p, 0, s);
     case 1: return launch_cfg<256, 128, 2, 2, E>(p, 0, s);
-    default: return launch_cfg<128, 128, 2, 2, E>(p, 0, s);
+    case 2: return launch_cfg<128, 128, 2, 2, E>(p, 0, s);
+    default: return launch_cfg<256, 64, 4, 1, E>(p, 0, s);
   }
 }
 

@@ -129,6 +129,9 @@ LINEAR_CASES = [
     # enough 256x256 tiles for a second, 128x256-tile launch over the last rows
     (BF16, ffi.EPI_BIAS_GELU, 21999, 3072, 768, 768, 768, 3072),
     (BF16, ffi.EPI_BIAS_RESID, 22000, 768, 3072, 3072, 3072, 768),
+    # outputs at most 64 wide: 256x64 tiles
+    (BF16, ffi.EPI_BIAS, 3001, 64, 256, 256, 256, 64),
+    (BF16, ffi.EPI_BIAS_RESID, 777, 40, 576, 576, 576, 48),
     (FP32, ffi.EPI_BIAS, 68, 192, 64, 64, 64, 192),
     (FP32, ffi.EPI_BIAS_GELU, 70, 67, 61, 64, 61, 128),
     (FP32, ffi.EPI_BIAS_RESID, 68, 64, 33, 64, 128, 64),
