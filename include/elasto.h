@@ -339,6 +339,24 @@ elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_
                                     int32_t heads, int32_t head_dim, float scale,
                                     void* hip_stream);
 
+/* Convolution of an NHWC bf16 batch, as the elastic ResNet's 3x3 and strided
+ * 1x1 layers run it (Section 4.1; a DN mode keeps a prefix of the input
+ * channels, i.e. Eq. 7's kernel masks, and reads the first `ca` channels of
+ * every tap):
+ *   y[(b*Ho + oh)*Wo + ow][j] = relu?(bias[j] + sum over i < kh, jj < kw,
+ *       c < ca of x[((b*H + ih)*W + iw)*cs + c] * w[j*ldw + (i*kw + jj)*wseg + c])
+ * with ih = oh*stride - pad + i, iw = ow*stride - pad + jj, zero outside the
+ * image, Ho = (H + 2*pad - kh)/stride + 1 (Wo likewise), j < n; row stride of
+ * y is ldy.  bf16 x, w, y; fp32 bias and accumulation.  cs, ca, wseg, ldw and
+ * ldy are multiples of 8, 8 <= ca <= min(cs, wseg), ldw >= kh*kw*wseg, and x,
+ * w, y, bias are 16-byte aligned; one image's input and the read part of w
+ * must each stay below 2 GiB.  Channels of x at or past ca, and entries of w
+ * past ca within each tap segment, are never used. */
+elasto_status_t elasto_op_conv2d(const void* x, int32_t batch, int32_t H, int32_t W, int32_t cs,
+                                 int32_t ca, int32_t kh, int32_t kw, int32_t stride, int32_t pad,
+                                 const void* w, int64_t ldw, int64_t wseg, const float* bias,
+                                 void* y, int64_t ldy, int32_t n, int32_t relu, void* hip_stream);
+
 /* ======================================== elastic bottleneck ResNet (CNN) */
 /* The paper applies the same elastic transformation to CNNs (Eq. 7 masks
  * whole convolution kernels; Table 2 reports ResNet-50 DNs).  This is the

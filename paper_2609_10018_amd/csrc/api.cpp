@@ -565,6 +565,37 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
   return ELASTO_OK;
 }
 
+elasto_status_t elasto_op_conv2d(const void* x, int32_t batch, int32_t H, int32_t W, int32_t cs,
+                                 int32_t ca, int32_t kh, int32_t kw, int32_t stride, int32_t pad,
+                                 const void* w, int64_t ldw, int64_t wseg, const float* bias,
+                                 void* y, int64_t ldy, int32_t n, int32_t relu, void* hip_stream) {
+  if (!x || !w || !bias || !y) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if (batch < 0 || H < 1 || W < 1 || kh < 1 || kw < 1 || stride < 1 || pad < 0 || n < 1 ||
+      H + 2 * pad < kh || W + 2 * pad < kw)
+    return fail(ELASTO_ERR_INVALID_ARG, "bad convolution sizes");
+  if (ca < 8 || ca % 8 || cs % 8 || ca > cs || wseg < ca || wseg % 8 || ldw % 8 ||
+      ldw < (int64_t)kh * kw * wseg || ldy < n || ldy % 8)
+    return fail(ELASTO_ERR_INVALID_ARG,
+                "convolution needs cs, ca, wseg, ldw, ldy %% 8 == 0, 8 <= ca <= min(cs, wseg), "
+                "ldw >= kh*kw*wseg, ldy >= n");
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16) || !aligned(bias, 16))
+    return fail(ELASTO_ERR_INVALID_ARG, "convolution needs 16-byte aligned x, w, y, bias");
+  const int64_t limit = ((int64_t)1 << 31) - 1;
+  if ((int64_t)H * W * cs * 2 > limit || ((int64_t)(n - 1) * ldw + (int64_t)kh * kw * wseg) * 2 > limit)
+    return fail(ELASTO_ERR_INVALID_ARG, "one image's input or the read weights exceed 2 GiB");
+  const int64_t ho = (H + 2 * pad - kh) / stride + 1, wo = (W + 2 * pad - kw) / stride + 1;
+  if ((int64_t)batch * ho * wo >= ((int64_t)1 << 31))
+    return fail(ELASTO_ERR_INVALID_ARG, "too many output pixels");
+  ConvArgs a;
+  a.x = x; a.batch = batch; a.H = H; a.W = W; a.Cs = cs; a.Ca = ca;
+  a.KH = kh; a.KW = kw; a.stride = stride; a.pad = pad;
+  a.weight = w; a.ldw = ldw; a.wseg = wseg;
+  a.C = y; a.ldc = ldy; a.bias = bias; a.N = n; a.relu = relu != 0;
+  const hipError_t e = launch_conv_bf16(a, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "conv2d: %s", hipGetErrorString(e));
+  return ELASTO_OK;
+}
+
 elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_stride, void* o,
                                     int64_t o_stride, int32_t batch, int32_t tokens,
                                     int32_t heads, int32_t head_dim, float scale,

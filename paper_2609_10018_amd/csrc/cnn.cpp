@@ -6,9 +6,11 @@
 //   3x3 stride-2 max pool                                       -> cur
 //   per bottleneck b:
 //     1x1 reduce: GEMM over cur, N = n (prefix of order1) + ReLU -> t1
-//     3x3: patch matrix of t1's first n channels (k = c*9 + tap), GEMM with
-//          K = 9n (prefix of each packed filter row), N = n (order2) + ReLU -> t2
-//     shortcut: cur, or a 1x1 (strided) projection GEMM        -> other
+//     3x3: implicit-GEMM convolution over t1's first n channels (K runs
+//          over the 9 taps, each reading the first n entries of its segment
+//          of the packed filter row), N = n (order2) + ReLU          -> t2
+//     shortcut: cur, or a 1x1 projection (implicit convolution when
+//          strided)                                              -> other
 //     1x1 expand: GEMM over t2, K = n, + shortcut, ReLU, in place into the
 //          shortcut buffer (which becomes cur)
 //   global average pool -> classifier GEMM (fp32 logits)
@@ -215,10 +217,10 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
       for (int c = 0; c < b.c_in; ++c) mat(o.c1w, (int64_t)j * b.c_in + c, c1w[(int64_t)o1[j] * b.c_in + c]);
       vec(o.c1b, j, c1b[o1[j]]);
     }
-    for (int j = 0; j < b.width; ++j) {  // 3x3: filter order2[j], input channel order1[i]
-      for (int i = 0; i < b.width; ++i)
-        for (int t = 0; t < 9; ++t)
-          mat(o.c2w, ((int64_t)j * b.width + i) * 9 + t,
+    for (int j = 0; j < b.width; ++j) {  // 3x3: filter order2[j], tap t, input channel order1[i]
+      for (int t = 0; t < 9; ++t)
+        for (int i = 0; i < b.width; ++i)
+          mat(o.c2w, ((int64_t)j * 9 + t) * b.width + i,
               c2w[(((int64_t)o2[j] * b.width) + o1[i]) * 9 + t]);
       vec(o.c2b, j, c2b[o2[j]]);
     }
@@ -245,8 +247,6 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
   int64_t col = B * hs * hs * h->stem_kpad, io = B * (hs / 2) * (hs / 2) * cfg->stem, t1 = 0, t2 = 0;
   for (const BlockSpec& b : bs) {
     const int64_t hi = b.hw_in, ho = b.hw_in / b.stride;
-    col = std::max(col, B * ho * ho * 9 * b.width);
-    if (b.down && b.stride > 1) col = std::max(col, B * ho * ho * b.c_in);
     io = std::max(io, B * ho * ho * b.c_out);
     t1 = std::max(t1, B * hi * hi * b.width);
     t2 = std::max(t2, B * ho * ho * b.width);
@@ -360,6 +360,19 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
     a.relu = relu;
     return launch_gemm_bf16(epi, a, s);
   };
+  // Square input (hw x hw, channel stride cs, first ca channels), ks x ks taps.
+  auto conv = [&](const void* x, int hw, int cs, int ca, int ks, int stride, int pad, int64_t wo,
+                  int64_t ldw, int64_t wseg, void* C, int64_t ldc, int64_t bo, int N, bool relu) {
+    ConvArgs a;
+    a.x = x; a.batch = batch; a.H = hw; a.W = hw; a.Cs = cs; a.Ca = ca;
+    a.KH = ks; a.KW = ks; a.stride = stride; a.pad = pad;
+    a.weight = Wp(wo); a.ldw = ldw; a.wseg = wseg;
+    a.C = C; a.ldc = ldc;
+    a.bias = Fp(bo);
+    a.N = N;
+    a.relu = relu;
+    return launch_conv_bf16(a, s);
+  };
   hipError_t e;
 #define ELASTO_TRY(call, what)                                                       \
   do {                                                                              \
@@ -383,20 +396,16 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
     const int64_t mi = B * hi * hi, mo = B * ho * ho;
     ELASTO_TRY(gemm(Epi::Bias, cur, b.c_in, o.c1w, b.c_in, h->t1, b.width, o.c1b, mi, n, b.c_in, true),
                "1x1 reduce");
-    ELASTO_TRY(launch_im2col_nhwc(h->t1, batch, hi, hi, b.width, n, 3, 3, b.stride, 1, h->col, s),
-               "3x3 patches");
-    ELASTO_TRY(gemm(Epi::Bias, h->col, 9 * n, o.c2w, 9 * b.width, h->t2, b.width, o.c2b, mo, n, 9 * n,
-                    true), "3x3");
+    ELASTO_TRY(conv(h->t1, hi, b.width, n, 3, b.stride, 1, o.c2w, 9 * b.width, b.width, h->t2,
+                    b.width, o.c2b, n, true), "3x3");
     void* shortcut = cur;
     if (b.down) {
-      const void* src = cur;
-      if (b.stride > 1) {
-        ELASTO_TRY(launch_im2col_nhwc(cur, batch, hi, hi, b.c_in, b.c_in, 1, 1, b.stride, 0, h->col, s),
-                   "projection rows");
-        src = h->col;
-      }
-      ELASTO_TRY(gemm(Epi::Bias, src, b.c_in, o.dnw, b.c_in, other, b.c_out, o.dnb, mo, b.c_out,
-                      b.c_in, false), "projection");
+      if (b.stride > 1)
+        ELASTO_TRY(conv(cur, hi, b.c_in, b.c_in, 1, b.stride, 0, o.dnw, b.c_in, b.c_in, other,
+                        b.c_out, o.dnb, b.c_out, false), "projection");
+      else
+        ELASTO_TRY(gemm(Epi::Bias, cur, b.c_in, o.dnw, b.c_in, other, b.c_out, o.dnb, mo, b.c_out,
+                        b.c_in, false), "projection");
       shortcut = other;
     }
     ELASTO_TRY(gemm(Epi::BiasResid, h->t2, b.width, o.c3w, b.width, shortcut, b.c_out, o.c3b, mo,

@@ -1,12 +1,8 @@
 // Data-movement kernels of the elastic bottleneck-ResNet path (Section 4.1's
 // CNN backbone, Table 2); the convolutions themselves run as bf16 MFMA GEMMs
-// (gemm_bf16.hip) over these operands.  Activations are NHWC bf16.
+// (gemm_bf16.hip, implicit for the 3x3 and strided 1x1 ones).  Activations
+// are NHWC bf16.
 //
-// * im2col_nhwc: [N,H,W,Cs] -> rows (n, oh, ow) x columns k = c*T + tap for
-//   the first Ca channels (T = KH*KW taps, zero padding).  Channel-major
-//   columns make the first Ca input channels of a filter a prefix of its row,
-//   which is what a narrower mode reads (Eq. 7).  One thread per (row, 8
-//   channels): T 16-byte reads, T 16-byte writes.
 // * im2col_nchw: the stem's 7x7 rows from NCHW images (any channel count),
 //   row length padded with zeros to a multiple of 8; one thread per 8
 //   columns (one 16-byte store).
@@ -20,44 +16,6 @@ namespace elasto {
 namespace {
 
 inline unsigned grid_for(int64_t n, int block) { return (unsigned)((n + block - 1) / block); }
-
-template <int KH, int KW>
-__global__ __launch_bounds__(256) void im2col_nhwc_kernel(const uint16_t* __restrict__ x, int H,
-                                                          int W, int Cs, int Ca, int stride,
-                                                          int pad, int Ho, int Wo, int64_t rows,
-                                                          uint16_t* __restrict__ out) {
-  constexpr int T = KH * KW;
-  const int c8n = Ca / 8;
-  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (id >= rows * c8n) return;
-  const int64_t m = id / c8n;
-  const int c8 = (int)(id - m * c8n);
-  const int64_t n = m / ((int64_t)Ho * Wo);
-  const int r = (int)(m - n * Ho * Wo), oh = r / Wo, ow = r - oh * Wo;
-  u32x4 v[T];
-#pragma unroll
-  for (int t = 0; t < T; ++t) {
-    const int ih = oh * stride - pad + t / KW, iw = ow * stride - pad + t % KW;
-    if (ih >= 0 && ih < H && iw >= 0 && iw < W)
-      v[t] = *reinterpret_cast<const u32x4*>(x + ((n * H + ih) * W + iw) * (int64_t)Cs + c8 * 8);
-    else
-      v[t] = u32x4{0u, 0u, 0u, 0u};
-  }
-  // Output element q of this thread's run (q = c*T + t) is channel c of tap t.
-  uint16_t* o = out + m * (int64_t)(Ca * T) + (int64_t)c8 * 8 * T;
-#pragma unroll
-  for (int j = 0; j < T; ++j) {
-    u32x4 w;
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const int q0 = 8 * j + 2 * h, q1 = q0 + 1;
-      const uint32_t e0 = (v[q0 % T][(q0 / T) >> 1] >> (16 * ((q0 / T) & 1))) & 0xffffu;
-      const uint32_t e1 = (v[q1 % T][(q1 / T) >> 1] >> (16 * ((q1 / T) & 1))) & 0xffffu;
-      w[h] = e0 | (e1 << 16);
-    }
-    *reinterpret_cast<u32x4*>(o + 8 * j) = w;
-  }
-}
 
 // One thread per (row, 8 consecutive columns): columns k = c*KH*KW + tap.
 template <int KH, int KW>
@@ -143,25 +101,6 @@ __global__ __launch_bounds__(256) void avg_pool_kernel(const uint16_t* __restric
 }
 
 }  // namespace
-
-hipError_t launch_im2col_nhwc(const void* x, int batch, int H, int W, int Cs, int Ca, int KH,
-                              int KW, int stride, int pad, void* out, hipStream_t s) {
-  if ((Ca & 7) != 0 || (Cs & 7) != 0 || Ca > Cs) return hipErrorInvalidValue;
-  const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
-  const int64_t rows = (int64_t)batch * Ho * Wo, work = rows * (Ca / 8);
-  if (work <= 0) return hipSuccess;
-  const auto* xp = static_cast<const uint16_t*>(x);
-  auto* op = static_cast<uint16_t*>(out);
-  if (KH == 3 && KW == 3)
-    hipLaunchKernelGGL((im2col_nhwc_kernel<3, 3>), dim3(grid_for(work, 256)), dim3(256), 0, s, xp,
-                       H, W, Cs, Ca, stride, pad, Ho, Wo, rows, op);
-  else if (KH == 1 && KW == 1)
-    hipLaunchKernelGGL((im2col_nhwc_kernel<1, 1>), dim3(grid_for(work, 256)), dim3(256), 0, s, xp,
-                       H, W, Cs, Ca, stride, pad, Ho, Wo, rows, op);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
-}
 
 hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, int KH, int KW,
                               int stride, int pad, int kpad, void* out, hipStream_t s) {

@@ -22,9 +22,19 @@
 // through registers instead, with every element at or past K zeroed in both
 // operands, so inactive weights never enter a product.
 //
+// Implicit convolution (CONV kernels): A is an NHWC bf16 activation and
+// output row m is pixel (image, oh, ow).  K walks the KH*KW taps, and within a
+// tap the first Ca input channels in steps of 64; W row j keeps tap t's
+// channels at j*ldw + t*wseg.  A and W land in LDS through range-checked
+// buffer loads: a 16-byte chunk whose pixel lies in the zero padding, or
+// whose channels are at or past Ca, gets an offset past the end of the
+// buffer and reads as zeros, so no patch matrix is ever written to memory.
+//
 // Workgroups are renumbered so that each XCD (workgroup i runs on XCD i % 8)
 // receives a contiguous run of tiles, ordered in groups of row panels so that
 // the tiles an XCD runs at the same time share A and W panels in its L2.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -57,7 +67,17 @@ struct Params {
   int tiles_n;
   int group_m;  // row panels per rasterisation group
   int relu;     // Bias / BiasResid: clamp the bf16 result at 0 (convolution blocks)
+  // Implicit convolution: input [*, H, W, Cs] (first Ca channels active),
+  // KH x KW taps (row-major), stride, zero padding, output Ho x Wo; weights
+  // stride wseg elements per tap; nc = 64-channel steps per tap; buffer
+  // sizes in bytes (each below 2^31) for the range checks.
+  int cv_H, cv_W, cv_Cs, cv_Ca, cv_KW, cv_T, cv_stride, cv_pad, cv_Ho, cv_Wo, cv_wseg, cv_nc;
+  int a_bytes, w_bytes;
 };
+
+// Buffer descriptor word 3 for raw (unswizzled, stride 0) buffers on CDNA.
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr unsigned kOutOfRange = 0x80000000u;  // at or past every buffer's size
 
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 
@@ -100,7 +120,7 @@ __device__ __forceinline__ u32x4 mask_tail(u32x4 v, int kbeg, int kend) {
   return o;
 }
 
-template <int BM, int BN, int WM, int WN, Epi E>
+template <int BM, int BN, int WM, int WN, Epi E, bool CONV>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -113,7 +133,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
   // Tile order: workgroup i runs on XCD i % 8, so each XCD first receives a
@@ -134,6 +155,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   const uint16_t* src[PER_WAVE];
   int chunk[PER_WAVE];
   int ldsoff[PER_WAVE];
+  // CONV: element offset of the row's tap-0 pixel (A) or of the weight row
+  // (W), and the tap-0 input coordinates (A).
+  int cbase[PER_WAVE], cih[PER_WAVE], ciw[PER_WAVE];
   const int prow = lane >> 3, pc = lane & 7;
 #pragma unroll
   for (int i = 0; i < PER_WAVE; ++i) {
@@ -143,7 +167,14 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       const int gm = min(m0 + r, p.M - 1);
       chunk[i] = pc ^ swz(r);
       ldsoff[i] = blk * 1024;
-      if constexpr (E == Epi::Patch) {
+      if constexpr (CONV) {
+        const int hw = p.cv_Ho * p.cv_Wo, im = gm / hw, rem = gm - im * hw;
+        const int oh = rem / p.cv_Wo, ow = rem - oh * p.cv_Wo;
+        cih[i] = oh * p.cv_stride - p.cv_pad;
+        ciw[i] = ow * p.cv_stride - p.cv_pad;
+        cbase[i] = ((im * p.cv_H + cih[i]) * p.cv_W + ciw[i]) * p.cv_Cs;
+        src[i] = nullptr;
+      } else if constexpr (E == Epi::Patch) {
         const int bi = gm / p.tokens, t = gm - bi * p.tokens;
         const int n = t > 0 ? t - 1 : 0, py = n / p.grid, px = n - py * p.grid;
         src[i] = p.img + ((int64_t)bi * p.chans * p.img_size + (int64_t)py * p.patch) * p.img_size +
@@ -156,6 +187,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       chunk[i] = pc ^ swz(r);
       ldsoff[i] = BM * kRowBytes + (blk - ABLK) * 1024;
       src[i] = p.W + (int64_t)min(n0 + r, p.N - 1) * p.ldw;
+      if constexpr (CONV) {
+        cbase[i] = min(n0 + r, p.N - 1) * (int)p.ldw;
+        cih[i] = ciw[i] = 0;
+      }
     }
   }
   // Element offset of k-index k within a source row (im2col for patches).
@@ -170,11 +205,35 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     return k;
   };
 
-  const int nk_full = p.K / kBK;
-  const int nk = (p.K + kBK - 1) / kBK;
+  const int nk_full = CONV ? p.cv_T * p.cv_nc : p.K / kBK;
+  const int nk = CONV ? nk_full : (p.K + kBK - 1) / kBK;
+  // Buffer descriptors of the CONV loads (unused otherwise).
+  const __amdgpu_buffer_rsrc_t rs_a =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.A), (short)0, p.a_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rs_w =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.W), (short)0, p.w_bytes, kRsrcWord3);
   auto issue = [&](int stage, int kt) {
     char* base = smem + stage * STAGE;
-    if (kt < nk_full) {
+    if constexpr (CONV) {
+      const int t = kt / p.cv_nc, c0 = (kt - t * p.cv_nc) * kBK;
+      const int ti = t / p.cv_KW, tj = t - ti * p.cv_KW;
+      const int tap = (ti * p.cv_W + tj) * p.cv_Cs, wtap = t * p.cv_wseg;
+#pragma unroll
+      for (int i = 0; i < PER_WAVE; ++i) {
+        const int ch = c0 + chunk[i] * 8;
+        if (wave * PER_WAVE + i < ABLK) {
+          const bool ok = ch < p.cv_Ca && (unsigned)(cih[i] + ti) < (unsigned)p.cv_H &&
+                          (unsigned)(ciw[i] + tj) < (unsigned)p.cv_W;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rs_a, (lds_void*)(base + ldsoff[i]), 16,
+              ok ? (unsigned)(cbase[i] + tap + ch) * 2u : kOutOfRange, 0, 0, 0);
+        } else {
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rs_w, (lds_void*)(base + ldsoff[i]), 16,
+              ch < p.cv_Ca ? (unsigned)(cbase[i] + wtap + ch) * 2u : kOutOfRange, 0, 0, 0);
+        }
+      }
+    } else if (kt < nk_full) {
 #pragma unroll
       for (int i = 0; i < PER_WAVE; ++i)
         __builtin_amdgcn_global_load_lds(
@@ -397,7 +456,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, Epi E>
+template <int BM, int BN, int WM, int WN, Epi E, bool CONV>
 hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   Params p = p0;
   p.row0 = row0;
@@ -408,12 +467,12 @@ hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   p.group_m = p.K >= 2048 ? 2 : 4;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E, CONV>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, p);
   return hipGetLastError();
 }
 
-template <Epi E>
+template <Epi E, bool CONV = false>
 hipError_t launch_epi(const Params& p, hipStream_t s) {
   // Pick the launch plan that keeps the chip busiest.  Estimated time is the
   // number of rounds of concurrent workgroups (one per CU) times the relative
@@ -443,16 +502,16 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
     if (t < best_t - 0.1) {
       Params head = p;
       head.M = (int)head_rows;
-      hipError_t e = launch_cfg<256, 256, 2, 4, E>(head, 0, s);
+      hipError_t e = launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
       if (e != hipSuccess) return e;
-      return launch_cfg<128, 256, 2, 4, E>(p, (int)head_rows, s);
+      return launch_cfg<128, 256, 2, 4, E, CONV>(p, (int)head_rows, s);
     }
   }
   switch (best) {
-    case 0: return launch_cfg<256, 256, 2, 4, E>(p, 0, s);
-    case 1: return launch_cfg<256, 128, 2, 2, E>(p, 0, s);
-    case 2: return launch_cfg<128, 128, 2, 2, E>(p, 0, s);
-    default: return launch_cfg<256, 64, 4, 1, E>(p, 0, s);
+    case 0: return launch_cfg<256, 256, 2, 4, E, CONV>(p, 0, s);
+    case 1: return launch_cfg<256, 128, 2, 2, E, CONV>(p, 0, s);
+    case 2: return launch_cfg<128, 128, 2, 2, E, CONV>(p, 0, s);
+    default: return launch_cfg<256, 64, 4, 1, E, CONV>(p, 0, s);
   }
 }
 
@@ -491,6 +550,47 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
     case Epi::Patch: return launch_epi<Epi::Patch>(p, s);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
+  const int T = a.KH * a.KW;
+  if (a.batch < 0 || a.H < 1 || a.W < 1 || a.KH < 1 || a.KW < 1 || a.stride < 1 || a.pad < 0 ||
+      a.N < 1 || a.Ca < 8 || (a.Ca & 7) != 0 || (a.Cs & 7) != 0 || a.Ca > a.Cs || a.wseg < a.Ca ||
+      (a.wseg & 7) != 0 || a.ldw < (int64_t)T * a.wseg || (a.ldw & 7) != 0 || a.ldc < a.N ||
+      (a.ldc & 7) != 0)
+    return hipErrorInvalidValue;
+  const int Ho = (a.H + 2 * a.pad - a.KH) / a.stride + 1, Wo = (a.W + 2 * a.pad - a.KW) / a.stride + 1;
+  if (Ho < 1 || Wo < 1) return hipErrorInvalidValue;
+  if (a.batch == 0) return hipSuccess;
+  const int64_t limit = ((int64_t)1 << 31) - 1;
+  const int64_t w_bytes = ((int64_t)(a.N - 1) * a.ldw + (int64_t)T * a.wseg) * 2;
+  const int64_t img_bytes = (int64_t)a.H * a.W * a.Cs * 2;
+  if (w_bytes > limit || img_bytes > limit) return hipErrorInvalidValue;
+  // The range checks take 32-bit offsets: run the batch in runs of images
+  // whose input stays below 2 GiB.
+  const int per = (int)std::min<int64_t>(a.batch, limit / img_bytes);
+  for (int b0 = 0; b0 < a.batch; b0 += per) {
+    const int nb = std::min(per, a.batch - b0);
+    Params p{};
+    p.A = static_cast<const uint16_t*>(a.x) + (int64_t)b0 * a.H * a.W * a.Cs;
+    p.W = static_cast<const uint16_t*>(a.weight);
+    p.ldw = a.ldw;
+    p.C = static_cast<uint16_t*>(a.C) + (int64_t)b0 * Ho * Wo * a.ldc;
+    p.ldc = a.ldc;
+    p.bias = a.bias;
+    p.M = nb * Ho * Wo;
+    p.N = a.N;
+    p.K = T * a.Ca;
+    p.relu = a.relu ? 1 : 0;
+    p.cv_H = a.H; p.cv_W = a.W; p.cv_Cs = a.Cs; p.cv_Ca = a.Ca; p.cv_KW = a.KW; p.cv_T = T;
+    p.cv_stride = a.stride; p.cv_pad = a.pad; p.cv_Ho = Ho; p.cv_Wo = Wo; p.cv_wseg = (int)a.wseg;
+    p.cv_nc = (a.Ca + kBK - 1) / kBK;
+    p.a_bytes = (int)(nb * img_bytes);
+    p.w_bytes = (int)w_bytes;
+    const hipError_t e = launch_epi<Epi::Bias, true>(p, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace elasto

@@ -42,6 +42,24 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
+
+// Implicit-GEMM convolution, bf16, Bias epilogue (optional ReLU):
+// C[(n, oh, ow)][j] = sum_{tap, c < Ca} x[n][ih][iw][c] * weight[j][tap*wseg + c] + bias[j]
+// with (ih, iw) = (oh*stride - pad + tap/KW, ow*stride - pad + tap%KW), zero
+// outside the image.  x NHWC with channel stride Cs; C rows of ldc elements.
+struct ConvArgs {
+  const void* x = nullptr;
+  int batch = 0, H = 0, W = 0, Cs = 0, Ca = 0;
+  int KH = 1, KW = 1, stride = 1, pad = 0;
+  const void* weight = nullptr;
+  int64_t ldw = 0, wseg = 0;
+  void* C = nullptr;
+  int64_t ldc = 0;
+  const float* bias = nullptr;
+  int N = 0;
+  bool relu = false;
+};
+hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s);
 hipError_t launch_gemm_f32(Epi epi, const GemmArgs& a, hipStream_t s);
 
 // out[r] = LN(x[r]) over d features; x row stride x_stride, out contiguous.
@@ -70,8 +88,6 @@ hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
 constexpr int kAttnMaxTokens = 240;
 
 // Elastic bottleneck-ResNet data movement (conv.hip).  NHWC bf16.
-hipError_t launch_im2col_nhwc(const void* x, int batch, int H, int W, int Cs, int Ca, int KH,
-                              int KW, int stride, int pad, void* out, hipStream_t s);
 hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, int KH, int KW,
                               int stride, int pad, int kpad, void* out, hipStream_t s);
 hipError_t launch_max_pool_3x3_s2(const void* x, int batch, int H, int W, int C, void* y,

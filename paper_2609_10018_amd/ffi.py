@@ -114,6 +114,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                              c_vp, c_i64, c_i32, c_i32, c_vp],
         "elasto_op_attention": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32,
                                 c_f32, c_vp],
+        "elasto_op_conv2d": [c_vp, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
+                             c_vp, c_i64, c_i64, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp],
         "elasto_select_mode": [P(DNLut), c_f64, c_f64, c_f64, c_f64, P(c_i32)],
         "elasto_profile_modes": [c_vp, c_vp, c_i32, c_vp, c_i32, c_i32, c_vp, P(c_f64), P(c_f64),
                                  P(c_f64)],
@@ -310,6 +312,14 @@ def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int,
     check(load_library().elasto_op_attention(dtype, qkv.data_ptr(), qkv_stride, o.data_ptr(),
                                              o_stride, batch, tokens, heads, head_dim, scale,
                                              _stream_ptr(stream)))
+
+
+def op_conv2d(x, batch: int, H: int, W: int, cs: int, ca: int, kh: int, kw: int, stride: int,
+              pad: int, w, ldw: int, wseg: int, bias, y, ldy: int, n: int, relu: bool = False,
+              stream=None) -> None:
+    check(load_library().elasto_op_conv2d(x.data_ptr(), batch, H, W, cs, ca, kh, kw, stride, pad,
+                                          w.data_ptr(), ldw, wseg, bias.data_ptr(), y.data_ptr(),
+                                          ldy, n, int(relu), _stream_ptr(stream)))
 
 
 class _HostCNN:

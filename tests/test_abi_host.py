@@ -202,3 +202,32 @@ def test_op_entry_points_validate_before_any_hip_call(lib):
     assert ln(0, p16, 768, p16, 197, p16, 4, 768, p16, p16, f, None) == 1   # x_cls needs bf16
     assert ln(1, p16, 768, p16, 0, p16, 4, 768, p16, p16, f, None) == 1     # tokens >= 1
     assert lib.elasto_last_error()
+
+
+def test_conv2d_validates_before_any_hip_call(lib):
+    """Channel counts, strides, alignment and the 2 GiB range-check limit are
+    refused with INVALID_ARG before any pointer is used."""
+    p16 = ctypes.c_void_p(1 << 20)
+    p8 = ctypes.c_void_p((1 << 20) + 8)
+    cv = lib.elasto_op_conv2d
+
+    def call(x=p16, batch=2, H=14, W=14, cs=64, ca=64, kh=3, kw=3, stride=1, pad=1, w=p16,
+             ldw=576, wseg=64, bias=p16, y=p16, ldy=64, n=64, relu=1):
+        return cv(x, batch, H, W, cs, ca, kh, kw, stride, pad, w, ldw, wseg, bias, y, ldy, n,
+                  relu, None)
+
+    assert call(ca=60) == 1                 # channel prefix not a multiple of 8
+    assert call(ca=0) == 1
+    assert call(ca=72) == 1                 # more active channels than stored
+    assert call(wseg=56) == 1               # tap segment shorter than the prefix
+    assert call(ldw=568) == 1               # rows shorter than kh*kw*wseg
+    assert call(ldy=60) == 1
+    assert call(n=0) == 1
+    assert call(stride=0) == 1
+    assert call(H=1, pad=0) == 1            # kernel larger than the padded image
+    assert call(x=p8) == 1
+    assert call(y=p8) == 1
+    assert call(x=None) == 1
+    assert call(H=4096, W=4096, cs=128, ca=128, ldw=1152, wseg=128) == 1  # one image > 2 GiB
+    assert lib.elasto_last_error()
+

@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
+from oracle import resnet as orn
 from paper_2609_10018_amd import ffi, inputs
 
 pytestmark = pytest.mark.gpu
@@ -206,3 +207,61 @@ def test_attention(dtype, B, T, h, hd, stride):
     got = host(od)[:, :h * hd]
     assert rel_err(got, ref) < (2e-2 if dtype == BF16 else 1e-5)
     assert (host(od)[:, h * hd:] == 0).all()
+
+
+# Implicit-GEMM convolution (elastic ResNet layers) against the oracle's fp64
+# conv2d.  Cases: ragged output width and rows, a channel prefix (ca < cs),
+# several 64-channel steps per tap, odd image sizes with stride 2, a
+# non-square kernel, the smallest channel count, and enough 256x256 tiles
+# for the split launch.
+CONV_CASES = [
+    # batch, H, W, cs, ca, kh, kw, stride, pad, wseg, n, ldy, relu
+    (3, 14, 14, 64, 56, 3, 3, 1, 1, 64, 40, 48, True),
+    (2, 15, 15, 128, 128, 3, 3, 2, 1, 136, 72, 72, False),
+    (2, 28, 28, 256, 256, 1, 1, 2, 0, 256, 512, 512, False),
+    (1, 5, 5, 16, 8, 3, 3, 1, 1, 8, 8, 8, True),
+    (2, 9, 13, 32, 24, 3, 1, 1, 1, 32, 16, 16, False),
+    (85, 28, 28, 64, 64, 3, 3, 1, 1, 64, 256, 256, True),
+]
+
+
+def _conv_case(batch, H, W, cs, ca, kh, kw, stride, pad, wseg, n, ldy, relu, seed=5,
+               poison=False):
+    rng = np.random.default_rng(seed)
+    x = inputs.bf16_round(rng.standard_normal((batch, H, W, cs)))
+    w = inputs.bf16_round(rng.standard_normal((n, kh * kw, wseg)) / math.sqrt(kh * kw * ca))
+    b = rng.standard_normal(n).astype(np.float32) * 0.1
+    y0 = inputs.bf16_round(rng.standard_normal((batch * ((H + 2 * pad - kh) // stride + 1) *
+                                                ((W + 2 * pad - kw) // stride + 1), ldy)))
+    if poison:  # what the kernel must never read
+        x[..., ca:] = np.nan
+        w[:, :, ca:] = np.nan
+    xd, wd, yd = dev(x, torch.bfloat16), dev(w.reshape(n, -1), torch.bfloat16), dev(y0, torch.bfloat16)
+    ffi.op_conv2d(xd, batch, H, W, cs, ca, kh, kw, stride, pad, wd, kh * kw * wseg, wseg,
+                  dev(b, torch.float32), yd, ldy, n, relu)
+    torch.cuda.synchronize()
+    got = host(yd)
+    x_nchw = np.nan_to_num(x[..., :ca]).transpose(0, 3, 1, 2)
+    w_oihw = np.nan_to_num(w[:, :, :ca]).reshape(n, kh, kw, ca).transpose(0, 3, 1, 2)
+    ref = orn.conv2d(x_nchw, w_oihw, b.astype(np.float64), stride, pad)
+    ref = ref.transpose(0, 2, 3, 1).reshape(-1, n)
+    if relu:
+        ref = np.maximum(ref, 0.0)
+    return got[:, :n], ref, got[:, n:], y0[:, n:]
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[f"b{c[0]}-{c[1]}x{c[2]}-c{c[4]}of{c[3]}-"
+                                                  f"k{c[5]}x{c[6]}s{c[7]}-n{c[10]}" for c in CONV_CASES])
+def test_conv2d(case):
+    got, ref, tail_after, tail_before = _conv_case(*case)
+    assert rel_err(got, ref) < 1e-2
+    np.testing.assert_array_equal(tail_after, tail_before)  # columns >= n untouched
+
+
+def test_conv2d_never_reads_inactive_channels():
+    case = CONV_CASES[0]
+    clean, ref, _, _ = _conv_case(*case)
+    poisoned, _, _, _ = _conv_case(*case, poison=True)
+    assert np.isfinite(poisoned).all()
+    np.testing.assert_array_equal(poisoned, clean)
+    assert rel_err(clean, ref) < 1e-2
