@@ -378,7 +378,8 @@ typedef struct elasto_cnn_s* elasto_cnn_t;
 /* Shape.  Blocks: blocks[s] bottlenecks in stage s, inner width widths[s],
  * output channels widths[s] * expansion; stage s > 0 starts with stride 2.
  * Needs img % 32 == 0, stem, widths[] and expansion * widths[] multiples of
- * 8, 1 <= num_stages <= 8, in_chans >= 1, dtype == ELASTO_BF16. */
+ * 8, 1 <= num_stages <= 8, 1 <= in_chans <= 4 (image channels), dtype ==
+ * ELASTO_BF16. */
 typedef struct {
   int32_t img, in_chans, stem, num_stages;
   int32_t widths[8], blocks[8];

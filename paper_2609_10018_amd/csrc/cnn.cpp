@@ -2,7 +2,9 @@
 // prefix layout, buffers, and the forward as a sequence of launches.
 //
 // One forward in mode k (NHWC bf16 activations; n = n_width[k][b]):
-//   stem: patch matrix of the NCHW images (7x7, stride 2) -> GEMM + ReLU
+//   stem: NCHW images -> zero-bordered NHWC with 4 channels; 7x7 stride-2
+//          implicit convolution (each kernel row one 8-pixel window, the
+//          8th pixel and 4th channel with zero weights) + ReLU
 //   3x3 stride-2 max pool                                       -> cur
 //   per bottleneck b:
 //     1x1 reduce: GEMM over cur, N = n (prefix of order1) + ReLU -> t1
@@ -58,11 +60,14 @@ std::vector<BlockSpec> block_specs(const elasto_cnn_config_t& c) {
 
 int64_t al256(int64_t v) { return (v + 255) / 256 * 256; }
 
+// Packed stem filter row: 7 kernel rows x (8 pixels x 4 channels).
+constexpr int kStemLdw = 7 * 32;
+
 bool check_cnn_config(const elasto_cnn_config_t* c) {
   if (!c) { set_error("config is NULL"); return false; }
   if (c->dtype != ELASTO_BF16) { set_error("the CNN path is bf16 only"); return false; }
   if (c->img < 32 || c->img % 32 != 0) { set_error("img must be a positive multiple of 32"); return false; }
-  if (c->in_chans < 1 || c->in_chans > 64) { set_error("in_chans outside [1, 64]"); return false; }
+  if (c->in_chans < 1 || c->in_chans > 4) { set_error("in_chans outside [1, 4]"); return false; }
   if (c->stem < 8 || c->stem % 8 != 0) { set_error("stem channels must be a multiple of 8"); return false; }
   if (c->num_stages < 1 || c->num_stages > 8) { set_error("num_stages outside [1, 8]"); return false; }
   if (c->expansion < 1 || c->num_classes < 1 || c->max_batch < 1) { set_error("bad size"); return false; }
@@ -121,7 +126,6 @@ struct elasto_cnn_s {
   uint8_t* dw = nullptr;
   uint8_t* ds = nullptr;
   int64_t wbytes = 0, sbytes = 0;
-  int stem_kpad = 0;
   int64_t stem_w = 0, stem_b = 0, fc_w = 0, fc_b = 0;
   std::vector<BlockOff> boff;
   void *col = nullptr, *stem_out = nullptr, *x = nullptr, *d = nullptr, *t1 = nullptr,
@@ -157,10 +161,10 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
 
   // Packed layout (offsets in bytes, 256-aligned): bf16 filters, fp32 biases.
   const int C = cfg->in_chans;
-  h->stem_kpad = (C * 49 + 7) / 8 * 8;
+
   int64_t off = 0;
   auto put = [&](int64_t bytes) { const int64_t o = off; off = al256(off + bytes); return o; };
-  h->stem_w = put((int64_t)cfg->stem * h->stem_kpad * 2);
+  h->stem_w = put((int64_t)cfg->stem * kStemLdw * 2);
   h->stem_b = put((int64_t)cfg->stem * 4);
   for (const BlockSpec& b : bs) {
     BlockOff o{};
@@ -199,7 +203,13 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
     const float* sw = T[ti++];
     const float* sb = T[ti++];
     for (int co = 0; co < cfg->stem; ++co) {
-      for (int k = 0; k < C * 49; ++k) mat(h->stem_w, (int64_t)co * h->stem_kpad + k, sw[(int64_t)co * C * 49 + k]);
+      // [co][i*32 + j*4 + c]: kernel row i, column j < 7, channel c < C; the
+      // rest (j == 7, c >= C) stays zero.
+      for (int c = 0; c < C; ++c)
+        for (int i = 0; i < 7; ++i)
+          for (int j = 0; j < 7; ++j)
+            mat(h->stem_w, (int64_t)co * kStemLdw + i * 32 + j * 4 + c,
+                sw[(((int64_t)co * C + c) * 7 + i) * 7 + j]);
       vec(h->stem_b, co, sb[co]);
     }
   }
@@ -244,7 +254,7 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
 
   // Scratch for max_batch images.
   const int64_t B = cfg->max_batch, hs = cfg->img / 2;
-  int64_t col = B * hs * hs * h->stem_kpad, io = B * (hs / 2) * (hs / 2) * cfg->stem, t1 = 0, t2 = 0;
+  int64_t col = B * (cfg->img + 6) * (cfg->img + 6) * 4, io = B * (hs / 2) * (hs / 2) * cfg->stem, t1 = 0, t2 = 0;
   for (const BlockSpec& b : bs) {
     const int64_t hi = b.hw_in, ho = b.hw_in / b.stride;
     io = std::max(io, B * ho * ho * b.c_out);
@@ -381,10 +391,18 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
   } while (0)
 
   const int hs = c.img / 2;
-  ELASTO_TRY(launch_im2col_nchw(images, batch, c.in_chans, c.img, c.img, 7, 7, 2, 3, h->stem_kpad,
-                                h->col, s), "stem patches");
-  ELASTO_TRY(gemm(Epi::Bias, h->col, h->stem_kpad, h->stem_w, h->stem_kpad, h->stem_out, c.stem,
-                  h->stem_b, B * hs * hs, c.stem, h->stem_kpad, true), "stem");
+  ELASTO_TRY(launch_pad_nhwc4(images, batch, c.in_chans, c.img, c.img, 3, h->col, s), "stem input");
+  {
+    ConvArgs a;
+    a.x = h->col; a.batch = batch; a.H = c.img + 6; a.W = c.img + 6; a.Cs = 4; a.Ca = 32;
+    a.KH = 7; a.KW = 1; a.stride = 2; a.pad = 0; a.row_window = 7;
+    a.weight = Wp(h->stem_w); a.ldw = kStemLdw; a.wseg = 32;
+    a.C = h->stem_out; a.ldc = c.stem;
+    a.bias = Fp(h->stem_b);
+    a.N = c.stem;
+    a.relu = true;
+    ELASTO_TRY(launch_conv_bf16(a, s), "stem");
+  }
   ELASTO_TRY(launch_max_pool_3x3_s2(h->stem_out, batch, hs, hs, c.stem, h->x, s), "max pool");
   void* cur = h->x;
   void* other = h->d;

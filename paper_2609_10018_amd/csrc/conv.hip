@@ -3,9 +3,9 @@
 // (gemm_bf16.hip, implicit for the 3x3 and strided 1x1 ones).  Activations
 // are NHWC bf16.
 //
-// * im2col_nchw: the stem's 7x7 rows from NCHW images (any channel count),
-//   row length padded with zeros to a multiple of 8; one thread per 8
-//   columns (one 16-byte store).
+// * pad_nhwc4: NCHW images (at most 4 channels) -> NHWC with 4 channels and
+//   a zero border, the stem convolution's input: with 4 channels a 7-pixel
+//   row of the stem's window is 56 contiguous bytes, read as one 64-byte run.
 // * max_pool_3x3_s2: 3x3 window, stride 2, padding 1, NHWC, 8 channels per
 //   thread.
 // * avg_pool: mean over all pixels of each image, fp32 sums, bf16 out.
@@ -17,31 +17,23 @@ namespace {
 
 inline unsigned grid_for(int64_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
-// One thread per (row, 8 consecutive columns): columns k = c*KH*KW + tap.
-template <int KH, int KW>
-__global__ __launch_bounds__(256) void im2col_nchw_kernel(const uint16_t* __restrict__ img, int C,
-                                                          int H, int W, int stride, int pad,
-                                                          int Ho, int Wo, int64_t rows, int kpad,
-                                                          uint16_t* __restrict__ out) {
-  constexpr int T = KH * KW;
-  const int chunks = kpad / 8;
+// One thread per padded output pixel: 4 channels (8 bytes), zero in the
+// border and in channels >= C.
+__global__ __launch_bounds__(256) void pad_nhwc4_kernel(const uint16_t* __restrict__ img, int C,
+                                                        int H, int W, int pad, int64_t pixels,
+                                                        uint16_t* __restrict__ out) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (id >= rows * chunks) return;
-  const int64_t m = id / chunks;
-  const int j = (int)(id - m * chunks);
-  const int64_t n = m / ((int64_t)Ho * Wo);
-  const int r = (int)(m - n * Ho * Wo), oh = r / Wo, ow = r - oh * Wo;
-  uint32_t h[8];
+  if (id >= pixels) return;
+  const int Hp = H + 2 * pad, Wp = W + 2 * pad;
+  const int64_t n = id / ((int64_t)Hp * Wp);
+  const int r = (int)(id - n * Hp * Wp), y = r / Wp - pad, x = r - (r / Wp) * Wp - pad;
+  uint32_t h[4] = {0u, 0u, 0u, 0u};
+  if (y >= 0 && y < H && x >= 0 && x < W) {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int k = 8 * j + e, c = k / T, t = k - c * T, i = t / KW, jj = t - i * KW;
-    const int ih = oh * stride - pad + i, iw = ow * stride - pad + jj;
-    h[e] = (c < C && ih >= 0 && ih < H && iw >= 0 && iw < W)
-               ? img[((n * C + c) * H + ih) * (int64_t)W + iw]
-               : 0u;
+    for (int c = 0; c < 4; ++c)
+      if (c < C) h[c] = img[((n * C + c) * H + y) * (int64_t)W + x];
   }
-  *reinterpret_cast<u32x4*>(out + m * (int64_t)kpad + 8 * j) =
-      u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  *reinterpret_cast<u32x2*>(out + id * 4) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
 }
 
 __global__ __launch_bounds__(256) void max_pool_kernel(const uint16_t* __restrict__ x, int H, int W,
@@ -102,15 +94,13 @@ __global__ __launch_bounds__(256) void avg_pool_kernel(const uint16_t* __restric
 
 }  // namespace
 
-hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, int KH, int KW,
-                              int stride, int pad, int kpad, void* out, hipStream_t s) {
-  const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
-  const int64_t rows = (int64_t)batch * Ho * Wo;
-  if (rows <= 0) return hipSuccess;
-  if (kpad < C * KH * KW || kpad % 8 != 0 || KH != 7 || KW != 7) return hipErrorInvalidValue;
-  const int64_t work = rows * (kpad / 8);
-  hipLaunchKernelGGL((im2col_nchw_kernel<7, 7>), dim3(grid_for(work, 256)), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(img), C, H, W, stride, pad, Ho, Wo, rows, kpad,
+hipError_t launch_pad_nhwc4(const void* img, int batch, int C, int H, int W, int pad, void* out,
+                            hipStream_t s) {
+  if (C < 1 || C > 4 || H < 1 || W < 1 || pad < 0) return hipErrorInvalidValue;
+  const int64_t pixels = (int64_t)batch * (H + 2 * pad) * (W + 2 * pad);
+  if (pixels <= 0) return hipSuccess;
+  hipLaunchKernelGGL(pad_nhwc4_kernel, dim3(grid_for(pixels, 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(img), C, H, W, pad, pixels,
                      static_cast<uint16_t*>(out));
   return hipGetLastError();
 }

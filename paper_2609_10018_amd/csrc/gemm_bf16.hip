@@ -24,11 +24,14 @@
 //
 // Implicit convolution (CONV kernels): A is an NHWC bf16 activation and
 // output row m is pixel (image, oh, ow).  K walks the KH*KW taps, and within a
-// tap the first Ca input channels in steps of 64; W row j keeps tap t's
-// channels at j*ldw + t*wseg.  A and W land in LDS through range-checked
-// buffer loads: a 16-byte chunk whose pixel lies in the zero padding, or
-// whose channels are at or past Ca, gets an offset past the end of the
-// buffer and reads as zeros, so no patch matrix is ever written to memory.
+// tap the first Ca input channels: in steps of 64 when Ca > 32, otherwise
+// 64 / Cp taps share one step (Cp = Ca rounded up to a power of two), so
+// narrow modes do not multiply mostly zeros.  W row j keeps tap t's channels
+// at j*ldw + t*wseg.  A and W land in LDS through range-checked buffer
+// loads: a 16-byte chunk whose pixel lies in the zero padding, whose
+// channels are at or past Ca, or whose tap is past the last, gets an offset
+// past the end of the buffer and reads as zeros, so no patch matrix is ever
+// written to memory.
 //
 // Workgroups are renumbered so that each XCD (workgroup i runs on XCD i % 8)
 // receives a contiguous run of tiles, ordered in groups of row panels so that
@@ -71,7 +74,10 @@ struct Params {
   // KH x KW taps (row-major), stride, zero padding, output Ho x Wo; weights
   // stride wseg elements per tap; nc = 64-channel steps per tap; buffer
   // sizes in bytes (each below 2^31) for the range checks.
+  // tps = taps per K step (1: nc steps per tap; > 1: each tap spans 2^cshift
+  // elements of the step); tap / KW = (tap * kwinv) >> 16.
   int cv_H, cv_W, cv_Cs, cv_Ca, cv_KW, cv_T, cv_stride, cv_pad, cv_Ho, cv_Wo, cv_wseg, cv_nc;
+  int cv_tps, cv_cshift, cv_kwinv;
   int a_bytes, w_bytes;
 };
 
@@ -205,7 +211,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     return k;
   };
 
-  const int nk_full = CONV ? p.cv_T * p.cv_nc : p.K / kBK;
+  const int nk_full = !CONV ? p.K / kBK
+                      : p.cv_tps == 1 ? p.cv_T * p.cv_nc
+                                      : (p.cv_T + p.cv_tps - 1) / p.cv_tps;
   const int nk = CONV ? nk_full : (p.K + kBK - 1) / kBK;
   // Buffer descriptors of the CONV loads (unused otherwise).
   const __amdgpu_buffer_rsrc_t rs_a =
@@ -215,6 +223,29 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   auto issue = [&](int stage, int kt) {
     char* base = smem + stage * STAGE;
     if constexpr (CONV) {
+      if (p.cv_tps > 1) {
+        // Several taps per step: this lane's chunk belongs to tap t0 + d.
+        const int t0 = kt * p.cv_tps, cmask = (1 << p.cv_cshift) - 1;
+#pragma unroll
+        for (int i = 0; i < PER_WAVE; ++i) {
+          const int q = chunk[i] * 8, t = t0 + (q >> p.cv_cshift), ch = q & cmask;
+          const bool tap_ok = t < p.cv_T && ch < p.cv_Ca;
+          const int ti = (t * p.cv_kwinv) >> 16, tj = t - ti * p.cv_KW;
+          if (wave * PER_WAVE + i < ABLK) {
+            const bool ok = tap_ok && (unsigned)(cih[i] + ti) < (unsigned)p.cv_H &&
+                            (unsigned)(ciw[i] + tj) < (unsigned)p.cv_W;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs_a, (lds_void*)(base + ldsoff[i]), 16,
+                ok ? (unsigned)(cbase[i] + (ti * p.cv_W + tj) * p.cv_Cs + ch) * 2u : kOutOfRange,
+                0, 0, 0);
+          } else {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs_w, (lds_void*)(base + ldsoff[i]), 16,
+                tap_ok ? (unsigned)(cbase[i] + t * p.cv_wseg + ch) * 2u : kOutOfRange, 0, 0, 0);
+          }
+        }
+        return;
+      }
       const int t = kt / p.cv_nc, c0 = (kt - t * p.cv_nc) * kBK;
       const int ti = t / p.cv_KW, tj = t - ti * p.cv_KW;
       const int tap = (ti * p.cv_W + tj) * p.cv_Cs, wtap = t * p.cv_wseg;
@@ -554,18 +585,37 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
 
 hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
   const int T = a.KH * a.KW;
+  // Row-window form: each tap (kernel row) reads Ca consecutive elements from
+  // its pixel on, i.e. a window of Ca / Cs pixels along the row.
+  const bool win = a.row_window > 0;
+  const int kw_out = win ? a.row_window : a.KW;
   if (a.batch < 0 || a.H < 1 || a.W < 1 || a.KH < 1 || a.KW < 1 || a.stride < 1 || a.pad < 0 ||
-      a.N < 1 || a.Ca < 8 || (a.Ca & 7) != 0 || (a.Cs & 7) != 0 || a.Ca > a.Cs || a.wseg < a.Ca ||
-      (a.wseg & 7) != 0 || a.ldw < (int64_t)T * a.wseg || (a.ldw & 7) != 0 || a.ldc < a.N ||
-      (a.ldc & 7) != 0)
+      a.N < 1 || a.Ca < 8 || (a.Ca & 7) != 0 || a.Cs < 1 || a.wseg < a.Ca || (a.wseg & 7) != 0 ||
+      a.ldw < (int64_t)T * a.wseg || (a.ldw & 7) != 0 || a.ldc < a.N || (a.ldc & 7) != 0 ||
+      T > 64)
     return hipErrorInvalidValue;
-  const int Ho = (a.H + 2 * a.pad - a.KH) / a.stride + 1, Wo = (a.W + 2 * a.pad - a.KW) / a.stride + 1;
+  if (win ? (a.KW != 1 || a.pad != 0 || (a.Cs & 3) != 0 || (a.stride * a.Cs) % 8 != 0 ||
+             (a.W * a.Cs) % 8 != 0 || a.Ca < a.row_window * a.Cs)
+          : ((a.Cs & 7) != 0 || a.Ca > a.Cs))
+    return hipErrorInvalidValue;
+  const int Ho = (a.H + 2 * a.pad - a.KH) / a.stride + 1;
+  const int Wo = (a.W + 2 * a.pad - kw_out) / a.stride + 1;
   if (Ho < 1 || Wo < 1) return hipErrorInvalidValue;
   if (a.batch == 0) return hipSuccess;
   const int64_t limit = ((int64_t)1 << 31) - 1;
   const int64_t w_bytes = ((int64_t)(a.N - 1) * a.ldw + (int64_t)T * a.wseg) * 2;
   const int64_t img_bytes = (int64_t)a.H * a.W * a.Cs * 2;
   if (w_bytes > limit || img_bytes > limit) return hipErrorInvalidValue;
+  // K steps: Ca > 32 takes ceil(Ca / 64) steps per tap; otherwise taps
+  // share a step, each spanning Cp = the next power of two >= Ca.
+  int tps = 1, cshift = 0;
+  if (a.Ca <= 32) {
+    cshift = a.Ca <= 8 ? 3 : a.Ca <= 16 ? 4 : 5;
+    tps = kBK >> cshift;
+  }
+  const int kwinv = 65536 / a.KW + 1;
+  for (int t = 0; t < T + tps; ++t)  // the division by multiplication is exact here
+    if ((t * kwinv) >> 16 != t / a.KW) return hipErrorInvalidValue;
   // The range checks take 32-bit offsets: run the batch in runs of images
   // whose input stays below 2 GiB.
   const int per = (int)std::min<int64_t>(a.batch, limit / img_bytes);
@@ -585,6 +635,7 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
     p.cv_H = a.H; p.cv_W = a.W; p.cv_Cs = a.Cs; p.cv_Ca = a.Ca; p.cv_KW = a.KW; p.cv_T = T;
     p.cv_stride = a.stride; p.cv_pad = a.pad; p.cv_Ho = Ho; p.cv_Wo = Wo; p.cv_wseg = (int)a.wseg;
     p.cv_nc = (a.Ca + kBK - 1) / kBK;
+    p.cv_tps = tps; p.cv_cshift = cshift; p.cv_kwinv = kwinv;
     p.a_bytes = (int)(nb * img_bytes);
     p.w_bytes = (int)w_bytes;
     const hipError_t e = launch_epi<Epi::Bias, true>(p, s);

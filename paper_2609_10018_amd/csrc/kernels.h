@@ -47,6 +47,10 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
 // C[(n, oh, ow)][j] = sum_{tap, c < Ca} x[n][ih][iw][c] * weight[j][tap*wseg + c] + bias[j]
 // with (ih, iw) = (oh*stride - pad + tap/KW, ow*stride - pad + tap%KW), zero
 // outside the image.  x NHWC with channel stride Cs; C rows of ldc elements.
+// row_window > 0 (KW = 1, pad = 0): tap i reads the Ca elements from pixel
+// (oh*stride + i, ow*stride) on, a window of Ca / Cs pixels along the row
+// (the caller keeps it inside the row); the output width is then
+// (W - row_window) / stride + 1.
 struct ConvArgs {
   const void* x = nullptr;
   int batch = 0, H = 0, W = 0, Cs = 0, Ca = 0;
@@ -58,6 +62,7 @@ struct ConvArgs {
   const float* bias = nullptr;
   int N = 0;
   bool relu = false;
+  int row_window = 0;
 };
 hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s);
 hipError_t launch_gemm_f32(Epi epi, const GemmArgs& a, hipStream_t s);
@@ -88,8 +93,8 @@ hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
 constexpr int kAttnMaxTokens = 240;
 
 // Elastic bottleneck-ResNet data movement (conv.hip).  NHWC bf16.
-hipError_t launch_im2col_nchw(const void* img, int batch, int C, int H, int W, int KH, int KW,
-                              int stride, int pad, int kpad, void* out, hipStream_t s);
+hipError_t launch_pad_nhwc4(const void* img, int batch, int C, int H, int W, int pad, void* out,
+                            hipStream_t s);
 hipError_t launch_max_pool_3x3_s2(const void* x, int batch, int H, int W, int C, void* y,
                                   hipStream_t s);
 hipError_t launch_avg_pool(const void* x, int batch, int HW, int C, void* y, hipStream_t s);

@@ -231,3 +231,26 @@ def test_conv2d_validates_before_any_hip_call(lib):
     assert call(H=4096, W=4096, cs=128, ca=128, ldw=1152, wseg=128) == 1  # one image > 2 GiB
     assert lib.elasto_last_error()
 
+
+
+def test_cnn_validation_rejects_bad_shapes_and_tables():
+    """elasto_cnn_validate: the shipped configs pass; bad image sizes, channel
+    counts and widths give BAD_CONFIG, bad DN tables BAD_TABLE."""
+    import dataclasses
+    from paper_2609_10018_amd.inputs_cnn import CNN_CONFIGS, make_cnn_table
+    for name in CNN_CONFIGS:
+        assert ffi.cnn_validate(CNN_CONFIGS[name], make_cnn_table(CNN_CONFIGS[name])) == 0
+    cfg = CNN_CONFIGS["resnet_small"]
+    t = make_cnn_table(cfg)
+    for change in ({"img": 48}, {"in_chans": 5}, {"in_chans": 0}, {"stem": 12},
+                   {"widths": (16, 32, 60, 128)}):
+        assert ffi.cnn_validate(dataclasses.replace(cfg, **change), t) == 2, change
+    bad = make_cnn_table(cfg)
+    bad.n_width[1, 0] = 12                      # not a multiple of 8
+    assert ffi.cnn_validate(cfg, bad) == 3
+    bad = make_cnn_table(cfg)
+    bad.n_width[0, 2] = cfg.block_specs()[2]["width"] + 8   # wider than the block
+    assert ffi.cnn_validate(cfg, bad) == 3
+    bad = make_cnn_table(cfg)
+    bad.order2[1][0] = bad.order2[1][1]         # not a permutation
+    assert ffi.cnn_validate(cfg, bad) == 3

@@ -212,8 +212,8 @@ def test_attention(dtype, B, T, h, hd, stride):
 # Implicit-GEMM convolution (elastic ResNet layers) against the oracle's fp64
 # conv2d.  Cases: ragged output width and rows, a channel prefix (ca < cs),
 # several 64-channel steps per tap, odd image sizes with stride 2, a
-# non-square kernel, the smallest channel count, and enough 256x256 tiles
-# for the split launch.
+# non-square kernel, the smallest channel count, enough 256x256 tiles for the
+# split launch, and channel counts of at most 32 (taps sharing a K step).
 CONV_CASES = [
     # batch, H, W, cs, ca, kh, kw, stride, pad, wseg, n, ldy, relu
     (3, 14, 14, 64, 56, 3, 3, 1, 1, 64, 40, 48, True),
@@ -222,6 +222,10 @@ CONV_CASES = [
     (1, 5, 5, 16, 8, 3, 3, 1, 1, 8, 8, 8, True),
     (2, 9, 13, 32, 24, 3, 1, 1, 1, 32, 16, 16, False),
     (85, 28, 28, 64, 64, 3, 3, 1, 1, 64, 256, 256, True),
+    # at most 32 active channels: several taps share one 64-wide K step
+    (4, 56, 56, 64, 16, 3, 3, 2, 1, 64, 16, 16, True),
+    (2, 14, 14, 64, 32, 3, 3, 1, 1, 64, 32, 32, True),
+    (3, 7, 7, 24, 24, 3, 3, 1, 1, 24, 24, 24, False),
 ]
 
 
