@@ -5,21 +5,27 @@ normalisation is ``F.layer_norm``, attention is
 ``F.scaled_dot_product_attention`` (default scale 1/sqrt(head_dim)) and the
 activation is ``F.gelu(approximate='none')``.  Used only to pin the oracle.
 """
+import contextlib
+
 import numpy as np
 import torch
 import torch.nn.functional as F
 
 
 def t64(a):
+    if isinstance(a, torch.Tensor):
+        return a
     return torch.as_tensor(np.asarray(a, dtype=np.float64))
 
 
-def torch_vit(w, images, cfg, layer_heads=None, head_dim=None):
+def torch_vit(w, images, cfg, layer_heads=None, head_dim=None, grad=False):
     """Full-width (or per-layer ``layer_heads``) ViT over stacked canonical
-    weights (or per-layer lists); ``head_dim`` defaults to dim / heads."""
+    weights (or per-layer lists); ``head_dim`` defaults to dim / heads.  With
+    ``grad`` the weights may be torch tensors that require gradients and the
+    logits come back as a tensor of the autograd graph."""
     d, P, eps = cfg.dim, cfg.patch, cfg.ln_eps
     hd = head_dim or cfg.dim // cfg.heads
-    with torch.no_grad():
+    with (contextlib.nullcontext() if grad else torch.no_grad()):
         x = F.conv2d(t64(images), t64(w["patch_w"]), t64(w["patch_b"]), stride=P)
         B = x.shape[0]
         x = x.flatten(2).transpose(1, 2)
@@ -39,7 +45,8 @@ def torch_vit(w, images, cfg, layer_heads=None, head_dim=None):
             g = F.gelu(F.linear(u, t64(w["fc1_w"][l]), t64(w["fc1_b"][l])), approximate="none")
             x = x + F.linear(g, t64(w["fc2_w"][l]), t64(w["fc2_b"][l]))
         c = F.layer_norm(x[:, 0], (d,), t64(w["norm_g"]), t64(w["norm_b"]), eps)
-        return F.linear(c, t64(w["head_w"]), t64(w["head_b"])).numpy()
+        logits = F.linear(c, t64(w["head_w"]), t64(w["head_b"]))
+        return logits if grad else logits.numpy()
 
 
 def loop_masked_weights(w, cfg, table, k):
