@@ -357,6 +357,51 @@ elasto_status_t elasto_op_conv2d(const void* x, int32_t batch, int32_t H, int32_
                                  const void* w, int64_t ldw, int64_t wseg, const float* bias,
                                  void* y, int64_t ldy, int32_t n, int32_t relu, void* hip_stream);
 
+/* ================================================ growth step (Section 4.2) */
+/* Growing DN mode k re-introduces the weights mode k holds and the next
+ * smaller mode k + 1 (the previous level) lacks; mode k + 1's weights are
+ * shared and frozen.  With the prefix layout the re-introduced weights of
+ * layer l are contiguous slices: q/k/v rows and biases of head slots
+ * [n_heads[k+1][l], n_heads[k][l]), the output projection's columns of
+ * those slots, fc1 rows and biases and fc2 columns of MLP units
+ * [n_mlp[k+1][l], n_mlp[k][l]).  Eq. 9's gradient mask G is 1 exactly there. */
+typedef struct elasto_growth_s* elasto_growth_t;
+
+/* Growth context of a bf16 handle for batches of up to max_batch images:
+ * fp32 master copies of the trainable matrices (initialised from the
+ * handle's bf16 weights), the activations one step keeps and the gradient
+ * buffers, all in device memory allocated here (on the handle's device).
+ * The handle must outlive the context.  BAD_CONFIG: not a bf16 handle, or
+ * head_dim != 64. */
+elasto_status_t elasto_growth_create(elasto_handle_t h, int32_t max_batch, elasto_growth_t* out);
+elasto_status_t elasto_growth_destroy(elasto_growth_t g);
+
+/* One growth step of mode k (Section 4.2: Eq. 9 and the selective gradient
+ * clipping): the mode-k forward of `batch` images (device, as for
+ * elasto_forward), the mean cross-entropy against labels (device int32
+ * [batch], each in [0, num_classes); another value makes the loss NaN), the
+ * backward, G (.) grad for the re-introduced slices only, scaled by
+ * min(1, clip_norm / |G (.) grad|_2), and W <- W - lr * that, applied to
+ * the fp32 masters and stored, rounded to bf16 (biases: fp32), into the
+ * handle's packed weights.  Every weight of mode k + 1 stays bit-identical.
+ * Needs 0 <= k < num_modes - 1, n_heads / n_mlp of mode k + 1 at most those
+ * of mode k in every layer, and the full embedding width in modes k and
+ * k + 1; lr finite, clip_norm > 0 (INFINITY: no clipping).  stats: device
+ * float[3] (or NULL) receiving mean loss, |G (.) grad|_2 and the clip
+ * factor.  Enqueued on hip_stream without synchronising; the handle's
+ * forward must not run on another stream meanwhile. */
+elasto_status_t elasto_growth_step(elasto_growth_t g, int32_t mode, const void* images,
+                                   const int32_t* labels, int32_t batch, float lr,
+                                   float clip_norm, float* stats, void* hip_stream);
+
+/* Synchronous copy to host memory: which = 0 the handle's packed weights
+ * (elasto_packed_bytes long), which = 1 the fp32 masters (one float per
+ * bf16 element of the packed image: float i mirrors the bf16 element at
+ * byte 2i; only the re-trainable matrices, WQKV, WO, W1 and W2, are kept).
+ * bytes must equal the full size. */
+elasto_status_t elasto_growth_read(elasto_growth_t g, int32_t which, void* host_dst,
+                                   int64_t bytes);
+
 /* ======================================== elastic bottleneck ResNet (CNN) */
 /* The paper applies the same elastic transformation to CNNs (Eq. 7 masks
  * whole convolution kernels; Table 2 reports ResNet-50 DNs).  This is the

@@ -61,4 +61,19 @@ __device__ __forceinline__ float gelu_poly(float z) {
   return z * fmaf(s, q, 0.5f);
 }
 
+// d/dz of gelu_poly: with s = z/Z inside (-Z, Z),
+// (z (0.5 + s q(s^2)))' = 0.5 + s q + s (q + 2 s^2 q'(s^2)); outside, s is
+// constant and only 0.5 + s q remains.
+__device__ __forceinline__ float gelu_poly_grad(float z) {
+  const float s = __builtin_amdgcn_fmed3f(z * (1.0f / kGeluZ), -1.0f, 1.0f);
+  const float s2 = s * s;
+  float q = kGeluC[9], dq = 9.0f * kGeluC[9];
+#pragma unroll
+  for (int k = 8; k >= 0; --k) q = fmaf(q, s2, kGeluC[k]);
+#pragma unroll
+  for (int k = 8; k >= 1; --k) dq = fmaf(dq, s2, (float)k * kGeluC[k]);
+  const float inner = fabsf(z) < kGeluZ ? s * fmaf(2.0f * s2, dq, q) : 0.0f;
+  return fmaf(s, q, 0.5f) + inner;
+}
+
 }  // namespace elasto

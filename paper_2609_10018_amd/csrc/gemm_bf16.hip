@@ -79,6 +79,16 @@ struct Params {
   int cv_H, cv_W, cv_Cs, cv_Ca, cv_KW, cv_T, cv_stride, cv_pad, cv_Ho, cv_Wo, cv_wseg, cv_nc;
   int cv_tps, cv_cshift, cv_kwinv;
   int a_bytes, w_bytes;
+  // BiasResid residual source (nullptr: C itself); BiasGelu pre-activation
+  // output / GeluBwd pre-activation input (nullptr: none).
+  const uint16_t* res;
+  int64_t ldres;
+  uint16_t* aux;
+  int64_t ldaux;
+  // BiasF32 split-K: blockIdx.y = chunk of kchunk K-elements, partial
+  // product to C + chunk * c_split.
+  int ksplit, kchunk;
+  int64_t c_split;
 };
 
 // Buffer descriptor word 3 for raw (unswizzled, stride 0) buffers on CDNA.
@@ -141,6 +151,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if constexpr (E == Epi::BiasF32) {
+    if (p.ksplit > 1) {
+      const int k0 = blockIdx.y * p.kchunk;
+      p.A += k0;
+      p.W += k0;
+      p.K = min(p.kchunk, p.K - k0);
+      p.C = static_cast<float*>(p.C) + blockIdx.y * p.c_split;
+    }
+  }
   const int wm = wave / WN, wn = wave % WN;
 
   // Tile order: workgroup i runs on XCD i % 8, so each XCD first receives a
@@ -343,7 +362,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   const int col = n0 + cc * 8;
   const bool col_in = col < p.N, full = col + 8 <= p.N;
   float bv[8];
-  if (full) {
+  if (p.bias == nullptr || E == Epi::GeluBwd) {  // no bias term
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bv[e] = 0.0f;
+  } else if (full) {
     const f32x4 b0 = *reinterpret_cast<const f32x4*>(p.bias + col);
     const f32x4 b1 = *reinterpret_cast<const f32x4*>(p.bias + col + 4);
     bv[0] = b0[0]; bv[1] = b0[1]; bv[2] = b0[2]; bv[3] = b0[3];
@@ -361,13 +383,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     // Residual rows of this pass: issued before the staging so that their
     // latency overlaps it.
     u32x4 res[ITER];
-    if constexpr (E == Epi::BiasResid) {
+    if constexpr (E == Epi::BiasResid || E == Epi::GeluBwd) {
+      const uint16_t* rsrc = E == Epi::GeluBwd ? p.aux
+                             : p.res != nullptr ? p.res : static_cast<const uint16_t*>(p.C);
+      const int64_t rld = E == Epi::GeluBwd ? p.ldaux : p.res != nullptr ? p.ldres : p.ldc;
 #pragma unroll
       for (int it = 0; it < ITER; ++it) {
         const int row = row_base + it * RSTEP;
         res[it] = (full && row < p.M)
-                      ? *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.C) +
-                                                        (int64_t)row * p.ldc + col)
+                      ? *reinterpret_cast<const u32x4*>(rsrc + (int64_t)row * rld + col)
                       : u32x4{0u, 0u, 0u, 0u};
       }
     }
@@ -414,8 +438,36 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] += bv[e];
       } else if constexpr (E == Epi::BiasGelu) {
+        if (p.aux != nullptr) {  // keep the pre-activation for the backward
+          uint16_t* ap = p.aux + (int64_t)row * p.ldaux + col;
+          if (full) {
+            u32x4 w;
+#pragma unroll
+            for (int h = 0; h < 4; ++h)
+              w[h] = (uint32_t)f32_to_bf16(v[2 * h] + bv[2 * h]) |
+                     ((uint32_t)f32_to_bf16(v[2 * h + 1] + bv[2 * h + 1]) << 16);
+            *reinterpret_cast<u32x4*>(ap) = w;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (col + e < p.N) ap[e] = f32_to_bf16(v[e] + bv[e]);
+          }
+        }
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = gelu_poly(v[e] + bv[e]);
+      } else if constexpr (E == Epi::GeluBwd) {
+        if (full) {
+          const u32x4 x = res[it];
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] *= gelu_poly_grad(
+                __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16)));
+        } else {
+          const uint16_t* ap = p.aux + (int64_t)row * p.ldaux + col;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = col + e < p.N ? v[e] * gelu_poly_grad(bf16_to_f32(ap[e])) : 0.0f;
+        }
       } else if constexpr (E == Epi::BiasResid) {
         if (cls_row != nullptr) {
 #pragma unroll
@@ -431,9 +483,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
             v[e] = __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16)) +
                    (v[e] + bv[e]);
         } else {
+          const uint16_t* rp = p.res != nullptr ? p.res + (int64_t)row * p.ldres + col : cp;
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            v[e] = col + e < p.N ? bf16_to_f32(cp[e]) + (v[e] + bv[e]) : 0.0f;
+            v[e] = col + e < p.N ? bf16_to_f32(rp[e]) + (v[e] + bv[e]) : 0.0f;
         }
       } else {  // Patch: class rows (t == 0) take cls + pos[0] and drop the product
         const int t = row % p.tokens;
@@ -498,7 +551,8 @@ hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   p.group_m = p.K >= 2048 ? 2 : 4;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E, CONV>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E, CONV>),
+                     dim3((unsigned)blocks, (unsigned)(p.ksplit > 1 ? p.ksplit : 1)),
                      dim3(64 * WM * WN), 0, s, p);
   return hipGetLastError();
 }
@@ -573,12 +627,28 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.ldpos = a.ldpos > 0 ? a.ldpos : a.N;
   p.ccls = a.ccls;
   p.relu = a.relu ? 1 : 0;
+  p.res = static_cast<const uint16_t*>(a.res);
+  p.ldres = a.ldres;
+  p.aux = static_cast<uint16_t*>(a.aux);
+  p.ldaux = a.ldaux;
+  p.ksplit = a.ksplit;
+  p.kchunk = a.kchunk;
+  p.c_split = a.c_split;
+  if (a.ksplit > 1 && (epi != Epi::BiasF32 || a.kchunk < kBK || a.kchunk % kBK != 0 ||
+                       (int64_t)(a.ksplit - 1) * a.kchunk >= a.K || a.c_split < (int64_t)a.M * a.ldc))
+    return hipErrorInvalidValue;
+  if (epi == Epi::GeluBwd && (a.aux == nullptr || a.ldaux < a.N || a.ldaux % 8 != 0))
+    return hipErrorInvalidValue;
+  if (a.res != nullptr && (a.ldres < a.N || a.ldres % 8 != 0)) return hipErrorInvalidValue;
+  if (a.aux != nullptr && epi == Epi::BiasGelu && (a.ldaux < a.N || a.ldaux % 8 != 0))
+    return hipErrorInvalidValue;
   switch (epi) {
     case Epi::Bias: return launch_epi<Epi::Bias>(p, s);
     case Epi::BiasGelu: return launch_epi<Epi::BiasGelu>(p, s);
     case Epi::BiasResid: return launch_epi<Epi::BiasResid>(p, s);
     case Epi::BiasF32: return launch_epi<Epi::BiasF32>(p, s);
     case Epi::Patch: return launch_epi<Epi::Patch>(p, s);
+    case Epi::GeluBwd: return launch_epi<Epi::GeluBwd>(p, s);
   }
   return hipErrorInvalidValue;
 }

@@ -17,6 +17,7 @@ enum class Epi : int {
   BiasF32 = 3,   // C (fp32) = acc + bias
   Patch = 4,     // patch embedding: A rows are image patches (row t == 0 of
                  // each sequence is the class row), C = acc + (cls|bias) + pos
+  GeluBwd = 5,   // C = acc * GELU'(aux) (aux: the pre-activation, bf16)
 };
 
 // C[m][n] = epi(sum_k A[m][k] W[n][k] + bias[n]).
@@ -39,6 +40,16 @@ struct GemmArgs {
   int64_t ldpos = 0;  // row stride of pos (elements); 0: N
   float* ccls = nullptr;
   bool relu = false;  // bf16 Bias / BiasResid epilogues: max(result, 0)
+  // BiasResid: residual read from res (row stride ldres) instead of C.
+  const void* res = nullptr;
+  int64_t ldres = 0;
+  // BiasGelu: also store the pre-activation to aux (bf16); GeluBwd: read it.
+  void* aux = nullptr;
+  int64_t ldaux = 0;
+  // BiasF32 only: split K into ksplit chunks of kchunk (a multiple of 64);
+  // chunk i writes its partial product to C + i * c_split (fp32 elements).
+  int ksplit = 1, kchunk = 0;
+  int64_t c_split = 0;
 };
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
@@ -87,6 +98,60 @@ struct AttnArgs {
 
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
+
+// Backward of launch_attention_bf16 (head_dim 64): from qkv (the forward's
+// input) and dout (gradient of o, slot s at columns s*64, row stride
+// dout_stride) write dq, dk, dv into dqkv, laid out like qkv.  stats holds
+// batch*heads*tokens*2 floats of scratch (per-query softmax statistics).
+struct AttnBwdArgs {
+  const void* qkv = nullptr;
+  int64_t qkv_stride = 0;
+  const void* dout = nullptr;
+  int64_t dout_stride = 0;
+  void* dqkv = nullptr;
+  int64_t dqkv_stride = 0;
+  float* stats = nullptr;
+  int batch = 0, tokens = 0, heads = 0, head_dim = 0;
+  float scale = 1.0f;
+};
+hipError_t launch_attention_bwd_bf16(const AttnBwdArgs& a, hipStream_t s);
+
+// Growth-step helpers (growth_kernels.hip).
+// out[c][r] = in[r][c0 + c], r < rows, c < n (bf16; ldo % 8 == 0, ldo >= rows).
+hipError_t launch_transpose_bf16(const void* in, int64_t ldi, int64_t c0, int rows, int n,
+                                 void* out, int64_t ldo, hipStream_t s);
+// LayerNorm backward (gamma only; beta and gamma are not trained): from x
+// (the LN input, bf16) and dy (bf16), dX[r] += dx (fp32) and dXb[r] = bf16(dX[r]).
+hipError_t launch_layernorm_bwd_bf16(const void* x, int64_t ldx, const void* dy, int64_t ldy,
+                                     const float* gamma, float eps, int rows, int d, float* dX,
+                                     int64_t lddx, void* dXb, int64_t lddxb, hipStream_t s);
+// Mean cross-entropy pieces: dlogits (bf16) = (softmax - onehot) / batch and
+// the per-image loss (NaN for a label outside [0, C)).
+hipError_t launch_cross_entropy(const float* logits, int64_t ldl, const int32_t* labels, int C,
+                                int batch, void* dlogits, int64_t ldd, float* rowloss,
+                                hipStream_t s);
+hipError_t launch_rowsum_bf16(const void* in, int64_t ld, int rows, int n, float* out,
+                              hipStream_t s);
+hipError_t launch_splitk_reduce(const float* part, int64_t c_split, int ksplit, int rows, int cols,
+                                int64_t ldp, float* out, int64_t ldo, hipStream_t s);
+// stats[0..2] = mean loss, L2 norm of grad[0, n), clip factor min(1, clip / norm);
+// part holds growth_sumsq_parts() floats of scratch.
+int growth_sumsq_parts();
+hipError_t launch_growth_norm(const float* grad, int64_t n, float* part, const float* rowloss,
+                              int batch, float clip, float* stats, hipStream_t s);
+// One trainable slice of the packed weights: rows x cols elements from byte
+// packed_off with row stride ld (elements); its gradient at grad + grad_off
+// with row stride grad_ld.  bf16 slices update the fp32 master element of
+// the same index (packed byte offset / 2) and store its rounding.
+struct GrowthSlice {
+  int64_t packed_off, ld, grad_off;
+  int32_t grad_ld, rows, cols, is_bf16;
+};
+hipError_t launch_growth_update(const GrowthSlice* slices, int nslices, const float* grad,
+                                float* master, void* packed, const float* stats, float lr,
+                                hipStream_t s);
+hipError_t launch_master_init(const void* packed, int64_t off, int64_t n, float* master,
+                              hipStream_t s);
 
 // Largest token count the bf16 attention kernel supports (K and V^T of one
 // head are staged whole in LDS).

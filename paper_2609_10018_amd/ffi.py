@@ -117,6 +117,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "elasto_op_conv2d": [c_vp, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
                              c_vp, c_i64, c_i64, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp],
         "elasto_select_mode": [P(DNLut), c_f64, c_f64, c_f64, c_f64, P(c_i32)],
+        "elasto_growth_create": [c_vp, c_i32, P(c_vp)],
+        "elasto_growth_destroy": [c_vp],
+        "elasto_growth_step": [c_vp, c_i32, c_vp, c_vp, c_i32, c_f32, c_f32, c_vp, c_vp],
+        "elasto_growth_read": [c_vp, c_i32, c_vp, c_i64],
         "elasto_profile_modes": [c_vp, c_vp, c_i32, c_vp, c_i32, c_i32, c_vp, P(c_f64), P(c_f64),
                                  P(c_f64)],
         "elasto_cnn_validate": [P(CNNConfig), P(CNNTableC)],
@@ -312,6 +316,47 @@ def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int,
     check(load_library().elasto_op_attention(dtype, qkv.data_ptr(), qkv_stride, o.data_ptr(),
                                              o_stride, batch, tokens, heads, head_dim, scale,
                                              _stream_ptr(stream)))
+
+
+class GrowthContext:
+    """Growth-step state of a bf16 ElasticViT handle (fp32 masters, saved
+    activations, gradients) for batches of up to max_batch images."""
+
+    def __init__(self, vit: "ElasticViT", max_batch: int):
+        self.lib = load_library()
+        self.vit = vit                      # the handle must outlive the context
+        g = c_vp()
+        check(self.lib.elasto_growth_create(vit.h, int(max_batch), ctypes.byref(g)))
+        self.g = g
+
+    def step(self, mode: int, images, labels, lr: float, clip: float, stats=None,
+             stream=None) -> None:
+        """images: bf16 device tensor NCHW; labels: int32 device tensor [batch];
+        stats: fp32 device tensor with 3 elements (loss, |G grad|, clip factor) or None."""
+        if not images.is_contiguous() or not labels.is_contiguous():
+            raise ValueError("images and labels must be contiguous")
+        check(self.lib.elasto_growth_step(self.g, int(mode), images.data_ptr(), labels.data_ptr(),
+                                          int(images.shape[0]), float(lr), float(clip),
+                                          _ptr(stats), _stream_ptr(stream)))
+
+    def read(self, which: int) -> np.ndarray:
+        """which 0: packed weights (uint8); 1: fp32 masters (float32, one per bf16 element)."""
+        total = packed_bytes(self.vit.cfg)
+        n = total if which == 0 else total // 2 * 4
+        buf = np.empty(n, dtype=np.uint8)
+        check(self.lib.elasto_growth_read(self.g, int(which), buf.ctypes.data, n))
+        return buf if which == 0 else buf.view(np.float32)
+
+    def close(self) -> None:
+        if getattr(self, "g", None) is not None and self.g.value:
+            check(self.lib.elasto_growth_destroy(self.g))
+            self.g = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def op_conv2d(x, batch: int, H: int, W: int, cs: int, ca: int, kh: int, kw: int, stride: int,
