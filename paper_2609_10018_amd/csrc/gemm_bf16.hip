@@ -239,7 +239,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.A), (short)0, p.a_bytes, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rs_w =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p.W), (short)0, p.w_bytes, kRsrcWord3);
-  auto issue = [&](int stage, int kt) {
+  // Loads blocks [lo, hi) of K step kt into stage `stage`.
+  auto issue = [&](int stage, int kt, int lo, int hi) {
     char* base = smem + stage * STAGE;
     if constexpr (CONV) {
       if (p.cv_tps > 1) {
@@ -247,6 +248,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         const int t0 = kt * p.cv_tps, cmask = (1 << p.cv_cshift) - 1;
 #pragma unroll
         for (int i = 0; i < PER_WAVE; ++i) {
+          if (i < lo || i >= hi) continue;
           const int q = chunk[i] * 8, t = t0 + (q >> p.cv_cshift), ch = q & cmask;
           const bool tap_ok = t < p.cv_T && ch < p.cv_Ca;
           const int ti = (t * p.cv_kwinv) >> 16, tj = t - ti * p.cv_KW;
@@ -270,6 +272,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       const int tap = (ti * p.cv_W + tj) * p.cv_Cs, wtap = t * p.cv_wseg;
 #pragma unroll
       for (int i = 0; i < PER_WAVE; ++i) {
+        if (i < lo || i >= hi) continue;
         const int ch = c0 + chunk[i] * 8;
         if (wave * PER_WAVE + i < ABLK) {
           const bool ok = ch < p.cv_Ca && (unsigned)(cih[i] + ti) < (unsigned)p.cv_H &&
@@ -286,6 +289,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     } else if (kt < nk_full) {
 #pragma unroll
       for (int i = 0; i < PER_WAVE; ++i)
+        if (i >= lo && i < hi)
         __builtin_amdgcn_global_load_lds(
             (global_void*)(src[i] + koff(i, kt * kBK + chunk[i] * 8)),
             (lds_void*)(base + ldsoff[i]), 16, 0, 0);
@@ -314,11 +318,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
   const int lr = lane & 31, lg = lane >> 5;
-  issue(0, 0);
+  issue(0, 0, 0, PER_WAVE);
   for (int kt = 0; kt < nk; ++kt) {
     wait_vm_lds<0>();
     __builtin_amdgcn_s_barrier();
-    if (kt + 1 < nk) issue((kt + 1) & 1, kt + 1);
+    if (kt + 1 < nk) issue((kt + 1) & 1, kt + 1, 0, PER_WAVE);
     const char* cur = smem + (kt & 1) * STAGE;
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
@@ -540,6 +544,213 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   }
 }
 
+
+// Persistent variant for the Bias and BiasGelu epilogues (the q/k/v and fc1
+// GEMMs, whose outputs are 3-4x wider than their inputs): one 512-thread
+// workgroup per CU walks 256x256 tiles v = blockIdx.x + gridDim.x * j (same
+// XCD-aware order as above).  Its epilogue is wave-local: each wave converts
+// its 128x64 block to bf16 in registers, transposes it through a private
+// 32x32 LDS slot and writes 16-byte row chunks with buffer stores.  Every wave
+// issues exactly 16 stores per tile (rows past M / chunks past N get an offset
+// past the buffer's end and are dropped), after the first K step of the next
+// tile has been put in flight; the next tile's first wait then leaves those 16
+// stores outstanding, so they drain under its main loop instead of stalling
+// the CU.  Operands are swapped in the MFMA (D = W A^T) so that a lane holds 4
+// consecutive output columns; accumulators live in AGPRs.
+// Requirements (checked by the launcher): a bias, no ReLU, K % 64 == 0,
+// N % 8 == 0, ldc % 8 == 0, no aux output, no split K.
+constexpr int kPersSlotStride = 72;  // bytes per row of a wave's 32x32 bf16 slot
+constexpr int kTilePers = 256;       // rows per persistent tile
+
+template <Epi E>
+__global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
+  static_assert(E == Epi::Bias || E == Epi::BiasGelu, "persistent epilogues");
+  asm volatile("" ::: "a0");  // let the accumulators take AGPRs
+  constexpr int BM = 256, BN = 256, WN = 4, NW = 8, WTM = 128, WTN = 64, TM = 4, TN = 2;
+  constexpr int STAGE = (BM + BN) * kRowBytes;
+  constexpr int ES = kPersSlotStride, SLOT = 32 * ES;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT];
+  auto bar = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int tiles_m = (p.M + BM - 1) / BM, total = tiles_m * p.tiles_n;
+  const int q = total >> 3, r8 = total & 7;
+  auto tile_of = [&](int v, int& m0, int& n0) {
+    const int xcd = v & 7, idx = v >> 3;
+    const int logical = (xcd < r8) ? xcd * (q + 1) + idx : r8 * (q + 1) + (xcd - r8) * q + idx;
+    const int gsz = p.group_m * p.tiles_n, group = logical / gsz, in_group = logical - group * gsz;
+    const int gm = min(p.group_m, tiles_m - group * p.group_m);
+    const int tile_n = in_group / gm, tile_m = group * p.group_m + (in_group - tile_n * gm);
+    m0 = tile_m * BM;
+    n0 = tile_n * BN;
+  };
+  // Loads: waves 0-3 bring A rows, waves 4-7 W rows; wave w covers rows
+  // (w & 3) * 64 .. +63 of its operand's tile as 8 blocks of 8 rows.  Block i
+  // lands at LDS block w * 8 + i (the A tile, then the W tile).  Rows past
+  // the end re-read the last row (their results are never stored).
+  const int prow = lane >> 3, pcx = (lane & 7) ^ prow;
+  const bool loads_a = wave < 4;
+  const uint16_t* lsrc = loads_a ? p.A : p.W;
+  const int lld = (int)(loads_a ? p.lda : p.ldw);
+  const int llim = (loads_a ? p.M : p.N) - 1;
+  const int loff = (wave & 3) * 64;
+  const int nk = p.K / kBK;
+  auto load1 = [&](int stage, int r0, int kt, int i, int xl, int pr) {
+    const int rb = min(r0 + loff + 8 * i, llim);
+    const int rl = min(r0 + loff + 8 * i + pr, llim) - rb;
+    const uint32_t off = (uint32_t)(rl * lld + ((xl ^ i) << 3)) * 2u;
+    const char* g = reinterpret_cast<const char*>(lsrc + (int64_t)rb * lld + kt * kBK);
+    __builtin_amdgcn_global_load_lds((global_void*)(g + off),
+                                     (lds_void*)(smem + stage * STAGE + (wave * 8 + i) * 1024), 16,
+                                     0, 0);
+  };
+  const int lr = lane & 31, lg = lane >> 5;
+  // LDS byte offset of fragment (quarter kk, block i) in a stage: base ^ (kk << 5).
+  int abase[TM], bbase[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + lr;
+    abase[i] = r * kRowBytes + ((lg ^ swz(r)) << 4);
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int r = wn * WTN + j * 32 + lr;
+    bbase[j] = BM * kRowBytes + r * kRowBytes + ((lg ^ swz(r)) << 4);
+  }
+  char* const slot = smem + 2 * STAGE + wave * SLOT;
+  int v = blockIdx.x;
+  if (v >= total) return;
+  int m0, n0;
+  tile_of(v, m0, n0);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) load1(0, loads_a ? m0 : n0, 0, i, pcx, prow);
+  int buf = 0;
+  bool stores_out = false;
+  while (true) {
+    const int vn = v + gridDim.x;
+    const bool has_next = vn < total;
+    int m1 = m0, n1 = n0;
+    if (has_next) tile_of(vn, m1, n1);
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+#pragma clang loop unroll(disable)
+    for (int kt = 0; kt < nk; ++kt) {
+      // After an epilogue the wave's last 16 memory operations are its
+      // stores; everything issued before them (this step's loads) is done.
+      if (kt == 0 && stores_out) wait_vm_lds<16>();
+      else wait_vm_lds<0>();
+      __builtin_amdgcn_s_barrier();
+      // Next step of this tile, or the first step of the next tile, into the
+      // other stage (every wave finished reading it before the barrier).
+      const bool more = kt + 1 < nk, go = more || has_next;
+      const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0;
+      const int so = buf * STAGE;
+      // Opaque copies: keeps the per-quarter addresses from being hoisted out
+      // of the loop into registers.
+      int xl = pcx, pr = prow, ab[TM], bb[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) ab[i] = abase[i];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bb[j] = bbase[j];
+      asm volatile("" : "+v"(xl), "+v"(pr));
+#pragma unroll
+      for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(ab[i]));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(bb[j]));
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        if (go && kk < 3) {
+#pragma unroll
+          for (int t = (8 * kk + 2) / 3; t < (8 * (kk + 1) + 2) / 3; ++t)
+            load1(buf ^ 1, nr0, nkt, t, xl, pr);
+        }
+        const int kx = kk << 5;
+        bf16x8 af[TM], bf[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[i] = *reinterpret_cast<const bf16x8*>(smem + ((ab[i] + so) ^ kx));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bf[j] = *reinterpret_cast<const bf16x8*>(smem + ((bb[j] + so) ^ kx));
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
+      }
+      buf ^= 1;
+    }
+
+    // Epilogue.  acc[i][j][e] is output row m0 + wm*128 + i*32 + lr, column
+    // n0 + wn*64 + j*32 + 8*(e/4) + 4*lg + e%4.
+    const int rows_valid = min(BM, p.M - m0);
+    const int nrec = rows_valid * (int)p.ldc * 2;
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        static_cast<uint16_t*>(p.C) + (int64_t)m0 * p.ldc, (short)0, nrec, kRsrcWord3);
+    // Bias of this lane's 32 columns (clamped into [0, N): the columns past N
+    // are computed from re-read rows and never stored).
+    f32x4 bv[TN][4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = min(n0 + wn * WTN + j * 32 + 8 * g + 4 * lg, p.N - 4);
+        bv[j][g] = *reinterpret_cast<const f32x4*>(p.bias + c);
+      }
+    const int lane_st = ((wm * WTM + (lane >> 2)) * (int)p.ldc + n0 + wn * WTN + (lane & 3) * 8) * 2;
+    const int wofs = lr * ES + lg * 8, rofs = (lane >> 2) * ES + (lane & 3) * 16;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      int lst = lane_st, wo = wofs, ro = rofs;
+      asm volatile("" : "+v"(lst), "+v"(wo), "+v"(ro));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float t[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            t[e] = acc[i][j][4 * g + e] + bv[j][g][e];
+            if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
+          }
+          u32x2 w;
+          w[0] = (uint32_t)f32_to_bf16(t[0]) | ((uint32_t)f32_to_bf16(t[1]) << 16);
+          w[1] = (uint32_t)f32_to_bf16(t[2]) | ((uint32_t)f32_to_bf16(t[3]) << 16);
+          *reinterpret_cast<u32x2*>(slot + wo + g * 16) = w;
+        }
+        wait_lds();
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const u32x2 lo = *reinterpret_cast<const u32x2*>(slot + ro + h * 16 * ES);
+          const u32x2 hi = *reinterpret_cast<const u32x2*>(slot + ro + h * 16 * ES + 8);
+          const int rl = wm * WTM + i * 32 + h * 16 + (lane >> 2);
+          const int col = n0 + wn * WTN + j * 32 + (lane & 3) * 8;
+          const bool ok = rl < rows_valid && col + 8 <= p.N;
+          const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+          __builtin_amdgcn_raw_buffer_store_b128(
+              w, rc, ok ? lst + (i * 32 + h * 16) * (int)p.ldc * 2 + j * 64 : nrec, 0, 0);
+        }
+        wait_lds();  // the slot is rewritten by the next block
+      }
+    }
+    if (!has_next) break;
+    v = vn;
+    m0 = m1;
+    n0 = n1;
+    stores_out = true;
+  }
+}
+
 template <int BM, int BN, int WM, int WN, Epi E, bool CONV>
 hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   Params p = p0;
@@ -555,6 +766,52 @@ hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
                      dim3((unsigned)blocks, (unsigned)(p.ksplit > 1 ? p.ksplit : 1)),
                      dim3(64 * WM * WN), 0, s, p);
   return hipGetLastError();
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+template <Epi E>
+bool persistent_ok(const Params& p) {
+  if constexpr (E != Epi::Bias && E != Epi::BiasGelu) {
+    return false;
+  } else {
+    return p.bias != nullptr && !p.relu && p.aux == nullptr && p.ksplit <= 1 && p.K >= kBK &&
+           p.K % kBK == 0 && p.N % 8 == 0 &&
+           p.ldc % 8 == 0 && (int64_t)kTilePers * p.ldc * 2 < ((int64_t)1 << 31);
+  }
+}
+
+// Rows [0, rows) of the 256x256 tiling with the persistent kernel.
+template <Epi E>
+hipError_t launch_persistent(const Params& p0, int rows, hipStream_t s) {
+  if constexpr (E != Epi::Bias && E != Epi::BiasGelu) {
+    return hipErrorInvalidValue;
+  } else {
+    Params p = p0;
+    p.M = rows;
+    p.row0 = 0;
+    p.tiles_n = (p.N + 255) / 256;
+    // Row panels per group of the tile order: measured best at 8 for outputs of
+    // at most 9 tiles across (q/k/v), 4 for wider ones (fc1).
+    p.group_m = p.tiles_n <= 9 ? 8 : 4;
+    const int64_t tiles = (int64_t)((rows + 255) / 256) * p.tiles_n;
+    if (tiles <= 0) return hipSuccess;
+    const int grid = (int)std::min<int64_t>(tiles, device_cus());
+    hipLaunchKernelGGL((gemm_bf16_persistent<E>), dim3(grid), dim3(512), 0, s, p);
+    return hipGetLastError();
+  }
 }
 
 template <Epi E, bool CONV = false>
@@ -587,13 +844,17 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
     if (t < best_t - 0.1) {
       Params head = p;
       head.M = (int)head_rows;
-      hipError_t e = launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
+      hipError_t e = (!CONV && persistent_ok<E>(p))
+                         ? launch_persistent<E>(p, (int)head_rows, s)
+                         : launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
       if (e != hipSuccess) return e;
       return launch_cfg<128, 256, 2, 4, E, CONV>(p, (int)head_rows, s);
     }
   }
   switch (best) {
-    case 0: return launch_cfg<256, 256, 2, 4, E, CONV>(p, 0, s);
+    case 0:
+      if (!CONV && persistent_ok<E>(p)) return launch_persistent<E>(p, p.M, s);
+      return launch_cfg<256, 256, 2, 4, E, CONV>(p, 0, s);
     case 1: return launch_cfg<256, 128, 2, 2, E, CONV>(p, 0, s);
     case 2: return launch_cfg<128, 128, 2, 2, E, CONV>(p, 0, s);
     default: return launch_cfg<256, 64, 4, 1, E, CONV>(p, 0, s);

@@ -130,6 +130,11 @@ LINEAR_CASES = [
     # enough 256x256 tiles for a second, 128x256-tile launch over the last rows
     (BF16, ffi.EPI_BIAS_GELU, 21999, 3072, 768, 768, 768, 3072),
     (BF16, ffi.EPI_BIAS_RESID, 22000, 768, 3072, 3072, 3072, 768),
+    # persistent 256x256 kernel (Bias / BiasGelu): one partial round with
+    # ragged rows; several tiles per CU with ragged rows; ragged N with ldc > N
+    (BF16, ffi.EPI_BIAS, 7000, 2304, 768, 768, 768, 2304),
+    (BF16, ffi.EPI_BIAS, 20000, 2304, 768, 768, 768, 2304),
+    (BF16, ffi.EPI_BIAS_GELU, 12800, 1272, 384, 384, 384, 1280),
     # outputs at most 64 wide: 256x64 tiles
     (BF16, ffi.EPI_BIAS, 3001, 64, 256, 256, 256, 64),
     (BF16, ffi.EPI_BIAS_RESID, 777, 40, 576, 576, 576, 48),
