@@ -166,7 +166,9 @@ const char* elasto_last_error(void);
 elasto_status_t elasto_mode_info(elasto_handle_t h, int32_t k, double* flops_per_image,
                                  int64_t* active_weight_bytes);
 
-/* Device bytes the handle holds: packed weights and activation scratch. */
+/* Device bytes the handle holds: weights (the packed image, plus on the bf16
+ * path the LayerNorm-folded copies of the q/k/v and fc1 matrices with their
+ * column sums and folded biases per embedding width) and activation scratch. */
 elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes,
                                    int64_t* scratch_bytes);
 

@@ -65,6 +65,45 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 }  // namespace
 
+// LayerNorm folding (bf16 path).  The q/k/v and fc1 GEMMs read the residual
+// stream x itself: with u = (x - mean) * rstd * gamma + beta,
+//   u . w = rstd * (x . (gamma (x) w)) - rstd * mean * sum_k gamma_k w_k + beta . w,
+// so each LayerNorm's gamma is folded into a copy of the next weights, and
+// per embedding width e the column sums of that copy and beta . w (plus the
+// bias) are precomputed over the first e channels; the GEMM that writes x
+// supplies mean and spread per 64-column segment of every row.
+hipError_t refold(elasto_handle_s* h, hipStream_t s) {
+  if (!h->dfold) return hipSuccess;
+  const elasto_config_t& c = h->cfg;
+  const int D = c.dim, M = c.mlp_hidden, nw = (int)h->widths.size();
+  constexpr int kChunk = 16;  // widths per fold launch
+  for (int l = 0; l < c.depth; ++l) {
+    uint8_t* f = h->dfold + (int64_t)l * h->fold_stride;
+    for (int w0 = 0; w0 < nw; w0 += kChunk) {
+      const int n = std::min(kChunk, nw - w0);
+      hipError_t e = launch_ln_fold(
+          h->dw + h->lay.get(ELASTO_T_WQKV, l).offset, 3 * D, D,
+          reinterpret_cast<const float*>(h->dw + h->lay.get(ELASTO_T_LN1_G, l).offset),
+          reinterpret_cast<const float*>(h->dw + h->lay.get(ELASTO_T_LN1_B, l).offset),
+          reinterpret_cast<const float*>(h->dw + h->lay.get(ELASTO_T_BQKV, l).offset),
+          h->widths.data() + w0, n, f + h->fold_wq,
+          reinterpret_cast<float*>(f + h->fold_sq) + (int64_t)w0 * 3 * D,
+          reinterpret_cast<float*>(f + h->fold_cq) + (int64_t)w0 * 3 * D, 3 * D, s);
+      if (e == hipSuccess)
+        e = launch_ln_fold(
+            h->dw + h->lay.get(ELASTO_T_W1, l).offset, M, D,
+            reinterpret_cast<const float*>(h->dw + h->lay.get(ELASTO_T_LN2_G, l).offset),
+            reinterpret_cast<const float*>(h->dw + h->lay.get(ELASTO_T_LN2_B, l).offset),
+            reinterpret_cast<const float*>(h->dw + h->lay.get(ELASTO_T_B1, l).offset),
+            h->widths.data() + w0, n, f + h->fold_w1,
+            reinterpret_cast<float*>(f + h->fold_s1) + (int64_t)w0 * M,
+            reinterpret_cast<float*>(f + h->fold_c1) + (int64_t)w0 * M, M, s);
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
 extern "C" {
 
 elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t* w,
@@ -107,17 +146,45 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
                 sz_g = al(rows * (int64_t)cfg->mlp_hidden * eb),
                 sz_cls = al((int64_t)cfg->max_batch * D * eb),
                 sz_xcls = al((int64_t)cfg->max_batch * D * 4);
-  h->sbytes = 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls;
+  const bool bf = cfg->dtype == ELASTO_BF16;
+  h->lnseg = bf ? (int)((D + 127) / 128 * 2) : 0;  // 64-column segments, rounded up to even
+  const int64_t sz_ln = bf ? al(rows * h->lnseg * 8) : 0;
+  h->sbytes = 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls + sz_ln;
   h->wbytes = h->lay.total;
+  if (bf) {
+    h->width_idx.resize((size_t)table->num_modes);
+    for (int k = 0; k < table->num_modes; ++k) {
+      const int32_t wv = h->n_embed[(size_t)k];
+      size_t i = 0;
+      while (i < h->widths.size() && h->widths[i] != wv) ++i;
+      if (i == h->widths.size()) h->widths.push_back(wv);
+      h->width_idx[(size_t)k] = (int32_t)i;
+    }
+    const int64_t nw = (int64_t)h->widths.size(), M = cfg->mlp_hidden;
+    int64_t off = 0;
+    h->fold_wq = off; off = al(off + 3 * D * D * 2);
+    h->fold_w1 = off; off = al(off + M * D * 2);
+    h->fold_sq = off; off = al(off + nw * 3 * D * 4);
+    h->fold_cq = off; off = al(off + nw * 3 * D * 4);
+    h->fold_s1 = off; off = al(off + nw * M * 4);
+    h->fold_c1 = off; off = al(off + nw * M * 4);
+    h->fold_stride = off;
+    h->fold_bytes = off * cfg->depth;
+  }
 
   hipError_t e = hipGetDevice(&h->device);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->dw), (size_t)h->wbytes);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->ds), (size_t)h->sbytes);
+  if (e == hipSuccess && h->fold_bytes > 0)
+    e = hipMalloc(reinterpret_cast<void**>(&h->dfold), (size_t)h->fold_bytes);
   if (e == hipSuccess) e = hipMemcpy(h->dw, host.data(), (size_t)h->wbytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess && h->dfold) e = refold(h, nullptr);
+  if (e == hipSuccess && h->dfold) e = hipStreamSynchronize(nullptr);
   if (e != hipSuccess) {
     const elasto_status_t st = (e == hipErrorOutOfMemory) ? ELASTO_ERR_OUT_OF_MEMORY : ELASTO_ERR_HIP;
     if (h->dw) (void)hipFree(h->dw);
     if (h->ds) (void)hipFree(h->ds);
+    if (h->dfold) (void)hipFree(h->dfold);
     delete h;
     (void)hipGetLastError();
     return fail(st, "create: %s", hipGetErrorString(e));
@@ -129,7 +196,8 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   h->qkv = p; p += sz_qkv;
   h->g = p; p += sz_g;
   h->ucls = p; p += sz_cls;
-  h->xcls = reinterpret_cast<float*>(p);
+  h->xcls = reinterpret_cast<float*>(p); p += sz_xcls;
+  h->lnpart = bf ? reinterpret_cast<float2*>(p) : nullptr;
   *out = h;
   clear_error();
   return ELASTO_OK;
@@ -141,6 +209,10 @@ elasto_status_t elasto_destroy(elasto_handle_t h) {
   hipError_t e1 = hipSuccess, e2 = hipSuccess;
   if (h->dw) e1 = hipFree(h->dw);
   if (h->ds) e2 = hipFree(h->ds);
+  if (h->dfold) {
+    const hipError_t e3 = hipFree(h->dfold);
+    if (e1 == hipSuccess) e1 = e3;
+  }
   delete h;
   if (e1 != hipSuccess || e2 != hipSuccess)
     return fail(ELASTO_ERR_HIP, "destroy: %s", hipGetErrorString(e1 != hipSuccess ? e1 : e2));
@@ -174,7 +246,7 @@ elasto_status_t elasto_mode_info(elasto_handle_t h, int32_t k, double* flops_per
 
 elasto_status_t elasto_memory_info(elasto_handle_t h, int64_t* weight_bytes, int64_t* scratch_bytes) {
   if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
-  if (weight_bytes) *weight_bytes = h->wbytes;
+  if (weight_bytes) *weight_bytes = h->wbytes + h->fold_bytes;
   if (scratch_bytes) *scratch_bytes = h->sbytes;
   return ELASTO_OK;
 }
@@ -291,6 +363,11 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
               : launch_layernorm_f32(h->x, D, h->u, rows, E, g, b, c.ln_eps, s);
   };
   const float scale = 1.0f / sqrtf((float)d.hd);
+  // bf16: LayerNorms folded into the q/k/v and fc1 GEMMs (see refold); the
+  // GEMMs that write the residual stream produce its segment statistics.
+  const bool fold = h->dfold != nullptr;
+  const int wi = fold ? h->width_idx[(size_t)k] : 0;
+  auto fold_ptr = [&](int l, int64_t off) { return h->dfold + (int64_t)l * h->fold_stride + off; };
 
   hipError_t e;
   {
@@ -313,19 +390,32 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     a.pos = F(h, ELASTO_T_POS);
     a.ldpos = D;
     a.ccls = xcls;
+    if (fold) {
+      a.ln_out = h->lnpart;
+      a.ln_ld = h->lnseg;
+    }
     e = timed(h, ELASTO_K_PATCH, s, [&] { return gemm(Epi::Patch, a, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "patch embedding: %s", hipGetErrorString(e));
   }
   for (int l = 0; l < L; ++l) {
     const int hh = h->n_heads[(size_t)k * L + l], mm = h->n_mlp[(size_t)k * L + l];
-    e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN1_G, l), F(h, ELASTO_T_LN1_B, l)); });
-    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln1 layer %d: %s", l, hipGetErrorString(e));
+    if (!fold) {
+      e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN1_G, l), F(h, ELASTO_T_LN1_B, l)); });
+      if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln1 layer %d: %s", l, hipGetErrorString(e));
+    }
     GemmArgs q;
     q.A = h->u; q.lda = E;
     q.W = W(h, ELASTO_T_WQKV, l); q.ldw = D;
     q.C = h->qkv; q.ldc = 3 * D;
     q.bias = F(h, ELASTO_T_BQKV, l);
     q.M = rows; q.N = 3 * d.hd * hh; q.K = E;
+    if (fold) {
+      q.A = h->x; q.lda = D;
+      q.W = fold_ptr(l, h->fold_wq);
+      q.bias = reinterpret_cast<const float*>(fold_ptr(l, h->fold_cq)) + (int64_t)wi * 3 * D;
+      q.ln_colsum = reinterpret_cast<const float*>(fold_ptr(l, h->fold_sq)) + (int64_t)wi * 3 * D;
+      q.ln_in = h->lnpart; q.ln_ld = h->lnseg; q.ln_eps = c.ln_eps;
+    }
     e = timed(h, ELASTO_K_QKV, s, [&] { return gemm(Epi::Bias, q, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "qkv layer %d: %s", l, hipGetErrorString(e));
     AttnArgs at;
@@ -342,16 +432,28 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     pr.ccls = xcls;
     pr.tokens = d.T;
     pr.M = rows; pr.N = E; pr.K = d.hd * hh;
+    if (fold) {
+      pr.ln_out = h->lnpart; pr.ln_ld = h->lnseg;
+    }
     e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
-    e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l)); });
-    if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln2 layer %d: %s", l, hipGetErrorString(e));
+    if (!fold) {
+      e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l)); });
+      if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln2 layer %d: %s", l, hipGetErrorString(e));
+    }
     GemmArgs f1;
     f1.A = h->u; f1.lda = E;
     f1.W = W(h, ELASTO_T_W1, l); f1.ldw = D;
     f1.C = h->g; f1.ldc = Mh;
     f1.bias = F(h, ELASTO_T_B1, l);
     f1.M = rows; f1.N = mm; f1.K = E;
+    if (fold) {
+      f1.A = h->x; f1.lda = D;
+      f1.W = fold_ptr(l, h->fold_w1);
+      f1.bias = reinterpret_cast<const float*>(fold_ptr(l, h->fold_c1)) + (int64_t)wi * Mh;
+      f1.ln_colsum = reinterpret_cast<const float*>(fold_ptr(l, h->fold_s1)) + (int64_t)wi * Mh;
+      f1.ln_in = h->lnpart; f1.ln_ld = h->lnseg; f1.ln_eps = c.ln_eps;
+    }
     e = timed(h, ELASTO_K_FC1, s, [&] { return gemm(Epi::BiasGelu, f1, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f2;
@@ -362,6 +464,9 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     f2.ccls = xcls;
     f2.tokens = d.T;
     f2.M = rows; f2.N = E; f2.K = mm;
+    if (fold) {
+      f2.ln_out = h->lnpart; f2.ln_ld = h->lnseg;
+    }
     e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
   }

@@ -89,7 +89,63 @@ struct Params {
   // product to C + chunk * c_split.
   int ksplit, kchunk;
   int64_t c_split;
+  // LayerNorm folding (see GemmArgs): producer statistics out, consumer
+  // statistics in, the consumer's column sums, epsilon.
+  float2* ln_out;
+  const float2* ln_in;
+  int64_t ln_ld;
+  const float* ln_colsum;
+  float ln_eps;
 };
+
+// Lane exchanges within a DPP row: quad_perm (1,0,3,2) and (2,3,0,1) swap
+// neighbours 1 and 2 apart; row_half_mirror maps lane i of each 8-lane half
+// to 7 - i.  The three together sum over aligned groups of 8 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
+__device__ __forceinline__ float sum8_lanes(float v) {
+  v += dpp_f<kDppXor1>(v);
+  v += dpp_f<kDppXor2>(v);
+  return v + dpp_f<kDppHalfMirror>(v);
+}
+
+// LayerNorm factors of a row from the (sum, sum of squares) of its 64-column
+// segments, stored row-major: segment j of row r at part[r * ld + j], ld even
+// so that segments 2i and 2i+1 form one 16-byte load.
+// ln_sums adds, over the 16-byte pairs i = first, first + step, ... < ceil(nseg / 2),
+// the row's sums into S and Q, four loads in flight at a time; ln_factors
+// turns the totals into (rstd, -rstd * mean): mean = S / K, biased variance
+// Q / K - mean^2 (fp32: relative error about 2^-24 (1 + mean^2 / variance)).
+__device__ __forceinline__ void ln_sums(const float2* row, int K, int first, int step, float& S,
+                                        float& Q) {
+  const int nseg = (K + 63) >> 6, npair = (nseg + 1) >> 1;
+  for (int i0 = first; i0 < npair; i0 += 4 * step) {
+    f32x4 q[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int i = i0 + t * step;
+      q[t] = i < npair ? *reinterpret_cast<const f32x4*>(row + 2 * i) : f32x4{0.f, 0.f, 0.f, 0.f};
+      if (2 * i + 1 >= nseg) {  // odd segment count: the pair's second half is not a segment
+        q[t][2] = 0.0f;
+        q[t][3] = 0.0f;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      S += q[t][0] + q[t][2];
+      Q += q[t][1] + q[t][3];
+    }
+  }
+}
+
+__device__ __forceinline__ float2 ln_factors(float S, float Q, int K, float eps) {
+  const float inv = 1.0f / (float)K, mean = S * inv;
+  const float rstd = 1.0f / sqrtf(fmaxf(fmaf(Q, inv, -mean * mean), 0.0f) + eps);
+  return make_float2(rstd, -rstd * mean);
+}
 
 // Buffer descriptor word 3 for raw (unswizzled, stride 0) buffers on CDNA.
 constexpr int kRsrcWord3 = 0x00020000;
@@ -123,6 +179,21 @@ __device__ __forceinline__ void store_f32x8(float* cp, const float* v, bool full
   }
 }
 
+// Store 8 values rounded to bf16 (the first `valid` of them when ragged).
+__device__ __forceinline__ void store_bf16x8(uint16_t* cp, const float* v, bool full, int valid) {
+  if (full) {
+    u32x4 w;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      w[h] = (uint32_t)f32_to_bf16(v[2 * h]) | ((uint32_t)f32_to_bf16(v[2 * h + 1]) << 16);
+    *reinterpret_cast<u32x4*>(cp) = w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (e < valid) cp[e] = f32_to_bf16(v[e]);
+  }
+}
+
 // Keep elements [kbeg, kend) of the 8-element chunk starting at kbeg.
 __device__ __forceinline__ u32x4 mask_tail(u32x4 v, int kbeg, int kend) {
   u32x4 o;
@@ -146,7 +217,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   static_assert((ABLK + BBLK) % NW == 0, "blocks must split evenly over waves");
   constexpr int STAGE = (BM + BN) * kRowBytes;
   constexpr int EPI_BYTES = (BM > 128 ? 128 : BM) * (BN + 8) * 4;
-  constexpr int SMEM = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
+  constexpr int SMEM_MAIN = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
+  constexpr bool LN_CONSUMER = E == Epi::Bias || E == Epi::BiasGelu;
+  constexpr bool LN_PRODUCER = E == Epi::BiasResid || E == Epi::Patch;
+  constexpr int SMEM = SMEM_MAIN + (LN_CONSUMER ? BM * 8 : 0);  // + per-row LN factors
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -379,6 +453,22 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     for (int e = 0; e < 8; ++e) bv[e] = col + e < p.N ? p.bias[col + e] : 0.0f;
   }
 
+  // Folded LayerNorm (consumer): column sums of this thread's 8 columns, and
+  // (rstd, -rstd * mean) of the tile's rows into LDS.
+  float cs[8];
+  float2* rowst = reinterpret_cast<float2*>(smem + SMEM_MAIN);
+  if constexpr (LN_CONSUMER) {
+    if (p.ln_in != nullptr) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) cs[e] = col + e < p.N ? p.ln_colsum[col + e] : 0.0f;
+      if (tid < BM) {
+        float S = 0.0f, Q = 0.0f;
+        ln_sums(p.ln_in + (int64_t)min(m0 + tid, p.M - 1) * p.ln_ld, p.K, 0, 1, S, Q);
+        rowst[tid] = ln_factors(S, Q, p.K, p.ln_eps);
+      }
+    }
+  }
+
   wait_lds();  // every wave has finished reading the last stage
   __builtin_amdgcn_s_barrier();
 #pragma unroll
@@ -416,7 +506,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     for (int it = 0; it < ITER; ++it) {
       const int rl = r_first + it * RSTEP;
       const int row = row_base + it * RSTEP;
-      if (row >= p.M || !col_in) continue;
+      if (row >= p.M) continue;  // the same row for every lane of an 8-lane group
+      // Values whose LayerNorm statistics this lane contributes (producers).
+      float st[8];
+      bool st_ok = false;
+      if (col_in) do {
       const f32x4 s0 = *reinterpret_cast<const f32x4*>(stg + rl * SS + cc * 8);
       const f32x4 s1 = *reinterpret_cast<const f32x4*>(stg + rl * SS + cc * 8 + 4);
       float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
@@ -426,7 +520,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] += bv[e];
         store_f32x8(cp, v, full, p.N - col);
-        continue;
+        break;
       }
       // Residual stream: bf16 rows, except the class-token rows (row % tokens
       // == 0), which live in fp32 in ccls when it is given.
@@ -438,27 +532,23 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         }
       }
       uint16_t* cp = static_cast<uint16_t*>(p.C) + o;
-      if constexpr (E == Epi::Bias) {
+      if constexpr (LN_CONSUMER) {
+        // Pre-activation: acc + bias, or with a folded LayerNorm
+        // rstd * acc - rstd * mean * colsum + bias.
+        if (p.ln_in != nullptr) {
+          const float2 rs = rowst[pass * SR + rl];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] += bv[e];
-      } else if constexpr (E == Epi::BiasGelu) {
-        if (p.aux != nullptr) {  // keep the pre-activation for the backward
-          uint16_t* ap = p.aux + (int64_t)row * p.ldaux + col;
-          if (full) {
-            u32x4 w;
+          for (int e = 0; e < 8; ++e) v[e] = fmaf(v[e], rs.x, fmaf(rs.y, cs[e], bv[e]));
+        } else {
 #pragma unroll
-            for (int h = 0; h < 4; ++h)
-              w[h] = (uint32_t)f32_to_bf16(v[2 * h] + bv[2 * h]) |
-                     ((uint32_t)f32_to_bf16(v[2 * h + 1] + bv[2 * h + 1]) << 16);
-            *reinterpret_cast<u32x4*>(ap) = w;
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (col + e < p.N) ap[e] = f32_to_bf16(v[e] + bv[e]);
-          }
+          for (int e = 0; e < 8; ++e) v[e] += bv[e];
         }
+      }
+      if constexpr (E == Epi::BiasGelu) {
+        if (p.aux != nullptr)  // keep the pre-activation for the backward
+          store_bf16x8(p.aux + (int64_t)row * p.ldaux + col, v, full, p.N - col);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = gelu_poly(v[e] + bv[e]);
+        for (int e = 0; e < 8; ++e) v[e] = gelu_poly(v[e]);
       } else if constexpr (E == Epi::GeluBwd) {
         if (full) {
           const u32x4 x = res[it];
@@ -478,7 +568,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           for (int e = 0; e < 8; ++e)
             v[e] = col + e < p.N ? cls_row[e] + (v[e] + bv[e]) : 0.0f;
           store_f32x8(cls_row, v, full, p.N - col);
-          continue;
+          if (p.ln_out != nullptr) {
+            store_bf16x8(cp, v, full, p.N - col);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) st[e] = v[e];
+            st_ok = true;
+          }
+          break;
         }
         if (full) {
           const u32x4 x = res[it];
@@ -492,7 +588,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           for (int e = 0; e < 8; ++e)
             v[e] = col + e < p.N ? bf16_to_f32(rp[e]) + (v[e] + bv[e]) : 0.0f;
         }
-      } else {  // Patch: class rows (t == 0) take cls + pos[0] and drop the product
+      } else if constexpr (E == Epi::Patch) {  // class rows (t == 0) take cls + pos[0], no product
         const int t = row % p.tokens;
         const float* pp = p.pos + (int64_t)t * p.ldpos + col;
         if (full) {
@@ -516,7 +612,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         }
         if (cls_row != nullptr) {
           store_f32x8(cls_row, v, full, p.N - col);
-          continue;
+          if (p.ln_out != nullptr) {
+            store_bf16x8(cp, v, full, p.N - col);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) st[e] = v[e];
+            st_ok = true;
+          }
+          break;
         }
       }
       if constexpr (E == Epi::Bias || E == Epi::BiasResid) {
@@ -525,16 +627,35 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.0f);
         }
       }
-      if (full) {
-        u32x4 w;
+      store_bf16x8(cp, v, full, p.N - col);
+      if constexpr (LN_PRODUCER) {  // statistics of the values (before rounding)
 #pragma unroll
-        for (int h = 0; h < 4; ++h)
-          w[h] = (uint32_t)f32_to_bf16(v[2 * h]) | ((uint32_t)f32_to_bf16(v[2 * h + 1]) << 16);
-        *reinterpret_cast<u32x4*>(cp) = w;
-      } else {
+        for (int e = 0; e < 8; ++e) st[e] = v[e];
+        st_ok = true;
+      }
+      } while (0);
+      if constexpr (LN_PRODUCER) {
+        if (p.ln_out != nullptr) {
+          // Sum and sum of squares over each 64-column segment: the 8 lanes of
+          // an aligned group hold its 8 chunks (N % 8 == 0).
+          float sum = 0.0f, sq = 0.0f;
+          if (st_ok) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (col + e < p.N) cp[e] = f32_to_bf16(v[e]);
+            for (int e = 0; e < 8; ++e) {
+              sum += st[e];
+              sq = fmaf(st[e], st[e], sq);
+            }
+          }
+          sum += dpp_f<kDppXor1>(sum);
+          sq += dpp_f<kDppXor1>(sq);
+          sum += dpp_f<kDppXor2>(sum);
+          sq += dpp_f<kDppXor2>(sq);
+          sum += dpp_f<kDppHalfMirror>(sum);
+          sq += dpp_f<kDppHalfMirror>(sq);
+          const int seg = (n0 >> 6) + (cc >> 3);
+          if ((cc & 7) == 0 && 64 * seg < p.N)
+            p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(sum, sq);
+        }
       }
     }
     if (pass + 1 < BM / SR) {
@@ -562,14 +683,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 constexpr int kPersSlotStride = 72;  // bytes per row of a wave's 32x32 bf16 slot
 constexpr int kTilePers = 256;       // rows per persistent tile
 
-template <Epi E>
+template <Epi E, bool LNF>
 __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   static_assert(E == Epi::Bias || E == Epi::BiasGelu, "persistent epilogues");
   asm volatile("" ::: "a0");  // let the accumulators take AGPRs
   constexpr int BM = 256, BN = 256, WN = 4, NW = 8, WTM = 128, WTN = 64, TM = 4, TN = 2;
   constexpr int STAGE = (BM + BN) * kRowBytes;
   constexpr int ES = kPersSlotStride, SLOT = 32 * ES;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT];
+  constexpr int ROWST = LNF ? 2 * BM * 8 : 0;  // LayerNorm factors of two tiles' rows
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT + ROWST];
   auto bar = [] {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -623,6 +745,8 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     bbase[j] = BM * kRowBytes + r * kRowBytes + ((lg ^ swz(r)) << 4);
   }
   char* const slot = smem + 2 * STAGE + wave * SLOT;
+  float2* const rowst = reinterpret_cast<float2*>(smem + 2 * STAGE + NW * SLOT);
+  int par = 0;  // half of rowst this tile uses
   int v = blockIdx.x;
   if (v >= total) return;
   int m0, n0;
@@ -652,6 +776,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       __builtin_amdgcn_s_barrier();
       // Next step of this tile, or the first step of the next tile, into the
       // other stage (every wave finished reading it before the barrier).
+      // Folded LayerNorm: at the first step, two threads a row sum the row's
+      // segment statistics; the loads go out before this step's tile loads so
+      // that waiting for them does not wait for those.
+      float lS = 0.0f, lQ = 0.0f;
+      if constexpr (LNF) {
+        if (kt == 0)
+          ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, lS, lQ);
+      }
       const bool more = kt + 1 < nk, go = more || has_next;
       const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0;
       const int so = buf * STAGE;
@@ -688,7 +820,23 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
       }
+      if constexpr (LNF) {
+        // Published by a later barrier: the next step's, or the one below.
+        // rowst is double-buffered: a wave in the next tile has passed this
+        // tile's barriers, which every wave reaches after its epilogue.
+        if (kt == 0) {
+          lS += dpp_f<kDppXor1>(lS);
+          lQ += dpp_f<kDppXor1>(lQ);
+          if ((tid & 1) == 0) rowst[par * BM + (tid >> 1)] = ln_factors(lS, lQ, p.K, p.ln_eps);
+        }
+      }
       buf ^= 1;
+    }
+    if constexpr (LNF) {
+      if (nk == 1) {  // no later step barrier in this tile
+        wait_lds();
+        bar();
+      }
     }
 
     // Epilogue.  acc[i][j][e] is output row m0 + wm*128 + i*32 + lr, column
@@ -699,14 +847,21 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         static_cast<uint16_t*>(p.C) + (int64_t)m0 * p.ldc, (short)0, nrec, kRsrcWord3);
     // Bias of this lane's 32 columns (clamped into [0, N): the columns past N
     // are computed from re-read rows and never stored).
-    f32x4 bv[TN][4];
+    f32x4 bv[TN][4], cs[TN][4];
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int c = min(n0 + wn * WTN + j * 32 + 8 * g + 4 * lg, p.N - 4);
         bv[j][g] = *reinterpret_cast<const f32x4*>(p.bias + c);
+        if constexpr (LNF) cs[j][g] = *reinterpret_cast<const f32x4*>(p.ln_colsum + c);
       }
+    // Folded LayerNorm: (rstd, -rstd * mean) of this lane's 4 rows.
+    float2 rs[TM];
+    if constexpr (LNF) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) rs[i] = rowst[par * BM + wm * WTM + i * 32 + lr];
+    }
     const int lane_st = ((wm * WTM + (lane >> 2)) * (int)p.ldc + n0 + wn * WTN + (lane & 3) * 8) * 2;
     const int wofs = lr * ES + lg * 8, rofs = (lane >> 2) * ES + (lane & 3) * 16;
 #pragma unroll
@@ -720,7 +875,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
           float t[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            t[e] = acc[i][j][4 * g + e] + bv[j][g][e];
+            if constexpr (LNF)
+              t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[j][g][e], bv[j][g][e]));
+            else
+              t[e] = acc[i][j][4 * g + e] + bv[j][g][e];
             if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
           }
           u32x2 w;
@@ -748,6 +906,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     m0 = m1;
     n0 = n1;
     stores_out = true;
+    par ^= 1;
   }
 }
 
@@ -809,7 +968,10 @@ hipError_t launch_persistent(const Params& p0, int rows, hipStream_t s) {
     const int64_t tiles = (int64_t)((rows + 255) / 256) * p.tiles_n;
     if (tiles <= 0) return hipSuccess;
     const int grid = (int)std::min<int64_t>(tiles, device_cus());
-    hipLaunchKernelGGL((gemm_bf16_persistent<E>), dim3(grid), dim3(512), 0, s, p);
+    if (p.ln_in != nullptr)
+      hipLaunchKernelGGL((gemm_bf16_persistent<E, true>), dim3(grid), dim3(512), 0, s, p);
+    else
+      hipLaunchKernelGGL((gemm_bf16_persistent<E, false>), dim3(grid), dim3(512), 0, s, p);
     return hipGetLastError();
   }
 }
@@ -895,6 +1057,18 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.ksplit = a.ksplit;
   p.kchunk = a.kchunk;
   p.c_split = a.c_split;
+  p.ln_out = a.ln_out;
+  p.ln_in = a.ln_in;
+  p.ln_ld = a.ln_ld;
+  p.ln_colsum = a.ln_colsum;
+  p.ln_eps = a.ln_eps;
+  const int64_t nseg_n = (a.N + 63) / 64, nseg_k = (a.K + 63) / 64;
+  if (a.ln_out != nullptr && (epi != Epi::BiasResid && epi != Epi::Patch || a.N % 8 != 0 ||
+                              a.ln_ld < nseg_n || a.ln_ld % 2 != 0))
+    return hipErrorInvalidValue;
+  if (a.ln_in != nullptr && (epi != Epi::Bias && epi != Epi::BiasGelu || a.ln_colsum == nullptr ||
+                             a.ln_ld < nseg_k || a.ln_ld % 2 != 0 || !(a.ln_eps > 0.0f)))
+    return hipErrorInvalidValue;
   if (a.ksplit > 1 && (epi != Epi::BiasF32 || a.kchunk < kBK || a.kchunk % kBK != 0 ||
                        (int64_t)(a.ksplit - 1) * a.kchunk >= a.K || a.c_split < (int64_t)a.M * a.ldc))
     return hipErrorInvalidValue;

@@ -466,6 +466,9 @@ elasto_status_t elasto_growth_step(elasto_growth_t g, int32_t mode, const void* 
         "gradient norm");
   G_TRY(launch_growth_update(plan.slices, plan.nslices, g->grad, g->master, h->dw, g->stats, lr, s),
         "update");
+  // The inference forward reads LayerNorm-folded copies of the q/k/v and fc1
+  // weights: bring them up to date with the updated packed weights.
+  G_TRY(refold(h, s), "refold");
   if (stats) G_TRY(hipMemcpyAsync(stats, g->stats, 3 * sizeof(float), hipMemcpyDeviceToDevice, s), "stats");
 #undef G_TRY
   return ELASTO_OK;

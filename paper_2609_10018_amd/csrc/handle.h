@@ -24,6 +24,17 @@ struct elasto_handle_s {
   int64_t wbytes = 0, sbytes = 0;
   void *x = nullptr, *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr, *ucls = nullptr;
   float* xcls = nullptr;  // fp32 class-token rows of the residual stream (bf16 path)
+  // LayerNorms folded into the q/k/v and fc1 GEMMs (bf16 path).  Per layer:
+  // gamma1 (x) WQKV [3d][d] and gamma2 (x) W1 [M][d] (bf16), then for each
+  // distinct embedding width w: column sums and folded biases of both
+  // ([nw][3d] + [nw][3d] + [nw][M] + [nw][M] fp32).
+  uint8_t* dfold = nullptr;
+  int64_t fold_bytes = 0, fold_stride = 0;
+  int64_t fold_wq = 0, fold_w1 = 0, fold_sq = 0, fold_cq = 0, fold_s1 = 0, fold_c1 = 0;
+  std::vector<int32_t> widths;     // distinct active embedding widths
+  std::vector<int32_t> width_idx;  // [num_modes] index into widths
+  float2* lnpart = nullptr;        // [max_batch * T][lnseg] per-segment LayerNorm statistics
+  int lnseg = 0;                   // 64-column segments of d, rounded up to even
   // kernel timing
   int timed_class = -1;
   std::vector<hipEvent_t> events;
@@ -31,3 +42,6 @@ struct elasto_handle_s {
   int64_t skipped = 0;
 };
 
+// Recompute the folded LayerNorm weights from the packed weights (after
+// create, and after anything that changes the packed weights).
+hipError_t refold(elasto_handle_s* h, hipStream_t s);

@@ -50,6 +50,25 @@ struct GemmArgs {
   // chunk i writes its partial product to C + i * c_split (fp32 elements).
   int ksplit = 1, kchunk = 0;
   int64_t c_split = 0;
+  // LayerNorm folded into the GEMMs (bf16 path).
+  // Producer (BiasResid, Patch): ln_out != nullptr also writes, for every
+  // output row r and every 64-column segment j of [0, N), the sum and the sum
+  // of squares of the row's values there (before their rounding to bf16) to
+  // ln_out[r * ln_ld + j] (ln_ld even, >= ceil(N / 64); class-token rows:
+  // of their fp32 values, which are then also stored rounded to bf16 in C).
+  // Needs N % 8 == 0.
+  // Consumer (Bias, BiasGelu): ln_in != nullptr treats A as the LayerNorm
+  // input: with mean mu_r and rstd r_r of A's row r over its K columns
+  // (from the ceil(K / 64) segments of ln_in, same layout) the result is
+  // epi(r_r * (A W^T)[r][n] - r_r * mu_r * ln_colsum[n] + bias[n]), i.e.
+  // LN(A) W^T + bias when W holds gamma (x) the weights, ln_colsum[n] the sum
+  // of W's row n over its K columns and bias the original bias plus
+  // beta . W.
+  float2* ln_out = nullptr;
+  const float2* ln_in = nullptr;
+  int64_t ln_ld = 0;
+  const float* ln_colsum = nullptr;
+  float ln_eps = 0.0f;
 };
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
@@ -152,6 +171,15 @@ hipError_t launch_growth_update(const GrowthSlice* slices, int nslices, const fl
                                 hipStream_t s);
 hipError_t launch_master_init(const void* packed, int64_t off, int64_t n, float* master,
                               hipStream_t s);
+
+// Weights of a LayerNorm folded into the following linear layer (bf16):
+// for n < N, Wf[n][k] = bf16(gamma[k] * W[n][k]) for k < D, and for every
+// width e = widths[w] (w < nw), colsum[w * ldv + n] = sum_{k<e} Wf[n][k] and
+// cbias[w * ldv + n] = bias[n] + sum_{k<e} beta[k] * W[n][k].  W and Wf have
+// row stride D (bf16).
+hipError_t launch_ln_fold(const void* W, int N, int D, const float* gamma, const float* beta,
+                          const float* bias, const int32_t* widths, int nw, void* Wf,
+                          float* colsum, float* cbias, int64_t ldv, hipStream_t s);
 
 // Largest token count the bf16 attention kernel supports (K and V^T of one
 // head are staged whole in LDS).

@@ -155,6 +155,58 @@ hipError_t launch_ln(const uint16_t* x, int64_t x_stride, const float* xcls, int
   return hipGetLastError();
 }
 
+// Weights of a LayerNorm folded into the following linear layer: one wave
+// per output row n.  Sums over the row accumulate in fp64 (the folded column
+// sum is of the bf16-rounded products the GEMM multiplies).
+constexpr int kFoldMaxWidths = 16;
+struct FoldWidths {
+  int n;
+  int e[kFoldMaxWidths];
+};
+
+__global__ __launch_bounds__(256) void ln_fold_kernel(const uint16_t* __restrict__ W, int N, int D,
+                                                      const float* __restrict__ gamma,
+                                                      const float* __restrict__ beta,
+                                                      const float* __restrict__ bias,
+                                                      FoldWidths wd, uint16_t* __restrict__ Wf,
+                                                      float* __restrict__ colsum,
+                                                      float* __restrict__ cbias, int64_t ldv) {
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const uint16_t* w = W + (int64_t)n * D;
+  uint16_t* wf = Wf + (int64_t)n * D;
+  double sw[kFoldMaxWidths], sb[kFoldMaxWidths];
+#pragma unroll
+  for (int i = 0; i < kFoldMaxWidths; ++i) sw[i] = sb[i] = 0.0;
+  for (int k = lane; k < D; k += 64) {
+    const float wv = bf16_to_f32(w[k]);
+    const uint16_t f = f32_to_bf16(gamma[k] * wv);
+    wf[k] = f;
+    const double fv = (double)bf16_to_f32(f), bv = (double)beta[k] * (double)wv;
+#pragma unroll
+    for (int i = 0; i < kFoldMaxWidths; ++i)
+      if (i < wd.n && k < wd.e[i]) {
+        sw[i] += fv;
+        sb[i] += bv;
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < kFoldMaxWidths; ++i) {
+    if (i >= wd.n) break;
+    double a = sw[i], c = sb[i];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      a += __shfl_xor(a, off, 64);
+      c += __shfl_xor(c, off, 64);
+    }
+    if (lane == 0) {
+      colsum[i * ldv + n] = (float)a;
+      cbias[i * ldv + n] = (float)((double)bias[n] + c);
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_layernorm_bf16(const void* x, int64_t x_stride, const float* xcls, int tokens,
@@ -181,6 +233,23 @@ hipError_t launch_layernorm_f32(const void* x, int64_t x_stride, void* out, int6
   hipLaunchKernelGGL(layernorm_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
                      static_cast<const float*>(x), x_stride, static_cast<float*>(out), rows, d,
                      g, b, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_fold(const void* W, int N, int D, const float* gamma, const float* beta,
+                          const float* bias, const int32_t* widths, int nw, void* Wf,
+                          float* colsum, float* cbias, int64_t ldv, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if (nw < 1 || nw > kFoldMaxWidths || D < 1 || ldv < N) return hipErrorInvalidValue;
+  FoldWidths wd{};
+  wd.n = nw;
+  for (int i = 0; i < nw; ++i) {
+    if (widths[i] < 1 || widths[i] > D) return hipErrorInvalidValue;
+    wd.e[i] = widths[i];
+  }
+  hipLaunchKernelGGL(ln_fold_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(W), N, D, gamma, beta, bias, wd,
+                     static_cast<uint16_t*>(Wf), colsum, cbias, ldv);
   return hipGetLastError();
 }
 
