@@ -291,7 +291,9 @@ elasto_status_t elasto_kernel_timing_read(elasto_handle_t h, double* total_ms, i
 /* Algorithmic work of one launch of class kc in mode k at the given batch
  * summed over the forward: FLOPs (contractions) and bytes (LayerNorm rows
  * read + written; for contractions the operand and result bytes) and the
- * number of launches of that class in one forward. */
+ * number of launches of that class in one forward.  On the bf16 path the
+ * per-layer LayerNorms are folded into the GEMMs and the LayerNorm class is
+ * the final norm of the class-token rows alone. */
 elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, int32_t kc,
                                    double* flops, double* bytes, int32_t* launches);
 

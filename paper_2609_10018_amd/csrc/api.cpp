@@ -546,8 +546,13 @@ elasto_status_t elasto_kernel_work(elasto_handle_t h, int32_t k, int32_t batch, 
       n = 1;
       break;
     case ELASTO_K_LN:
-      by = 2.0 * c.depth * Mr * D * 2.0 * eb + B * D * (4.0 + eb);
-      n = 2 * c.depth + 1;
+      if (h->dfold) {  // pre-norms folded into the GEMMs: the final norm of the class rows
+        by = B * D * (4.0 + eb);
+        n = 1;
+      } else {
+        by = 2.0 * c.depth * Mr * D * 2.0 * eb + B * D * (4.0 + eb);
+        n = 2 * c.depth + 1;
+      }
       break;
     case ELASTO_K_HEAD:
       f = 2.0 * B * c.num_classes * D;

@@ -58,7 +58,7 @@ def classify(names):
     """Kernel class of each dispatch, given the kernel names in dispatch order."""
     out, last = [], None
     for n in names:
-        if "gemm_bf16_kernel" in n or "gemm_f32_kernel" in n:
+        if "gemm_bf16_kernel" in n or "gemm_f32_kernel" in n or "gemm_bf16_persistent" in n:
             m = re.search(r"\(elasto::Epi\)(\d)", n)
             e = m.group(1) if m else "?"
             if e == "2":

@@ -11,6 +11,7 @@ from paper_2609_10018_amd import pmc
 
 G = "void elasto::(anonymous namespace)::gemm_bf16_kernel<{}, {}, 2, 4, (elasto::Epi){}>(elasto::(anonymous namespace)::Params)"
 LN = "elasto::(anonymous namespace)::layernorm_bf16_kernel(...)"
+GP = "void elasto::(anonymous namespace)::gemm_bf16_persistent<(elasto::Epi){}, true>(elasto::(anonymous namespace)::Params)"
 ATT = "void elasto::(anonymous namespace)::attention_bf16_kernel<13>(elasto::(anonymous namespace)::AttnP)"
 COPY = "void at::native::vectorized_elementwise_kernel<4, at::native::BinaryFunctor<float, float, float, at::native::binary_internal::MulFunctor<float> > >(...)"
 
@@ -39,6 +40,24 @@ def test_classify_and_launches():
                      "head": 1}
     per = pmc.per_launch(cls, [1.0] * len(cls))
     assert per["fc1"] == (2, 2.0) and per["ln"] == (5, 1.0) and per["head"] == (1, 1.0)
+
+
+def test_classify_persistent_and_folded_layernorm():
+    # bf16 forward with LayerNorm folded into the GEMMs: the q/k/v and fc1
+    # GEMMs run the persistent kernel (fc1 plus a 128x256 tail launch); only
+    # the final LayerNorm remains.
+    n = [G.format(256, 256, 4), G.format(128, 256, 4)]
+    for _ in range(2):
+        n += [GP.format(0), ATT, G.format(256, 256, 2), G.format(128, 256, 2), GP.format(1),
+              G.format(128, 256, 1), G.format(256, 256, 2), G.format(128, 256, 2)]
+    n += [LN, G.format(128, 128, 3)]
+    cls = pmc.classify(n)
+    assert cls[2:10] == ["qkv", "attn", "proj", "proj", "fc1", "fc1", "fc2", "fc2"]
+    count = {}
+    for c, idx in pmc.launches(cls):
+        count[c] = count.get(c, 0) + 1
+    assert count == {"patch": 1, "qkv": 2, "attn": 2, "proj": 2, "fc1": 2, "fc2": 2, "ln": 1,
+                     "head": 1}
 
 
 def _write_counters(path, names, counters):
