@@ -666,8 +666,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 }
 
 
-// Persistent variant for the Bias and BiasGelu epilogues (the q/k/v and fc1
-// GEMMs, whose outputs are 3-4x wider than their inputs): one 512-thread
+// Persistent variant for the Bias, BiasGelu and BiasResid epilogues (the
+// q/k/v, fc1, projection and fc2 GEMMs of the forward): one 512-thread
 // workgroup per CU walks 256x256 tiles v = blockIdx.x + gridDim.x * j (same
 // XCD-aware order as above).  Its epilogue is wave-local: each wave converts
 // its 128x64 block to bf16 in registers, transposes it through a private
@@ -679,17 +679,21 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 // the CU.  Operands are swapped in the MFMA (D = W A^T) so that a lane holds 4
 // consecutive output columns; accumulators live in AGPRs.
 // Requirements (checked by the launcher): a bias, no ReLU, K % 64 == 0,
-// N % 8 == 0, ldc % 8 == 0, no aux output, no split K.
-constexpr int kPersSlotStride = 72;  // bytes per row of a wave's 32x32 bf16 slot
+// N % 8 == 0, ldc % 8 == 0 (and ldres % 8 == 0), no aux output, no split K.
+constexpr int kPersSlotStride = 72;     // bytes per row of a wave's 32x32 bf16 slot
+constexpr int kPersSlotStrideF32 = 80;  // bytes per row of a wave's 32x16 fp32 slot
 constexpr int kTilePers = 256;       // rows per persistent tile
 
 template <Epi E, bool LNF>
 __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
-  static_assert(E == Epi::Bias || E == Epi::BiasGelu, "persistent epilogues");
+  static_assert(E == Epi::Bias || E == Epi::BiasGelu || E == Epi::BiasResid, "persistent epilogues");
+  static_assert(!(LNF && E == Epi::BiasResid), "LayerNorm consumers are Bias / BiasGelu");
   asm volatile("" ::: "a0");  // let the accumulators take AGPRs
   constexpr int BM = 256, BN = 256, WN = 4, NW = 8, WTM = 128, WTN = 64, TM = 4, TN = 2;
   constexpr int STAGE = (BM + BN) * kRowBytes;
-  constexpr int ES = kPersSlotStride, SLOT = 32 * ES;
+  // Epilogue slot per wave: 32 rows x 32 bf16 columns, or (residual epilogue,
+  // fp32 staging) 32 rows x 16 fp32 columns.
+  constexpr int ES = E == Epi::BiasResid ? kPersSlotStrideF32 : kPersSlotStride, SLOT = 32 * ES;
   constexpr int ROWST = LNF ? 2 * BM * 8 : 0;  // LayerNorm factors of two tiles' rows
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT + ROWST];
   auto bar = [] {
@@ -856,49 +860,166 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         bv[j][g] = *reinterpret_cast<const f32x4*>(p.bias + c);
         if constexpr (LNF) cs[j][g] = *reinterpret_cast<const f32x4*>(p.ln_colsum + c);
       }
-    // Folded LayerNorm: (rstd, -rstd * mean) of this lane's 4 rows.
-    float2 rs[TM];
-    if constexpr (LNF) {
+    if constexpr (E == Epi::BiasResid) {
+      // C = residual + acc + bias: fp32 staging of acc + bias, 16 columns per
+      // pass (i, j, h); lane l then holds row r = l/2 of the 32-row block,
+      // columns 8 (l%2) .. +7 of the pass.  The residual comes from res (or C
+      // in place), except on the class-token rows (row % tokens == 0) when
+      // ccls is given: there it is the fp32 ccls row, which takes the fp32
+      // result (and C its bf16 rounding when the LayerNorm statistics are
+      // produced).  A lane's 4 rows are 32 apart, so at most one of them is a
+      // class row: its fp32 residual chunks are loaded with the bias.
+      const uint16_t* rsrc = p.res != nullptr ? p.res : static_cast<const uint16_t*>(p.C);
+      const int64_t rld = p.res != nullptr ? p.ldres : p.ldc;
+      const int rloc = lane >> 1, cloc = (lane & 1) * 8;
+      const int row_l0 = m0 + wm * WTM + rloc;  // this lane's row in block i: row_l0 + 32 i
+      int cls_i = -1, cls_b = 0;
+      if (p.ccls != nullptr) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) rs[i] = rowst[par * BM + wm * WTM + i * 32 + lr];
-    }
-    const int lane_st = ((wm * WTM + (lane >> 2)) * (int)p.ldc + n0 + wn * WTN + (lane & 3) * 8) * 2;
-    const int wofs = lr * ES + lg * 8, rofs = (lane >> 2) * ES + (lane & 3) * 16;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      int lst = lane_st, wo = wofs, ro = rofs;
-      asm volatile("" : "+v"(lst), "+v"(wo), "+v"(ro));
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          float t[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if constexpr (LNF)
-              t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[j][g][e], bv[j][g][e]));
-            else
-              t[e] = acc[i][j][4 * g + e] + bv[j][g][e];
-            if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
+        for (int i = 0; i < TM; ++i) {
+          const int r = row_l0 + i * 32, bi = r / p.tokens;
+          if (r < p.M && r == bi * p.tokens) {
+            cls_i = i;
+            cls_b = bi;
           }
-          u32x2 w;
-          w[0] = (uint32_t)f32_to_bf16(t[0]) | ((uint32_t)f32_to_bf16(t[1]) << 16);
-          w[1] = (uint32_t)f32_to_bf16(t[2]) | ((uint32_t)f32_to_bf16(t[3]) << 16);
-          *reinterpret_cast<u32x2*>(slot + wo + g * 16) = w;
         }
-        wait_lds();
+      }
+      f32x4 cres[TN][2][2];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(slot + ro + h * 16 * ES);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(slot + ro + h * 16 * ES + 8);
-          const int rl = wm * WTM + i * 32 + h * 16 + (lane >> 2);
-          const int col = n0 + wn * WTN + j * 32 + (lane & 3) * 8;
-          const bool ok = rl < rows_valid && col + 8 <= p.N;
-          const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-          __builtin_amdgcn_raw_buffer_store_b128(
-              w, rc, ok ? lst + (i * 32 + h * 16) * (int)p.ldc * 2 + j * 64 : nrec, 0, 0);
+          const int c = min(n0 + wn * WTN + j * 32 + h * 16 + cloc, p.N - 8);
+          if (cls_i >= 0) {
+            const float* cp = p.ccls + (int64_t)cls_b * p.N + c;
+            cres[j][h][0] = *reinterpret_cast<const f32x4*>(cp);
+            cres[j][h][1] = *reinterpret_cast<const f32x4*>(cp + 4);
+          } else {
+            cres[j][h][0] = cres[j][h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
         }
-        wait_lds();  // the slot is rewritten by the next block
+      auto load_res = [&](int i, u32x4 (&rz)[TN][2]) {
+        const int r = min(row_l0 + i * 32, p.M - 1);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int c = min(n0 + wn * WTN + j * 32 + h * 16 + cloc, p.N - 8);
+            rz[j][h] = *reinterpret_cast<const u32x4*>(rsrc + (int64_t)r * rld + c);
+          }
+      };
+      u32x4 rz[2][TN][2];
+      load_res(0, rz[0]);
+      const int seg = (n0 + wn * WTN) >> 6;  // this wave's 64 columns: one statistics segment
+      const int wo = lr * ES + lg * 16, ro = rloc * ES + (lane & 1) * 32;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        if (i + 1 < TM) load_res(i + 1, rz[(i + 1) & 1]);
+        const int row = row_l0 + i * 32;
+        const bool row_ok = row < p.M, cls = i == cls_i;
+        float ssum = 0.0f, ssq = 0.0f;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int gg = 0; gg < 2; ++gg) {
+              const int g = 2 * h + gg;
+              const f32x4 w = {acc[i][j][4 * g] + bv[j][g][0], acc[i][j][4 * g + 1] + bv[j][g][1],
+                               acc[i][j][4 * g + 2] + bv[j][g][2], acc[i][j][4 * g + 3] + bv[j][g][3]};
+              *reinterpret_cast<f32x4*>(slot + wo + gg * 32) = w;
+            }
+            wait_lds();
+            const f32x4 s0 = *reinterpret_cast<const f32x4*>(slot + ro);
+            const f32x4 s1 = *reinterpret_cast<const f32x4*>(slot + ro + 16);
+            const int col = n0 + wn * WTN + j * 32 + h * 16 + cloc;
+            const bool ok = row_ok && col + 8 <= p.N;
+            float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+            if (cls) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                v[e] += cres[j][h][0][e];
+                v[4 + e] += cres[j][h][1][e];
+              }
+              if (ok) {
+                float* cp = p.ccls + (int64_t)cls_b * p.N + col;
+                *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[1], v[2], v[3]};
+                *reinterpret_cast<f32x4*>(cp + 4) = f32x4{v[4], v[5], v[6], v[7]};
+              }
+            } else {
+              const u32x4 x = rz[i & 1][j][h];
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                v[e] += __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16));
+            }
+            u32x4 w;
+#pragma unroll
+            for (int q2 = 0; q2 < 4; ++q2)
+              w[q2] = (uint32_t)f32_to_bf16(v[2 * q2]) | ((uint32_t)f32_to_bf16(v[2 * q2 + 1]) << 16);
+            const bool st = ok && (!cls || p.ln_out != nullptr);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                w, rc, st ? ((row - m0) * (int)p.ldc + col) * 2 : nrec, 0, 0);
+            if (ok) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                ssum += v[e];
+                ssq = fmaf(v[e], v[e], ssq);
+              }
+            }
+            wait_lds();  // the slot is rewritten by the next pass
+          }
+        if (p.ln_out != nullptr) {  // this row's 64-column segment: lanes l and l ^ 1
+          ssum += dpp_f<kDppXor1>(ssum);
+          ssq += dpp_f<kDppXor1>(ssq);
+          if ((lane & 1) == 0 && row_ok && 64 * seg < p.N)
+            p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(ssum, ssq);
+        }
+      }
+    } else {
+      // Folded LayerNorm: (rstd, -rstd * mean) of this lane's 4 rows.
+      float2 rs[TM];
+      if constexpr (LNF) {
+  #pragma unroll
+        for (int i = 0; i < TM; ++i) rs[i] = rowst[par * BM + wm * WTM + i * 32 + lr];
+      }
+      const int lane_st = ((wm * WTM + (lane >> 2)) * (int)p.ldc + n0 + wn * WTN + (lane & 3) * 8) * 2;
+      const int wofs = lr * ES + lg * 8, rofs = (lane >> 2) * ES + (lane & 3) * 16;
+  #pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        int lst = lane_st, wo = wofs, ro = rofs;
+        asm volatile("" : "+v"(lst), "+v"(wo), "+v"(ro));
+  #pragma unroll
+        for (int j = 0; j < TN; ++j) {
+  #pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            float t[4];
+  #pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if constexpr (LNF)
+                t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[j][g][e], bv[j][g][e]));
+              else
+                t[e] = acc[i][j][4 * g + e] + bv[j][g][e];
+              if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
+            }
+            u32x2 w;
+            w[0] = (uint32_t)f32_to_bf16(t[0]) | ((uint32_t)f32_to_bf16(t[1]) << 16);
+            w[1] = (uint32_t)f32_to_bf16(t[2]) | ((uint32_t)f32_to_bf16(t[3]) << 16);
+            *reinterpret_cast<u32x2*>(slot + wo + g * 16) = w;
+          }
+          wait_lds();
+  #pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const u32x2 lo = *reinterpret_cast<const u32x2*>(slot + ro + h * 16 * ES);
+            const u32x2 hi = *reinterpret_cast<const u32x2*>(slot + ro + h * 16 * ES + 8);
+            const int rl = wm * WTM + i * 32 + h * 16 + (lane >> 2);
+            const int col = n0 + wn * WTN + j * 32 + (lane & 3) * 8;
+            const bool ok = rl < rows_valid && col + 8 <= p.N;
+            const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+            __builtin_amdgcn_raw_buffer_store_b128(
+                w, rc, ok ? lst + (i * 32 + h * 16) * (int)p.ldc * 2 + j * 64 : nrec, 0, 0);
+          }
+          wait_lds();  // the slot is rewritten by the next block
+        }
       }
     }
     if (!has_next) break;
@@ -943,9 +1064,12 @@ int device_cus() {
 
 template <Epi E>
 bool persistent_ok(const Params& p) {
-  if constexpr (E != Epi::Bias && E != Epi::BiasGelu) {
+  if constexpr (E != Epi::Bias && E != Epi::BiasGelu && E != Epi::BiasResid) {
     return false;
   } else {
+    // Residual GEMMs: only with short K (the projection), where the epilogue is a
+    // large share of a tile (measured: K = 128 -10%, K = 768 -1%, K = 3072 +2%).
+    if (E == Epi::BiasResid && (p.K > 1024 || (p.res != nullptr && p.ldres % 8 != 0))) return false;
     return p.bias != nullptr && !p.relu && p.aux == nullptr && p.ksplit <= 1 && p.K >= kBK &&
            p.K % kBK == 0 && p.N % 8 == 0 &&
            p.ldc % 8 == 0 && (int64_t)kTilePers * p.ldc * 2 < ((int64_t)1 << 31);
@@ -955,7 +1079,7 @@ bool persistent_ok(const Params& p) {
 // Rows [0, rows) of the 256x256 tiling with the persistent kernel.
 template <Epi E>
 hipError_t launch_persistent(const Params& p0, int rows, hipStream_t s) {
-  if constexpr (E != Epi::Bias && E != Epi::BiasGelu) {
+  if constexpr (E != Epi::Bias && E != Epi::BiasGelu && E != Epi::BiasResid) {
     return hipErrorInvalidValue;
   } else {
     Params p = p0;
@@ -963,15 +1087,23 @@ hipError_t launch_persistent(const Params& p0, int rows, hipStream_t s) {
     p.row0 = 0;
     p.tiles_n = (p.N + 255) / 256;
     // Row panels per group of the tile order: measured best at 8 for outputs of
-    // at most 9 tiles across (q/k/v), 4 for wider ones (fc1).
-    p.group_m = p.tiles_n <= 9 ? 8 : 4;
+    // at most 9 tiles across (q/k/v), 4 for wider ones (fc1); the residual
+    // GEMMs keep the non-persistent kernel's choice.
+    if (E == Epi::BiasResid)
+      p.group_m = p.K >= 2048 ? 2 : 4;
+    else
+      p.group_m = p.tiles_n <= 9 ? 8 : 4;
     const int64_t tiles = (int64_t)((rows + 255) / 256) * p.tiles_n;
     if (tiles <= 0) return hipSuccess;
     const int grid = (int)std::min<int64_t>(tiles, device_cus());
-    if (p.ln_in != nullptr)
-      hipLaunchKernelGGL((gemm_bf16_persistent<E, true>), dim3(grid), dim3(512), 0, s, p);
-    else
+    if constexpr (E == Epi::BiasResid) {
       hipLaunchKernelGGL((gemm_bf16_persistent<E, false>), dim3(grid), dim3(512), 0, s, p);
+    } else {
+      if (p.ln_in != nullptr)
+        hipLaunchKernelGGL((gemm_bf16_persistent<E, true>), dim3(grid), dim3(512), 0, s, p);
+      else
+        hipLaunchKernelGGL((gemm_bf16_persistent<E, false>), dim3(grid), dim3(512), 0, s, p);
+    }
     return hipGetLastError();
   }
 }

@@ -135,6 +135,8 @@ LINEAR_CASES = [
     (BF16, ffi.EPI_BIAS, 7000, 2304, 768, 768, 768, 2304),
     (BF16, ffi.EPI_BIAS, 20000, 2304, 768, 768, 768, 2304),
     (BF16, ffi.EPI_BIAS_GELU, 12800, 1272, 384, 384, 384, 1280),
+    (BF16, ffi.EPI_BIAS_RESID, 12800, 1272, 384, 384, 384, 1280),
+    (BF16, ffi.EPI_BIAS_RESID, 30000, 768, 1024, 1024, 1024, 768),
     # outputs at most 64 wide: 256x64 tiles
     (BF16, ffi.EPI_BIAS, 3001, 64, 256, 256, 256, 64),
     (BF16, ffi.EPI_BIAS_RESID, 777, 40, 576, 576, 576, 48),
