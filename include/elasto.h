@@ -337,7 +337,10 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
  * of `tokens` rows.  qkv row (b*tokens + t) holds, for slot s, q at columns
  * s*3*hd + [0,hd), k at + [hd,2hd), v at + [2hd,3hd), with row stride
  * qkv_stride; o row holds slot s at columns s*hd + [0,hd), row stride
- * o_stride.  Scores are scaled by `scale`.  BF16 path: head_dim == 64. */
+ * o_stride.  Scores are scaled by `scale`.  BF16 path: head_dim == 64,
+ * tokens <= 240, qkv 16-byte aligned with qkv_stride a multiple of 8, o
+ * 8-byte aligned with o_stride a multiple of 4 and tokens * o_stride * 2
+ * below 2^31. */
 elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_stride, void* o,
                                     int64_t o_stride, int32_t batch, int32_t tokens,
                                     int32_t heads, int32_t head_dim, float scale,

@@ -699,8 +699,11 @@ elasto_status_t elasto_op_attention(int32_t dtype, const void* qkv, int64_t qkv_
   a.batch = batch; a.tokens = tokens; a.heads = heads; a.head_dim = head_dim; a.scale = scale;
   hipError_t e;
   if (dtype == ELASTO_BF16) {
-    if (head_dim != 64 || tokens > kAttnMaxTokens || qkv_stride % 8 || !aligned(qkv, 16))
-      return fail(ELASTO_ERR_INVALID_ARG, "bf16 attention needs head_dim 64, tokens <= %d, aligned qkv", kAttnMaxTokens);
+    if (head_dim != 64 || tokens > kAttnMaxTokens || qkv_stride % 8 || !aligned(qkv, 16) ||
+        o_stride % 4 || !aligned(o, 8) || (int64_t)tokens * o_stride * 2 > INT32_MAX)
+      return fail(ELASTO_ERR_INVALID_ARG,
+                  "bf16 attention needs head_dim 64, tokens <= %d, aligned qkv and o, o range < 2^31",
+                  kAttnMaxTokens);
     e = launch_attention_bf16(a, static_cast<hipStream_t>(hip_stream));
   } else if (dtype == ELASTO_FP32) {
     if (head_dim > 128) return fail(ELASTO_ERR_INVALID_ARG, "fp32 attention needs head_dim <= 128");

@@ -2,21 +2,25 @@
 // o = softmax(q k^T * scale) v per (sequence, head slot).
 //
 // bf16 path (head_dim 64): one workgroup of 8 waves per (sequence, head
-// slot), so no wave takes more than two of the (up to 15) query blocks.  K is
-// staged whole in LDS by direct global->LDS loads (rows of 128 B, 16-byte
-// chunks XOR-swizzled) and V is staged transposed (V^T, one row per feature);
-// padding keys past the last token repeat that token and are masked (zero
-// probability).  Each wave takes 16-query blocks in turn and computes the score
-// block transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16: lane l then
-// holds the scores of query l%16 against keys 16j + 4*(l/16) + {0..3}.  The
-// softmax of a query is reduced over its 4 lanes with two xor-shuffles and
-// is exact (single pass: the whole key row fits in registers).  The
-// probabilities are rounded to bf16 and fed straight back as the A operand
-// of O = P V: a k-slot of the MFMA is only a label, so the 8 keys a lane
-// holds for two adjacent key tiles form its k-slots, and the V operand is
-// read from V^T with the same key-to-slot assignment (two 8-byte reads).
-// The 1/rowsum normalisation is applied to O in fp32; each wave stages its
-// 16x64 O block in LDS and writes it as 16-byte row chunks.
+// slot), so no wave takes more than two of the (up to 15) query blocks.  K and
+// V are staged whole in LDS by direct global->LDS loads, both in token-row
+// layout (rows of 128 B, 16-byte chunks XOR-swizzled); padding keys past the
+// last token repeat that token and are masked (zero probability).  Each wave
+// takes 16-query blocks in turn and computes the score block transposed,
+// S^T = K Q^T, with v_mfma_f32_16x16x32_bf16: lane l then holds the scores of
+// query l%16 against keys 16j + 4*(l/16) + {0..3}.  The softmax of a query is
+// reduced over its 4 lanes with two xor-shuffles and is exact (single pass:
+// the whole key row fits in registers).  The probabilities are rounded to
+// bf16 and are reused unchanged as the k-slots of the second product, which
+// is also taken transposed, O^T = V^T P^T: the MFMA's k-slots are only
+// labels, so the 8 keys a lane holds for two adjacent key tiles form its
+// k-slots, and the V^T operand is read from the row-major V with the LDS
+// transpose read (ds_read_b64_tr_b16: in each group of 16 lanes, lane i
+// receives element i%4 of the 8-byte pieces that lanes i/4, 4 + i/4, 8 + i/4
+// and 12 + i/4 address, so four key rows x 16 feature columns come back as
+// four keys per lane, one column per lane).  Lane l then holds features
+// 16n + 4*(l/16) + {0..3} of query l%16: the 1/rowsum normalisation is
+// applied in fp32 and each lane writes 8-byte pieces of its query's row.
 //
 // fp32 path: a plain per-query loop (two passes over the keys: max, then
 // exp-sum and weighted V sum), fp32 FMA throughout.
@@ -28,15 +32,16 @@ namespace {
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kHd = 64;
-constexpr int kNtMax = 15;  // 16-key tiles: tokens <= 240
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kOs = 72;     // O staging row stride (elements): 144 B, 16-byte aligned
-constexpr int kOStage = 16 * kOs * 2;  // bytes per wave
+constexpr int kRsrcWord3 = 0x00020000;  // buffer resource: raw (unswizzled) 32-bit records
 
-__device__ __forceinline__ int k_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+// Byte offset of logical 16-byte chunk c of token row r in a staged K or V.
+__device__ __forceinline__ int kv_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
 struct AttnP {
   const uint16_t* qkv;
@@ -51,12 +56,11 @@ struct AttnP {
 // keys is fully unrolled and only the last tile carries the key < T mask.
 template <int NT>
 __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
-  constexpr int TV = NT * 16;  // keys staged in V^T
-  constexpr int VS = TV + 4;   // V^T row stride (elements): rows land on distinct banks
+  constexpr int KV = NT * 16 * 128;  // bytes of the staged K (and of V)
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int T = p.T;
-  char* kl = smem;
-  uint16_t* vt = reinterpret_cast<uint16_t*>(smem + NT * 16 * 128);
+  const char* kl = smem;
+  const char* vl = smem + KV;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x / p.heads, s = blockIdx.x - b * p.heads;
@@ -74,43 +78,33 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
   bf16x8 qf[2];
   if (wave < NT) load_q(wave, qf);
 
-  // K: direct global->LDS loads in 1-KB blocks of 8 rows.  Lane l lands at
-  // block + 16 l, i.e. row 8*blk + l/8, physical chunk l%8, so it fetches the
-  // logical chunk that k_off() places there.  Rows past the last token re-read
-  // token T-1: their scores are masked out of the softmax.
+  // K and V: direct global->LDS loads in 1-KB blocks of 8 token rows (blocks
+  // 0 .. 2NT-1 are K, the next 2NT are V).  Lane l lands at block + 16 l,
+  // i.e. row 8*blk + l/8, physical chunk l%8, so it fetches the logical chunk
+  // that kv_off() places there.  Rows past the last token re-read token T-1:
+  // their scores are masked out and their probabilities are 0.
 #pragma unroll
-  for (int i = 0; i < (2 * NT + kWaves - 1) / kWaves; ++i) {
+  for (int i = 0; i < (4 * NT + kWaves - 1) / kWaves; ++i) {
     const int blk = wave + kWaves * i;
-    if (blk < 2 * NT) {
-      const int r = blk * 8 + (lane >> 3);
+    if (blk < 4 * NT) {
+      const int isv = blk >= 2 * NT;
+      const int r = (blk - (isv ? 2 * NT : 0)) * 8 + (lane >> 3);
       const int c = (lane & 7) ^ (r & 7);
-      const uint16_t* src = base + (int64_t)min(r, T - 1) * p.qs + kHd + c * 8;
-      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)(kl + blk * 1024), 16, 0, 0);
+      const uint16_t* src = base + (int64_t)min(r, T - 1) * p.qs + (1 + isv) * kHd + c * 8;
+      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)(smem + blk * 1024), 16, 0, 0);
     }
   }
-  // V: every 16-byte chunk load is issued before any transposed LDS write.
-  // Keys past the last token re-read token T-1: their probabilities are 0.
-  constexpr int kVLoads = (TV * 8 + kThreads - 1) / kThreads;
-  u32x4 vv[kVLoads];
-#pragma unroll
-  for (int i = 0; i < kVLoads; ++i) {
-    const int idx = tid + kThreads * i, key = min(idx >> 3, T - 1), c = idx & 7;
-    vv[i] = *reinterpret_cast<const u32x4*>(base + (int64_t)key * p.qs + 2 * kHd + c * 8);
-  }
-#pragma unroll
-  for (int i = 0; i < kVLoads; ++i) {
-    const int idx = tid + kThreads * i, key = idx >> 3, c = idx & 7;
-    if (key < TV) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        vt[(c * 8 + e) * VS + key] =
-            (uint16_t)((e & 1) ? (vv[i][e >> 1] >> 16) : (vv[i][e >> 1] & 0xffffu));
-    }
-  }
+  // Nothing reads the staged rows by register dependence: wait for every
+  // vector memory operation of this wave (vmcnt 0), then for every wave.
+  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
   __syncthreads();
 
+  // Output rows of this (sequence, head slot): T rows of p.os elements from
+  // column s*64; an offset of nrec drops the store (rows past the last token).
+  const int nrec = T * (int)p.os * 2;
+  const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+      p.o + (int64_t)b * T * p.os + (int64_t)s * kHd, (short)0, nrec, kRsrcWord3);
   const float c2 = p.scale_log2;
-  uint16_t* ost = reinterpret_cast<uint16_t*>(smem + NT * 16 * 128 + kHd * VS * 2 + wave * kOStage);
   for (int qb = wave; qb < NT; qb += kWaves) {
     const int q0 = qb * 16;
     f32x4 st[NT];
@@ -119,7 +113,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + k_off(j * 16 + lq, kk * 4 + lg));
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + kv_off(j * 16 + lq, kk * 4 + lg));
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], acc, 0, 0, 0);
       }
       st[j] = acc;
@@ -156,9 +150,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     sum += __shfl_xor(sum, 32, 64);
     __builtin_amdgcn_sched_barrier(0);
 
+    // O^T = V^T P^T over key pairs of tiles (2kb, 2kb+1): k-slot 8*lg + r is
+    // key 32kb + 4lg + r, k-slot 8*lg + 4 + r is key 32kb + 16 + 4lg + r.
     f32x4 o[4];
 #pragma unroll
     for (int n = 0; n < 4; ++n) o[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int vr = 4 * lg + (lq >> 2);  // key row this lane addresses, within a 32-key pair
 #pragma unroll
     for (int kb = 0; kb < (NT + 1) / 2; ++kb) {
       const bool has_hi = 2 * kb + 1 < NT;
@@ -171,33 +168,31 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
       }
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
-        const uint16_t* vp = vt + (n * 16 + lq) * VS + kb * 32 + 4 * lg;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
+        // This lane addresses columns 16n + 4(lq%4) .. +3 of key row 32kb + vr
+        // (and of the row 16 keys further for the upper k-slots).
+        const int col = n * 16 + 4 * (lq & 3), half = (col & 4) * 2;
+        const int r0 = kb * 32 + vr;
+        const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4*)(vl + kv_off(r0, col >> 3) + half)));
         u32x2 hi = {0u, 0u};
-        if (has_hi) hi = *reinterpret_cast<const u32x2*>(vp + 16);
+        if (has_hi)
+          hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(vl + kv_off(r0 + 16, col >> 3) + half)));
         const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-        o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8, w), o[n],
+        o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), pa, o[n],
                                                        0, 0, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    // Lane (lg, lq) holds O[q0 + lq][16n + 4lg + r], r = 0..3.
     const float inv = 1.0f / sum;  // for query lq
+    const int q = q0 + lq;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qr = 4 * lg + r;
-      const float ir = __shfl(inv, qr, 64);
-#pragma unroll
-      for (int n = 0; n < 4; ++n) ost[qr * kOs + n * 16 + lq] = f32_to_bf16(o[n][r] * ir);
-    }
-    // The block's own LDS writes are complete before its lanes read them back.
-    __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int qr = h * 8 + (lane >> 3), c = lane & 7;
-      const int q = q0 + qr;
-      const u32x4 w = *reinterpret_cast<const u32x4*>(ost + qr * kOs + c * 8);
-      if (q < T)
-        *reinterpret_cast<u32x4*>(p.o + ((int64_t)b * T + q) * p.os + (int64_t)s * kHd + c * 8) = w;
+    for (int n = 0; n < 4; ++n) {
+      const u32x2 w = {(uint32_t)f32_to_bf16(o[n][0] * inv) | ((uint32_t)f32_to_bf16(o[n][1] * inv) << 16),
+                       (uint32_t)f32_to_bf16(o[n][2] * inv) | ((uint32_t)f32_to_bf16(o[n][3] * inv) << 16)};
+      __builtin_amdgcn_raw_buffer_store_b64(w, ro, q < T ? (q * (int)p.os + 16 * n + 4 * lg) * 2 : nrec,
+                                            0, 0);
     }
     qf[0] = qn[0];
     qf[1] = qn[1];
@@ -206,8 +201,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
 
 template <int NT>
 hipError_t launch_attn_nt(const AttnP& p, int batch, int heads, hipStream_t s) {
-  const size_t lds =
-      (size_t)NT * 16 * 128 + (size_t)kHd * (NT * 16 + 4) * 2 + (size_t)kWaves * kOStage;
+  const size_t lds = 2 * (size_t)NT * 16 * 128;
   hipLaunchKernelGGL(attention_bf16_kernel<NT>, dim3((unsigned)(batch * heads)), dim3(kThreads),
                      lds, s, p);
   return hipGetLastError();
@@ -262,6 +256,11 @@ __global__ __launch_bounds__(256) void attention_f32_kernel(AttnF p) {
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.batch <= 0 || a.heads <= 0 || a.tokens <= 0) return hipSuccess;
   if (a.head_dim != kHd || a.tokens > kAttnMaxTokens) return hipErrorInvalidValue;
+  // The output of a (sequence, head slot) is addressed as one buffer range of
+  // T rows: the rows must hold every head slot and the range must fit 31 bits.
+  if (a.o_stride < (int64_t)a.heads * kHd || a.qkv_stride < (int64_t)a.heads * 3 * kHd ||
+      (int64_t)a.tokens * a.o_stride * 2 > INT32_MAX)
+    return hipErrorInvalidValue;
   AttnP p;
   p.qkv = static_cast<const uint16_t*>(a.qkv);
   p.qs = a.qkv_stride;
