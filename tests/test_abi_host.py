@@ -202,6 +202,20 @@ def test_op_entry_points_validate_before_any_hip_call(lib):
     assert ln(0, p16, 768, p16, 197, p16, 4, 768, p16, p16, f, None) == 1   # x_cls needs bf16
     assert ln(1, p16, 768, p16, 0, p16, 4, 768, p16, p16, f, None) == 1     # tokens >= 1
     assert lib.elasto_last_error()
+    # bf16 attention: head_dim 64, tokens <= 240, qkv 16-byte and o 8-byte aligned,
+    # o_stride a multiple of 4 covering every head slot, the o range of one
+    # sequence below 2^31 bytes
+    at = lib.elasto_op_attention
+    p4 = ctypes.c_void_p((1 << 20) + 4)
+    s = ctypes.c_float(0.125)
+    assert at(1, p16, 384, p16, 128, 2, 197, 2, 32, s, None) == 1          # head_dim
+    assert at(1, p16, 384, p16, 128, 2, 241, 2, 64, s, None) == 1          # tokens
+    assert at(1, p8, 384, p16, 128, 2, 197, 2, 64, s, None) == 1           # qkv alignment
+    assert at(1, p16, 384, p4, 128, 2, 197, 2, 64, s, None) == 1           # o alignment
+    assert at(1, p16, 384, p16, 130, 2, 197, 2, 64, s, None) == 1          # o_stride % 4
+    assert at(1, p16, 384, p16, 64, 2, 197, 2, 64, s, None) == 1           # o_stride < heads * 64
+    assert at(1, p16, 384, p16, 1 << 23, 2, 240, 2, 64, s, None) == 1      # o range >= 2^31
+    assert at(1, p16, 320, p16, 128, 2, 197, 2, 64, s, None) == 1          # qkv_stride < 3 heads 64
 
 
 def test_conv2d_validates_before_any_hip_call(lib):
