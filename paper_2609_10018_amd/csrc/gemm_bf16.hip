@@ -1114,9 +1114,10 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
   // number of rounds of concurrent workgroups (one per CU) times the relative
   // cost of one tile.  Besides single launches of one tile shape there is a
   // split plan against wave quantisation: the whole rounds of 256x256 tiles
-  // first, then the remaining row panels as 128x256 tiles in a second launch.
+  // first, then the remaining row panels as 128x256 or 128x128 tiles
+  // (whichever takes fewer tile-weighted rounds) in a second launch.
   constexpr int kCUs = 256;
-  constexpr double kRel128x256 = 0.6;
+  constexpr double kRel128x256 = 0.6, kRel128x128 = 0.36;
   auto rounds = [](int64_t tiles) { return (double)((tiles + kCUs - 1) / kCUs); };
   struct Cfg { int bm, bn; double rel; };
   // 256x64 (four waves stacked along M) only for outputs at most 64 wide,
@@ -1133,8 +1134,10 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
   const int64_t tn = (p.N + 255) / 256, total = tn * ((p.M + 255) / 256);
   const int64_t head_rows = (total / kCUs) * kCUs / tn * 256;  // rows in whole rounds
   if (head_rows > 0 && head_rows < p.M) {
-    const int64_t tail_tiles = ((p.M - head_rows + 127) / 128) * tn;
-    const double t = rounds(head_rows / 256 * tn) + kRel128x256 * rounds(tail_tiles);
+    const int64_t tail_panels = (p.M - head_rows + 127) / 128;
+    const double t_wide = kRel128x256 * rounds(tail_panels * tn);
+    const double t_sq = kRel128x128 * rounds(tail_panels * ((p.N + 127) / 128));
+    const double t = rounds(head_rows / 256 * tn) + std::min(t_wide, t_sq);
     if (t < best_t - 0.1) {
       Params head = p;
       head.M = (int)head_rows;
@@ -1142,6 +1145,7 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
                          ? launch_persistent<E>(p, (int)head_rows, s)
                          : launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
       if (e != hipSuccess) return e;
+      if (t_sq < t_wide - 1e-9) return launch_cfg<128, 128, 2, 2, E, CONV>(p, (int)head_rows, s);
       return launch_cfg<128, 256, 2, 4, E, CONV>(p, (int)head_rows, s);
     }
   }
