@@ -181,7 +181,7 @@ hipError_t launch_ln_fold(const void* W, int N, int D, const float* gamma, const
                           const float* bias, const int32_t* widths, int nw, void* Wf,
                           float* colsum, float* cbias, int64_t ldv, hipStream_t s);
 
-// Largest token count the bf16 attention kernel supports (K and V^T of one
+// Largest token count the bf16 attention kernel supports (K and V of one
 // head are staged whole in LDS).
 constexpr int kAttnMaxTokens = 240;
 
