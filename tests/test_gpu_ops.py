@@ -194,6 +194,10 @@ def _attention_ref(qkv, B, T, h, hd, scale):
     (BF16, 2, 17, 2, 64, 384),
     (BF16, 1, 240, 3, 64, 576),
     (BF16, 2, 1, 2, 64, 384),
+    # the last key tile exactly full: one tile, an even and an odd tile count
+    (BF16, 3, 16, 2, 64, 384),
+    (BF16, 2, 32, 3, 64, 576),
+    (BF16, 2, 224, 2, 64, 384),
     # more (sequence, head) pairs than workgroups: each walks several pairs
     (BF16, 100, 197, 3, 64, 576),
     (BF16, 130, 33, 4, 64, 768),
