@@ -207,8 +207,12 @@ __device__ __forceinline__ u32x4 mask_tail(u32x4 v, int kbeg, int kend) {
   return o;
 }
 
-template <int BM, int BN, int WM, int WN, Epi E, bool CONV>
+// STAGES: LDS stages of the tile loads (2: the next K step in flight while
+// this one computes; 4: three steps in flight, for launches of few tiles whose
+// K chain is bound by the load latency; needs K % 64 == 0 and no CONV).
+template <int BM, int BN, int WM, int WN, Epi E, bool CONV, int STAGES = 2>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
+  static_assert(STAGES == 2 || (STAGES == 4 && !CONV), "stage counts");
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -217,7 +221,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   static_assert((ABLK + BBLK) % NW == 0, "blocks must split evenly over waves");
   constexpr int STAGE = (BM + BN) * kRowBytes;
   constexpr int EPI_BYTES = (BM > 128 ? 128 : BM) * (BN + 8) * 4;
-  constexpr int SMEM_MAIN = 2 * STAGE > EPI_BYTES ? 2 * STAGE : EPI_BYTES;
+  constexpr int SMEM_MAIN = STAGES * STAGE > EPI_BYTES ? STAGES * STAGE : EPI_BYTES;
   constexpr bool LN_CONSUMER = E == Epi::Bias || E == Epi::BiasGelu;
   constexpr bool LN_PRODUCER = E == Epi::BiasResid || E == Epi::Patch;
   constexpr int SMEM = SMEM_MAIN + (LN_CONSUMER ? BM * 8 : 0);  // + per-row LN factors
@@ -392,12 +396,29 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
   const int lr = lane & 31, lg = lane >> 5;
-  issue(0, 0, 0, PER_WAVE);
+  if constexpr (STAGES == 2) issue(0, 0, 0, PER_WAVE);
+  else {
+#pragma unroll
+    for (int s0 = 0; s0 < STAGES - 1; ++s0)
+      if (s0 < nk) issue(s0, s0, 0, PER_WAVE);
+  }
   for (int kt = 0; kt < nk; ++kt) {
-    wait_vm_lds<0>();
-    __builtin_amdgcn_s_barrier();
-    if (kt + 1 < nk) issue((kt + 1) & 1, kt + 1, 0, PER_WAVE);
-    const char* cur = smem + (kt & 1) * STAGE;
+    if constexpr (STAGES == 2) {
+      wait_vm_lds<0>();
+      __builtin_amdgcn_s_barrier();
+      if (kt + 1 < nk) issue((kt + 1) & 1, kt + 1, 0, PER_WAVE);
+    } else {
+      // Step kt's loads have landed when no more than the later steps' loads
+      // (PER_WAVE each, issued in order) are in flight.
+      const int ahead = min(STAGES - 2, nk - 1 - kt);
+      if (ahead >= 2) wait_vm_lds<2 * PER_WAVE>();
+      else if (ahead == 1) wait_vm_lds<PER_WAVE>();
+      else wait_vm_lds<0>();
+      __builtin_amdgcn_s_barrier();
+      // The stage of step kt - 1, which every wave has finished reading.
+      if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1, 0, PER_WAVE);
+    }
+    const char* cur = smem + (STAGES == 2 ? (kt & 1) : (kt % STAGES)) * STAGE;
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       const int c = kk * 2 + lg;
@@ -1031,7 +1052,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, Epi E, bool CONV>
+template <int BM, int BN, int WM, int WN, Epi E, bool CONV, int STAGES = 2>
 hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   Params p = p0;
   p.row0 = row0;
@@ -1042,7 +1063,7 @@ hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   p.group_m = p.K >= 2048 ? 2 : 4;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E, CONV>),
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E, CONV, STAGES>),
                      dim3((unsigned)blocks, (unsigned)(p.ksplit > 1 ? p.ksplit : 1)),
                      dim3(64 * WM * WN), 0, s, p);
   return hipGetLastError();
@@ -1154,7 +1175,15 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
       if (!CONV && persistent_ok<E>(p)) return launch_persistent<E>(p, p.M, s);
       return launch_cfg<256, 256, 2, 4, E, CONV>(p, 0, s);
     case 1: return launch_cfg<256, 128, 2, 2, E, CONV>(p, 0, s);
-    case 2: return launch_cfg<128, 128, 2, 2, E, CONV>(p, 0, s);
+    case 2:
+      // Less than a round of tiles: each workgroup's K chain is the critical
+      // path, so keep three steps of loads in flight.
+      if constexpr (!CONV && (E == Epi::Bias || E == Epi::BiasGelu || E == Epi::BiasResid)) {
+        const int64_t tiles = ((p.M + 127) / 128) * ((p.N + 127) / 128);
+        if (tiles < kCUs && p.K % kBK == 0 && p.K / kBK >= 4)
+          return launch_cfg<128, 128, 2, 2, E, CONV, 4>(p, 0, s);
+      }
+      return launch_cfg<128, 128, 2, 2, E, CONV>(p, 0, s);
     default: return launch_cfg<256, 64, 4, 1, E, CONV>(p, 0, s);
   }
 }
