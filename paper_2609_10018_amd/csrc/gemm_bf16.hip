@@ -1166,7 +1166,14 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
                          ? launch_persistent<E>(p, (int)head_rows, s)
                          : launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
       if (e != hipSuccess) return e;
-      if (t_sq < t_wide - 1e-9) return launch_cfg<128, 128, 2, 2, E, CONV>(p, (int)head_rows, s);
+      if (t_sq < t_wide - 1e-9) {
+        // One round or less of square tiles: the K chains are the critical path.
+        if constexpr (!CONV && (E == Epi::Bias || E == Epi::BiasGelu || E == Epi::BiasResid)) {
+          if (tail_panels * ((p.N + 127) / 128) < kCUs && p.K % kBK == 0 && p.K / kBK >= 4)
+            return launch_cfg<128, 128, 2, 2, E, CONV, 4>(p, (int)head_rows, s);
+        }
+        return launch_cfg<128, 128, 2, 2, E, CONV>(p, (int)head_rows, s);
+      }
       return launch_cfg<128, 256, 2, 4, E, CONV>(p, (int)head_rows, s);
     }
   }
