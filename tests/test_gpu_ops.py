@@ -137,6 +137,9 @@ LINEAR_CASES = [
     (BF16, ffi.EPI_BIAS_GELU, 12800, 1272, 384, 384, 384, 1280),
     (BF16, ffi.EPI_BIAS_RESID, 12800, 1272, 384, 384, 384, 1280),
     (BF16, ffi.EPI_BIAS_RESID, 30000, 768, 1024, 1024, 1024, 768),
+    # fewer 128x128 tiles than CUs: 4-stage load pipeline (48 K steps; exactly 4)
+    (BF16, ffi.EPI_BIAS_RESID, 400, 768, 3072, 3072, 3072, 768),
+    (BF16, ffi.EPI_BIAS, 500, 512, 256, 256, 256, 512),
     # outputs at most 64 wide: 256x64 tiles
     (BF16, ffi.EPI_BIAS, 3001, 64, 256, 256, 256, 64),
     (BF16, ffi.EPI_BIAS_RESID, 777, 40, 576, 576, 576, 48),
