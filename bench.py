@@ -101,6 +101,95 @@ def cpu_baseline(cfg, table, w_stored, x_stored, budget_s=15.0, max_images=256):
             "cpu_model": cpu_model, "blas": blas, "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
+def next_rows(torch, ffi, inputs, stream, with_cpu, steps=20, warmup=3):
+    """The widened rows, measured like the headline: the elastic ResNet-50 forward
+    (batch 256, every DN mode) and the ViT-B growth step (batch 64, mode 0 grown
+    from mode 1), each with the fp64 oracle timed beside it on a small sample."""
+    from paper_2609_10018_amd import cost
+    from paper_2609_10018_amd.inputs_cnn import (CNN_CONFIGS, make_cnn_images, make_cnn_table,
+                                                 make_cnn_weights, stored_cnn_weights)
+    out = {}
+    # Elastic ResNet-50 (Eq. 7 channel prefixes), bf16, batch 256.
+    ccfg = CNN_CONFIGS["resnet50"]
+    cw, ct = make_cnn_weights(ccfg), make_cnn_table(ccfg)
+    B = ccfg.batch
+    cx = make_cnn_images(ccfg, B)
+    net = ffi.ElasticResNet(ccfg, cw, ct, B)
+    cxd = torch.from_numpy(cx).to(torch.bfloat16).cuda().contiguous()
+    clog = torch.empty((B, ccfg.num_classes), dtype=torch.float32, device="cuda")
+    modes = []
+    for k in range(ct.num_modes):
+        net.set_mode(k)
+        for _ in range(warmup):
+            net.forward(cxd, clog, stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            net.set_mode(k)
+            net.forward(cxd, clog, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        flop = 2.0 * cost.cnn_macs(ccfg, ct, k)
+        modes.append({"mode": k, "ms": ms, "images_per_s": B * 1e3 / ms,
+                      "gflop_per_image": flop / 1e9,
+                      "tflops": flop * B / (ms * 1e-3) / 1e12,
+                      "mfu": flop * B / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS})
+    net.close()
+    res = {"workload": "elastic ResNet-50 forward, batch 256, 224x224x3, bf16",
+           "steps": steps, "per_mode": modes}
+    log(f"resnet50 b256 mode 0: {modes[0]['images_per_s']:.0f} images/s")
+    if with_cpu:
+        import oracle.resnet as orn
+        sw, xs = stored_cnn_weights(ccfg, cw), inputs.bf16_round(cx[:32])
+        n, t0 = 0, time.perf_counter()
+        while n < 32 and time.perf_counter() - t0 < 5.0:
+            orn.elastic_forward(sw, ccfg, ct, 0, xs[n:n + 2])
+            n += 2
+        dt = time.perf_counter() - t0
+        res["cpu_oracle"] = {"value": n / dt, "unit": "images/s", "kind": "oracle",
+                             "sample": f"{n} images, DN mode 0, fp64 numpy, {dt:.1f} s wall"}
+    out["resnet50"] = res
+    # Growth step (Eq. 9): ViT-B, batch 64, mode 0 grown from mode 1.
+    cfg = inputs.CONFIGS["vit_b"]
+    w, t = inputs.make_weights(cfg), inputs.make_dn_table(cfg)
+    GB = 64
+    x = inputs.make_images(cfg, GB)
+    y = np.random.default_rng(4).integers(0, cfg.num_classes, size=GB)
+    vit = ffi.ElasticViT(cfg, w, t, GB)
+    gc = ffi.GrowthContext(vit, GB)
+    xd = torch.from_numpy(x).to(torch.bfloat16).cuda().contiguous()
+    yd = torch.from_numpy(y.astype(np.int32)).cuda()
+    for _ in range(warmup):
+        gc.step(0, xd, yd, 1e-4, 1.0, None, stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    gsteps = max(1, steps // 2)
+    e0.record(stream)
+    for _ in range(gsteps):
+        gc.step(0, xd, yd, 1e-4, 1.0, None, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / gsteps
+    gres = {"workload": "ViT-B/16 growth step (mode 0 from mode 1), batch 64, bf16 with fp32 "
+                        "masters", "steps": gsteps, "ms_per_step": ms,
+            "images_per_s": GB * 1e3 / ms}
+    gc.close()
+    vit.close()
+    log(f"growth step b64: {ms:.2f} ms")
+    if with_cpu:
+        import oracle.growth as og
+        t0 = time.perf_counter()
+        og.growth_step(inputs.stored_weights(cfg, w), cfg, t, 0, inputs.stored_images(cfg, x[:2]),
+                       y[:2], lr=1e-4, clip=1.0)
+        dt = time.perf_counter() - t0
+        gres["cpu_oracle"] = {"value": 2 / dt, "unit": "images/s", "kind": "oracle",
+                              "sample": f"one step on 2 images, fp64 numpy, {dt:.1f} s wall"}
+    out["growth_step"] = gres
+    return out
+
+
 def latency_regime(torch, ffi, inputs, cfg, w, table, calls=1000, warmup=10):
     out = {}
     seq = inputs.mode_sequence(calls + warmup, table.num_modes)
@@ -167,6 +256,10 @@ def main():
                     help="skip the modes that also narrow the embedding (ViT-B, d 768..192)")
     ap.add_argument("--work-out", type=str, default=None,
                     help="write the algorithmic work per kernel class (mode 0) to this JSON file")
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip the widened rows (ResNet-50 forward, growth step)")
+    ap.add_argument("--next-only", action="store_true",
+                    help="measure only the widened rows and print them as one JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the elastic-ViT forward is not sharded across GPUs "
@@ -177,6 +270,10 @@ def main():
     from paper_2609_10018_amd import cost, ffi, inputs
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.next_only:
+        print(json.dumps({"next_rows": next_rows(torch, ffi, inputs, torch.cuda.current_stream(),
+                                                 not args.no_cpu)}), flush=True)
+        return
     cfg = inputs.CONFIGS["vit_b"]
     B = cfg.batch
     w = inputs.make_weights(cfg)
@@ -314,6 +411,8 @@ def main():
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(cfg, table, inputs.stored_weights(cfg, w),
                                               inputs.stored_images(cfg, x))
+    if not args.no_next and args.modes == "all":
+        result["next_rows"] = next_rows(torch, ffi, inputs, stream, not args.no_cpu)
     if args.work_out:
         classes = {}
         for kc in ffi.KERNELS:
