@@ -322,8 +322,10 @@ typedef enum {
 
 /* C[m][n] = epi(sum_{k<K} A[m*lda + k] * W[n*ldw + k] + bias[n]), m < M,
  * n < N.  Only the first K columns of A / W rows and the first N rows of W
- * are read.  GELU is exact erf GELU (fp32 path: the device erff; bf16 path:
- * erf to 1.5e-7 absolute).  BF16 path: lda and ldw multiples of 8, ldc a
+ * are read.  GELU is the erf GELU of Eq. 5 (fp32 path: the device erff;
+ * bf16 path: a polynomial form within 1e-4 absolute of it for |z| <= 12 and
+ * 1e-4 relative where |GELU(z)| > 0.1, below the bf16 rounding of its
+ * result).  BF16 path: lda and ldw multiples of 8, ldc a
  * multiple of 8 (bf16 out) or 4 (fp32 out), A, W, C, bias 16-byte aligned;
  * with ELASTO_EPI_BIAS_RESID a non-NULL C_cls holds the class-token rows
  * (m % tokens == 0) of C in fp32, [M / tokens][N], and those rows of C are
@@ -332,6 +334,39 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
                                  const void* W, int64_t ldw, void* C, int64_t ldc, float* C_cls,
                                  int32_t tokens, const float* bias, int64_t M, int32_t N,
                                  int32_t K, void* hip_stream);
+
+/* The bf16 linear with a LayerNorm folded in, as the forward runs its
+ * pre-norm blocks (Section 4.1): the GEMM that writes the residual stream
+ * also emits per-row statistics, and the next q/k/v or fc1 GEMM applies the
+ * LayerNorm of its input through them instead of a separate pass.
+ *
+ * Statistics: row m, 64-column segment j (n_j = min(64, width - 64 j)
+ * columns) at stats[2 * (m*stats_ld + j)]: the sum of the row's values in the
+ * segment, then the sum of their squared deviations from the segment's mean
+ * (fp32).  stats_ld is even and >= ceil(width / 64).
+ *
+ * stats_out != NULL (producer; epilogue ELASTO_EPI_BIAS_RESID): C and C_cls
+ * as in elasto_op_linear, and the statistics of every output row over its N
+ * columns (width = N, N % 8 == 0), of the values before their rounding to
+ * bf16 (class-token rows: of their fp32 values, which are then also written
+ * to C, rounded to bf16).
+ *
+ * stats_in != NULL (consumer; epilogue ELASTO_EPI_BIAS or
+ * ELASTO_EPI_BIAS_GELU): with the mean mu_m and biased variance v_m of A's row
+ * m over its K columns (width = K), combined from its segments,
+ *   C[m][n] = epi(rstd_m * sum_k A[m][k] W[n][k] - rstd_m * mu_m * colsum[n]
+ *                 + bias[n]),  rstd_m = 1 / sqrt(v_m + eps),
+ * which equals epi(LayerNorm(A[m]) . w_n + b_n) when W holds gamma (.) w,
+ * colsum[n] = sum_k W[n][k] and bias[n] = b_n + beta . w_n.
+ *
+ * Exactly one of stats_out, stats_in is non-NULL; stats are 16-byte
+ * aligned; other requirements as for the bf16 elasto_op_linear. */
+elasto_status_t elasto_op_linear_ln(int32_t epilogue, const void* A, int64_t lda, const void* W,
+                                    int64_t ldw, void* C, int64_t ldc, float* C_cls,
+                                    int32_t tokens, const float* bias, int64_t M, int32_t N,
+                                    int32_t K, float* stats_out, const float* stats_in,
+                                    int64_t stats_ld, const float* colsum, float eps,
+                                    void* hip_stream);
 
 /* Multi-head attention (Eq. 3) over `heads` head slots of `batch` sequences
  * of `tokens` rows.  qkv row (b*tokens + t) holds, for slot s, q at columns
@@ -417,7 +452,8 @@ elasto_status_t elasto_growth_read(elasto_growth_t g, int32_t which, void* host_
  * stride and 1x1 expand, a 1x1 projection shortcut with the same stride on
  * each stage's first block, ReLU after the sum, global average pooling,
  * linear classifier), BF16 only: bf16 NHWC activations, MFMA convolutions
- * (as GEMMs over explicit patch matrices), fp32 biases and logits.  Batch
+ * (implicit GEMMs: each tile's input patches are loaded straight from the
+ * activation, no patch matrix is written), fp32 biases and logits.  Batch
  * norm at inference is a per-channel affine map: the caller folds it into
  * each convolution's weights and bias.
  *

@@ -6,8 +6,11 @@ every token counted in every layer.  Element-wise work (LayerNorm, GELU,
 softmax, adds) is not counted.  ``paper_macs`` is the convention that matches
 the base ViT-B figure of Table 1: linear-layer MACs only (no QK^T / PV).
 
-Bytes are the algorithmic HBM bytes of the memory-bound kernels: a LayerNorm
-reads one fp32 residual-stream row and writes one bf16 activation row.
+``layernorm_bytes_per_image`` is the algorithmic HBM traffic of a standalone
+LayerNorm over every token (read one residual-stream row, write one LayerNorm
+output row): the fp32 path runs one per block input; the bf16 path folds the
+per-block LayerNorms into the next GEMM and runs only the final one, on the
+class-token rows.
 """
 from __future__ import annotations
 
@@ -53,9 +56,10 @@ def paper_macs(cfg: ModelConfig, table, k: int) -> float:
     return (f["patch"] + f["qkv"] + f["proj"] + f["fc1"] + f["fc2"] + f["head"]) / 2.0
 
 
-def layernorm_bytes_per_image(cfg: ModelConfig, out_bytes: int = 2) -> float:
-    """One LayerNorm over all tokens: read T*d fp32 + write T*d activations."""
-    return cfg.tokens * cfg.dim * (4.0 + out_bytes)
+def layernorm_bytes_per_image(cfg: ModelConfig, in_bytes: int = 4, out_bytes: int = 4) -> float:
+    """One standalone LayerNorm over all tokens: read T*d inputs + write T*d
+    outputs (element sizes in bytes; fp32 path: 4 and 4)."""
+    return cfg.tokens * cfg.dim * float(in_bytes + out_bytes)
 
 
 def active_weight_elems(cfg: ModelConfig, table, k: int) -> int:
@@ -64,6 +68,19 @@ def active_weight_elems(cfg: ModelConfig, table, k: int) -> int:
     h, m = layer_widths(table, k)
     per_layer = 3 * hd * h * d + d * hd * h + m * d + d * m
     return int(d * cfg.patch_k + per_layer.sum() + C * d)
+
+
+def dense_model_bytes(cfg: ModelConfig, table, k: int, matrix_bytes: int = 2,
+                      vector_bytes: int = 4) -> int:
+    """Bytes of mode k as a dense model of its own (the DN's weights copied
+    out, as a bag of per-mode models would store it): matrices at
+    matrix_bytes per element, biases, norms, class token and positions at
+    vector_bytes."""
+    d, hd, C, T = embed_width(cfg, table, k), cfg.head_dim, cfg.num_classes, cfg.tokens
+    h, m = layer_widths(table, k)
+    vec = 2 * d + T * d + 2 * d + C                          # patch_b, cls, pos, norm, head_b
+    vec += int(np.sum(2 * d + 3 * hd * h + d + 2 * d + m + d))  # per layer: ln1, bqkv, bo, ln2, b1, b2
+    return int(active_weight_elems(cfg, table, k) * matrix_bytes + vec * vector_bytes)
 
 
 def cnn_layer_macs(cfg, table, k: int):

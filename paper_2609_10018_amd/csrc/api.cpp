@@ -63,6 +63,44 @@ hipError_t timed(elasto_handle_s* h, int kc, hipStream_t s, Fn&& fn) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Activation buffers of one forward.
+struct Acts {
+  void *x = nullptr, *u = nullptr, *o = nullptr, *qkv = nullptr, *g = nullptr, *ucls = nullptr;
+  float* xcls = nullptr;
+  float2* lnpart = nullptr;
+};
+
+// Carves the activation buffers of a forward of up to `batch` images out of
+// `base` (nullptr: sizes only) and returns the bytes they take.  x is the
+// residual stream and u, o, qkv, g, ucls hold activations, all in the path's
+// dtype; on the bf16 path the class-token rows of the residual stream are
+// kept in fp32 in xcls (they alone decide the logits) and lnpart holds the
+// per-segment LayerNorm statistics of every row of x (lnseg float2 a row).
+int64_t scratch_layout(const elasto_config_t& cfg, const Dims& d, int lnseg, int64_t batch,
+                       uint8_t* base, Acts* a) {
+  const int64_t eb = cfg.dtype == ELASTO_BF16 ? 2 : 4;
+  const int64_t rows = batch * d.T, D = cfg.dim;
+  auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
+  const int64_t sz_x = al(rows * D * eb), sz_qkv = al(rows * 3 * D * eb),
+                sz_g = al(rows * (int64_t)cfg.mlp_hidden * eb), sz_cls = al(batch * D * eb),
+                sz_xcls = al(batch * D * 4), sz_ln = lnseg > 0 ? al(rows * lnseg * 8) : 0;
+  if (base && a) {
+    uint8_t* p = base;
+    a->x = p; p += sz_x;
+    a->u = p; p += sz_x;
+    a->o = p; p += sz_x;
+    a->qkv = p; p += sz_qkv;
+    a->g = p; p += sz_g;
+    a->ucls = p; p += sz_cls;
+    a->xcls = reinterpret_cast<float*>(p); p += sz_xcls;
+    a->lnpart = lnseg > 0 ? reinterpret_cast<float2*>(p) : nullptr;
+  }
+  return 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls + sz_ln;
+}
+
+elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
+                             void* hip_stream, const Acts& act);
+
 }  // namespace
 
 // LayerNorm folding (bf16 path).  The q/k/v and fc1 GEMMs read the residual
@@ -136,20 +174,11 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   }
   pack(*cfg, *w, *table, h->lay, host.data());
 
-  const int64_t eb = cfg->dtype == ELASTO_BF16 ? 2 : 4;
-  const int64_t rows = (int64_t)cfg->max_batch * h->dims.T, D = cfg->dim;
+  const int64_t D = cfg->dim;
   auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
-  // x is the residual stream and u, o, qkv, g, ucls hold activations, all in
-  // the path's dtype; on the bf16 path the class-token rows of the residual
-  // stream are kept in fp32 in xcls (they alone decide the logits).
-  const int64_t sz_x = al(rows * D * eb), sz_qkv = al(rows * 3 * D * eb),
-                sz_g = al(rows * (int64_t)cfg->mlp_hidden * eb),
-                sz_cls = al((int64_t)cfg->max_batch * D * eb),
-                sz_xcls = al((int64_t)cfg->max_batch * D * 4);
   const bool bf = cfg->dtype == ELASTO_BF16;
   h->lnseg = bf ? (int)((D + 127) / 128 * 2) : 0;  // 64-column segments, rounded up to even
-  const int64_t sz_ln = bf ? al(rows * h->lnseg * 8) : 0;
-  h->sbytes = 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls + sz_ln;
+  h->sbytes = scratch_layout(*cfg, h->dims, h->lnseg, cfg->max_batch, nullptr, nullptr);
   h->wbytes = h->lay.total;
   if (bf) {
     h->width_idx.resize((size_t)table->num_modes);
@@ -189,15 +218,16 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
     (void)hipGetLastError();
     return fail(st, "create: %s", hipGetErrorString(e));
   }
-  uint8_t* p = h->ds;
-  h->x = p; p += sz_x;
-  h->u = p; p += sz_x;
-  h->o = p; p += sz_x;
-  h->qkv = p; p += sz_qkv;
-  h->g = p; p += sz_g;
-  h->ucls = p; p += sz_cls;
-  h->xcls = reinterpret_cast<float*>(p); p += sz_xcls;
-  h->lnpart = bf ? reinterpret_cast<float2*>(p) : nullptr;
+  Acts a;
+  scratch_layout(*cfg, h->dims, h->lnseg, cfg->max_batch, h->ds, &a);
+  h->x = a.x;
+  h->u = a.u;
+  h->o = a.o;
+  h->qkv = a.qkv;
+  h->g = a.g;
+  h->ucls = a.ucls;
+  h->xcls = a.xcls;
+  h->lnpart = a.lnpart;
   *out = h;
   clear_error();
   return ELASTO_OK;
@@ -335,6 +365,18 @@ elasto_status_t elasto_profile_modes(elasto_handle_t h, const void* images, int3
 elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t batch, float* logits,
                                void* hip_stream) {
   if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  Acts a;
+  a.x = h->x; a.u = h->u; a.o = h->o; a.qkv = h->qkv; a.g = h->g; a.ucls = h->ucls;
+  a.xcls = h->xcls; a.lnpart = h->lnpart;
+  return forward_impl(h, images, batch, logits, hip_stream, a);
+}
+
+}  // extern "C"
+
+namespace {
+
+elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
+                             void* hip_stream, const Acts& act) {
   if (!images || !logits) return fail(ELASTO_ERR_INVALID_ARG, "images / logits is NULL");
   if (batch < 1 || batch > h->cfg.max_batch)
     return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
@@ -356,11 +398,11 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   const int64_t rows = (int64_t)batch * d.T;
   auto gemm = bf ? launch_gemm_bf16 : launch_gemm_f32;
   auto attn = bf ? launch_attention_bf16 : launch_attention_f32;
-  float* xcls = bf ? h->xcls : nullptr;
+  float* xcls = bf ? act.xcls : nullptr;
   // LayerNorm over all rows of the residual stream.
   auto ln = [&](const float* g, const float* b) {
-    return bf ? launch_layernorm_bf16(h->x, D, xcls, d.T, h->u, rows, E, g, b, c.ln_eps, s)
-              : launch_layernorm_f32(h->x, D, h->u, rows, E, g, b, c.ln_eps, s);
+    return bf ? launch_layernorm_bf16(act.x, D, xcls, d.T, act.u, rows, E, g, b, c.ln_eps, s)
+              : launch_layernorm_f32(act.x, D, act.u, rows, E, g, b, c.ln_eps, s);
   };
   const float scale = 1.0f / sqrtf((float)d.hd);
   // bf16: LayerNorms folded into the q/k/v and fc1 GEMMs (see refold); the
@@ -374,7 +416,7 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     GemmArgs a;
     a.W = W(h, ELASTO_T_PATCH_W);
     a.ldw = d.patch_k;
-    a.C = h->x;
+    a.C = act.x;
     a.ldc = D;
     a.bias = F(h, ELASTO_T_PATCH_B);
     a.M = rows;
@@ -391,7 +433,7 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
     a.ldpos = D;
     a.ccls = xcls;
     if (fold) {
-      a.ln_out = h->lnpart;
+      a.ln_out = act.lnpart;
       a.ln_ld = h->lnseg;
     }
     e = timed(h, ELASTO_K_PATCH, s, [&] { return gemm(Epi::Patch, a, s); });
@@ -404,36 +446,36 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
       if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln1 layer %d: %s", l, hipGetErrorString(e));
     }
     GemmArgs q;
-    q.A = h->u; q.lda = E;
+    q.A = act.u; q.lda = E;
     q.W = W(h, ELASTO_T_WQKV, l); q.ldw = D;
-    q.C = h->qkv; q.ldc = 3 * D;
+    q.C = act.qkv; q.ldc = 3 * D;
     q.bias = F(h, ELASTO_T_BQKV, l);
     q.M = rows; q.N = 3 * d.hd * hh; q.K = E;
     if (fold) {
-      q.A = h->x; q.lda = D;
+      q.A = act.x; q.lda = D;
       q.W = fold_ptr(l, h->fold_wq);
       q.bias = reinterpret_cast<const float*>(fold_ptr(l, h->fold_cq)) + (int64_t)wi * 3 * D;
       q.ln_colsum = reinterpret_cast<const float*>(fold_ptr(l, h->fold_sq)) + (int64_t)wi * 3 * D;
-      q.ln_in = h->lnpart; q.ln_ld = h->lnseg; q.ln_eps = c.ln_eps;
+      q.ln_in = act.lnpart; q.ln_ld = h->lnseg; q.ln_eps = c.ln_eps;
     }
     e = timed(h, ELASTO_K_QKV, s, [&] { return gemm(Epi::Bias, q, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "qkv layer %d: %s", l, hipGetErrorString(e));
     AttnArgs at;
-    at.qkv = h->qkv; at.qkv_stride = 3 * D;
-    at.o = h->o; at.o_stride = D;
+    at.qkv = act.qkv; at.qkv_stride = 3 * D;
+    at.o = act.o; at.o_stride = D;
     at.batch = batch; at.tokens = d.T; at.heads = hh; at.head_dim = d.hd; at.scale = scale;
     e = timed(h, ELASTO_K_ATTN, s, [&] { return attn(at, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "attention layer %d: %s", l, hipGetErrorString(e));
     GemmArgs pr;
-    pr.A = h->o; pr.lda = D;
+    pr.A = act.o; pr.lda = D;
     pr.W = W(h, ELASTO_T_WO, l); pr.ldw = D;
-    pr.C = h->x; pr.ldc = D;
+    pr.C = act.x; pr.ldc = D;
     pr.bias = F(h, ELASTO_T_BO, l);
     pr.ccls = xcls;
     pr.tokens = d.T;
     pr.M = rows; pr.N = E; pr.K = d.hd * hh;
     if (fold) {
-      pr.ln_out = h->lnpart; pr.ln_ld = h->lnseg;
+      pr.ln_out = act.lnpart; pr.ln_ld = h->lnseg;
     }
     e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
@@ -442,44 +484,44 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
       if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "ln2 layer %d: %s", l, hipGetErrorString(e));
     }
     GemmArgs f1;
-    f1.A = h->u; f1.lda = E;
+    f1.A = act.u; f1.lda = E;
     f1.W = W(h, ELASTO_T_W1, l); f1.ldw = D;
-    f1.C = h->g; f1.ldc = Mh;
+    f1.C = act.g; f1.ldc = Mh;
     f1.bias = F(h, ELASTO_T_B1, l);
     f1.M = rows; f1.N = mm; f1.K = E;
     if (fold) {
-      f1.A = h->x; f1.lda = D;
+      f1.A = act.x; f1.lda = D;
       f1.W = fold_ptr(l, h->fold_w1);
       f1.bias = reinterpret_cast<const float*>(fold_ptr(l, h->fold_c1)) + (int64_t)wi * Mh;
       f1.ln_colsum = reinterpret_cast<const float*>(fold_ptr(l, h->fold_s1)) + (int64_t)wi * Mh;
-      f1.ln_in = h->lnpart; f1.ln_ld = h->lnseg; f1.ln_eps = c.ln_eps;
+      f1.ln_in = act.lnpart; f1.ln_ld = h->lnseg; f1.ln_eps = c.ln_eps;
     }
     e = timed(h, ELASTO_K_FC1, s, [&] { return gemm(Epi::BiasGelu, f1, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f2;
-    f2.A = h->g; f2.lda = Mh;
+    f2.A = act.g; f2.lda = Mh;
     f2.W = W(h, ELASTO_T_W2, l); f2.ldw = Mh;
-    f2.C = h->x; f2.ldc = D;
+    f2.C = act.x; f2.ldc = D;
     f2.bias = F(h, ELASTO_T_B2, l);
     f2.ccls = xcls;
     f2.tokens = d.T;
     f2.M = rows; f2.N = E; f2.K = mm;
     if (fold) {
-      f2.ln_out = h->lnpart; f2.ln_ld = h->lnseg;
+      f2.ln_out = act.lnpart; f2.ln_ld = h->lnseg;
     }
     e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
   }
   // Final norm on the class-token rows only.
   e = timed(h, ELASTO_K_LN, s, [&] {
-    return bf ? launch_layernorm_bf16(xcls, E, xcls, 1, h->ucls, batch, E, F(h, ELASTO_T_NORM_G),
+    return bf ? launch_layernorm_bf16(xcls, E, xcls, 1, act.ucls, batch, E, F(h, ELASTO_T_NORM_G),
                                       F(h, ELASTO_T_NORM_B), c.ln_eps, s)
-              : launch_layernorm_f32(h->x, (int64_t)d.T * D, h->ucls, batch, E,
+              : launch_layernorm_f32(act.x, (int64_t)d.T * D, act.ucls, batch, E,
                                      F(h, ELASTO_T_NORM_G), F(h, ELASTO_T_NORM_B), c.ln_eps, s);
   });
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "final norm: %s", hipGetErrorString(e));
   GemmArgs hg;
-  hg.A = h->ucls; hg.lda = E;
+  hg.A = act.ucls; hg.lda = E;
   hg.W = W(h, ELASTO_T_HEAD_W); hg.ldw = D;
   hg.C = logits; hg.ldc = c.num_classes;
   hg.bias = F(h, ELASTO_T_HEAD_B);
@@ -488,6 +530,10 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "head: %s", hipGetErrorString(e));
   return ELASTO_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 elasto_status_t elasto_kernel_timing(elasto_handle_t h, int32_t kc, int32_t max_launches) {
   if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
@@ -652,6 +698,55 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
     return fail(ELASTO_ERR_INVALID_ARG, "bad dtype %d", dtype);
   }
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "linear: %s", hipGetErrorString(e));
+  return ELASTO_OK;
+}
+
+elasto_status_t elasto_op_linear_ln(int32_t epilogue, const void* A, int64_t lda, const void* Wt,
+                                    int64_t ldw, void* C, int64_t ldc, float* C_cls,
+                                    int32_t tokens, const float* bias, int64_t M, int32_t N,
+                                    int32_t K, float* stats_out, const float* stats_in,
+                                    int64_t stats_ld, const float* colsum, float eps,
+                                    void* hip_stream) {
+  if (!A || !Wt || !C || !bias) return fail(ELASTO_ERR_INVALID_ARG, "NULL pointer");
+  if ((stats_out != nullptr) == (stats_in != nullptr))
+    return fail(ELASTO_ERR_INVALID_ARG, "exactly one of stats_out, stats_in must be given");
+  if (M < 0 || M >= ((int64_t)1 << 31) || N < 1 || K < 1 || lda < K || ldw < K || ldc < N)
+    return fail(ELASTO_ERR_INVALID_ARG, "bad linear sizes");
+  if (lda % 8 || ldw % 8 || ldc % 8 || !aligned(A, 16) || !aligned(Wt, 16) || !aligned(C, 16) ||
+      !aligned(bias, 16))
+    return fail(ELASTO_ERR_INVALID_ARG,
+                "linear needs lda, ldw, ldc %% 8 == 0 and 16-byte aligned A, W, C, bias");
+  const float* st = stats_out ? stats_out : stats_in;
+  const int64_t width = stats_out ? N : K;
+  if (!aligned(st, 16) || stats_ld % 2 || stats_ld < (width + 63) / 64)
+    return fail(ELASTO_ERR_INVALID_ARG, "stats need 16-byte alignment and an even stats_ld >= ceil(width / 64)");
+  GemmArgs a;
+  a.A = A; a.lda = lda; a.W = Wt; a.ldw = ldw; a.C = C; a.ldc = ldc; a.bias = bias;
+  a.M = M; a.N = N; a.K = K;
+  a.ln_ld = stats_ld;
+  Epi epi;
+  if (stats_out) {
+    if (epilogue != ELASTO_EPI_BIAS_RESID || N % 8)
+      return fail(ELASTO_ERR_INVALID_ARG, "the producer needs the residual epilogue and N %% 8 == 0");
+    if (C_cls && (tokens < 1 || !aligned(C_cls, 16)))
+      return fail(ELASTO_ERR_INVALID_ARG, "C_cls needs tokens >= 1 and 16-byte alignment");
+    a.ccls = C_cls;
+    a.tokens = tokens;
+    a.ln_out = reinterpret_cast<float2*>(stats_out);
+    epi = Epi::BiasResid;
+  } else {
+    if (epilogue != ELASTO_EPI_BIAS && epilogue != ELASTO_EPI_BIAS_GELU)
+      return fail(ELASTO_ERR_INVALID_ARG, "the consumer needs the bias or bias+GELU epilogue");
+    if (C_cls) return fail(ELASTO_ERR_INVALID_ARG, "C_cls is for the producer");
+    if (!colsum || !aligned(colsum, 16) || !(eps > 0.0f))
+      return fail(ELASTO_ERR_INVALID_ARG, "the consumer needs 16-byte aligned colsum and eps > 0");
+    a.ln_in = reinterpret_cast<const float2*>(stats_in);
+    a.ln_colsum = colsum;
+    a.ln_eps = eps;
+    epi = static_cast<Epi>(epilogue);
+  }
+  const hipError_t e = launch_gemm_bf16(epi, a, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "linear_ln: %s", hipGetErrorString(e));
   return ELASTO_OK;
 }
 

@@ -37,6 +37,7 @@
 // receives a contiguous run of tiles, ordered in groups of row panels so that
 // the tiles an XCD runs at the same time share A and W panels in its L2.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -100,51 +101,92 @@ struct Params {
 
 // Lane exchanges within a DPP row: quad_perm (1,0,3,2) and (2,3,0,1) swap
 // neighbours 1 and 2 apart; row_half_mirror maps lane i of each 8-lane half
-// to 7 - i.  The three together sum over aligned groups of 8 lanes.
+// to 7 - i.  The three together reach every lane of an aligned group of 8.
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
-__device__ __forceinline__ float sum8_lanes(float v) {
-  v += dpp_f<kDppXor1>(v);
-  v += dpp_f<kDppXor2>(v);
-  return v + dpp_f<kDppHalfMirror>(v);
+
+// LayerNorm statistics.  The GEMM that writes a row of the residual stream
+// stores, for each of the row's 64-column segments j (n_j = min(64, K - 64 j)
+// columns), the pair (S_j, M2_j): the sum of the segment's values and the sum
+// of their squared deviations from the segment's mean.  Pairs are merged with
+// the pairwise update of Chan, Golub and LeVeque: for counts n_a, n_b, means
+// m_a, m_b and deviation sums M2_a, M2_b, with d = m_b - m_a and n = n_a + n_b,
+//   mean = m_a + d n_b / n,   M2 = M2_a + M2_b + d^2 n_a n_b / n,
+// which never subtracts two large sums, so rows whose mean is large against
+// their spread keep an accurate variance.
+struct LnStat {
+  float n, mean, m2;
+};
+
+__device__ __forceinline__ void ln_merge(LnStat& a, float nb, float mb, float m2b) {
+  const float n = a.n + nb;
+  const float f = n > 0.0f ? nb * __builtin_amdgcn_rcpf(n) : 0.0f;
+  const float d = mb - a.mean;
+  a.mean = fmaf(d, f, a.mean);
+  a.m2 += fmaf(d * d, a.n * f, m2b);
+  a.n = n;
 }
 
-// LayerNorm factors of a row from the (sum, sum of squares) of its 64-column
-// segments, stored row-major: segment j of row r at part[r * ld + j], ld even
-// so that segments 2i and 2i+1 form one 16-byte load.
-// ln_sums adds, over the 16-byte pairs i = first, first + step, ... < ceil(nseg / 2),
-// the row's sums into S and Q, four loads in flight at a time; ln_factors
-// turns the totals into (rstd, -rstd * mean): mean = S / K, biased variance
-// Q / K - mean^2 (fp32: relative error about 2^-24 (1 + mean^2 / variance)).
-__device__ __forceinline__ void ln_sums(const float2* row, int K, int first, int step, float& S,
-                                        float& Q) {
+// Merge into `a` the statistics held by the lane selected by DPP control CTRL.
+template <int CTRL>
+__device__ __forceinline__ void ln_merge_dpp(LnStat& a) {
+  const float nb = dpp_f<CTRL>(a.n), mb = dpp_f<CTRL>(a.mean), m2b = dpp_f<CTRL>(a.m2);
+  ln_merge(a, nb, mb, m2b);
+}
+
+// Statistics of 8 values (all of them valid, or none).
+__device__ __forceinline__ LnStat ln_of8(const float* v, bool valid) {
+  LnStat s{0.0f, 0.0f, 0.0f};
+  if (valid) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t += v[e];
+    const float m = t * 0.125f;
+    float q = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q = fmaf(v[e] - m, v[e] - m, q);
+    s = LnStat{8.0f, m, q};
+  }
+  return s;
+}
+
+// Merges, in segment order, the segments of a row (stored row-major: segment j
+// of row r at part[r * ld + j], ld even so that segments 2i and 2i+1 form one
+// 16-byte load) whose pair index is i = first, first + step, ... <
+// ceil(nseg / 2), four loads in flight at a time.  Branch-free: a pair past
+// the last re-reads pair 0, and a segment past the last (n_j <= 0) merges as
+// an empty one.
+__device__ __forceinline__ void ln_sums(const float2* row, int K, int first, int step, LnStat& st) {
   const int nseg = (K + 63) >> 6, npair = (nseg + 1) >> 1;
   for (int i0 = first; i0 < npair; i0 += 4 * step) {
     f32x4 q[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int i = i0 + t * step;
-      q[t] = i < npair ? *reinterpret_cast<const f32x4*>(row + 2 * i) : f32x4{0.f, 0.f, 0.f, 0.f};
-      if (2 * i + 1 >= nseg) {  // odd segment count: the pair's second half is not a segment
-        q[t][2] = 0.0f;
-        q[t][3] = 0.0f;
-      }
+      q[t] = *reinterpret_cast<const f32x4*>(row + 2 * (i < npair ? i : 0));
     }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      S += q[t][0] + q[t][2];
-      Q += q[t][1] + q[t][3];
+      const int i = i0 + t * step;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int nj = i < npair ? min(64, K - 64 * (2 * i + h)) : 0;
+        const float nb = (float)max(nj, 0);
+        ln_merge(st, nb, q[t][2 * h] * __builtin_amdgcn_rcpf(fmaxf(nb, 1.0f)),
+                 nj > 0 ? q[t][2 * h + 1] : 0.0f);
+      }
     }
   }
 }
 
-__device__ __forceinline__ float2 ln_factors(float S, float Q, int K, float eps) {
-  const float inv = 1.0f / (float)K, mean = S * inv;
-  const float rstd = 1.0f / sqrtf(fmaxf(fmaf(Q, inv, -mean * mean), 0.0f) + eps);
-  return make_float2(rstd, -rstd * mean);
+// (rstd, -rstd * mean) of a row from its merged statistics (biased variance).
+__device__ __forceinline__ float2 ln_factors(const LnStat& st, float eps) {
+  const float var = fmaxf(st.m2 * __builtin_amdgcn_rcpf(st.n), 0.0f);
+  const float rstd = 1.0f / sqrtf(var + eps);
+  return make_float2(rstd, -rstd * st.mean);
 }
 
 // Buffer descriptor word 3 for raw (unswizzled, stride 0) buffers on CDNA.
@@ -483,9 +525,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) cs[e] = col + e < p.N ? p.ln_colsum[col + e] : 0.0f;
       if (tid < BM) {
-        float S = 0.0f, Q = 0.0f;
-        ln_sums(p.ln_in + (int64_t)min(m0 + tid, p.M - 1) * p.ln_ld, p.K, 0, 1, S, Q);
-        rowst[tid] = ln_factors(S, Q, p.K, p.ln_eps);
+        LnStat st{0.0f, 0.0f, 0.0f};
+        ln_sums(p.ln_in + (int64_t)min(m0 + tid, p.M - 1) * p.ln_ld, p.K, 0, 1, st);
+        rowst[tid] = ln_factors(st, p.ln_eps);
       }
     }
   }
@@ -657,25 +699,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       } while (0);
       if constexpr (LN_PRODUCER) {
         if (p.ln_out != nullptr) {
-          // Sum and sum of squares over each 64-column segment: the 8 lanes of
-          // an aligned group hold its 8 chunks (N % 8 == 0).
-          float sum = 0.0f, sq = 0.0f;
-          if (st_ok) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              sum += st[e];
-              sq = fmaf(st[e], st[e], sq);
-            }
-          }
-          sum += dpp_f<kDppXor1>(sum);
-          sq += dpp_f<kDppXor1>(sq);
-          sum += dpp_f<kDppXor2>(sum);
-          sq += dpp_f<kDppXor2>(sq);
-          sum += dpp_f<kDppHalfMirror>(sum);
-          sq += dpp_f<kDppHalfMirror>(sq);
+          // Statistics of each 64-column segment: the 8 lanes of an aligned
+          // group hold its 8 chunks (N % 8 == 0, so a chunk is whole or
+          // absent); three DPP merges give every lane the group's total.
+          LnStat ls = ln_of8(st, st_ok);
+          ln_merge_dpp<kDppXor1>(ls);
+          ln_merge_dpp<kDppXor2>(ls);
+          ln_merge_dpp<kDppHalfMirror>(ls);
           const int seg = (n0 >> 6) + (cc >> 3);
           if ((cc & 7) == 0 && 64 * seg < p.N)
-            p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(sum, sq);
+            p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(ls.n * ls.mean, ls.m2);
         }
       }
     }
@@ -792,70 +825,144 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-#pragma clang loop unroll(disable)
-    for (int kt = 0; kt < nk; ++kt) {
-      // After an epilogue the wave's last 16 memory operations are its
-      // stores; everything issued before them (this step's loads) is done.
-      if (kt == 0 && stores_out) wait_vm_lds<16>();
-      else wait_vm_lds<0>();
-      __builtin_amdgcn_s_barrier();
-      // Next step of this tile, or the first step of the next tile, into the
-      // other stage (every wave finished reading it before the barrier).
-      // Folded LayerNorm: at the first step, two threads a row sum the row's
-      // segment statistics; the loads go out before this step's tile loads so
-      // that waiting for them does not wait for those.
-      float lS = 0.0f, lQ = 0.0f;
-      if constexpr (LNF) {
-        if (kt == 0)
-          ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, lS, lQ);
+    if constexpr (E != Epi::BiasResid) {
+      // Fragments of two K quarters in flight: a quarter's MFMAs run while the
+      // LDS reads of the next quarter are issued between them, so a wave never
+      // waits on reads issued just before.  A step's last quarter is
+      // multiplied after the next step's barrier (the stage it came from may
+      // be overwritten only after that barrier, and its fragments are already
+      // in registers), behind that step's first reads.  Every step issues its
+      // eight tile loads (the last step of the last tile re-reads its own first
+      // step into the idle stage), so each quarter is one straight-line block.
+      bf16x8 fa[2][TM], fb[2][TN];
+  #define ELASTO_PERS_STEP(FIRST)                                                              \
+      {                                                                                        \
+        if ((FIRST) && stores_out) wait_vm_lds<16>();                                          \
+        else wait_vm_lds<0>();                                                                 \
+        __builtin_amdgcn_s_barrier();                                                          \
+        __builtin_amdgcn_sched_barrier(0);                                                     \
+        LnStat lst{0.0f, 0.0f, 0.0f};                                                          \
+        if (LNF && (FIRST))                                                                    \
+          ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, \
+                  lst);                                                                        \
+        const bool more = kt + 1 < nk;                                                         \
+        const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0; \
+        const int so = buf * STAGE;                                                            \
+        int xl = pcx, pr = prow, ab[TM], bb[TN];                                               \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i) ab[i] = abase[i];                       \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j) bb[j] = bbase[j];                       \
+        asm volatile("" : "+v"(xl), "+v"(pr));                                                 \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(ab[i]));         \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(bb[j]));         \
+        _Pragma("unroll") for (int kk = 0; kk < kBK / 16; ++kk) {                              \
+          const int rs = kk & 1, ms = rs ^ 1, kx = kk << 5;                                    \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i)                                       \
+            fa[rs][i] = *reinterpret_cast<const bf16x8*>(smem + ((ab[i] + so) ^ kx));          \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j)                                       \
+            fb[rs][j] = *reinterpret_cast<const bf16x8*>(smem + ((bb[j] + so) ^ kx));          \
+          if (kk < 3) {                                                                        \
+            _Pragma("unroll") for (int t = (8 * kk + 2) / 3; t < (8 * (kk + 1) + 2) / 3; ++t)  \
+              load1(buf ^ 1, nr0, nkt, t, xl, pr);                                             \
+          }                                                                                    \
+          if (!((FIRST) && kk == 0)) {                                                         \
+            _Pragma("unroll") for (int i = 0; i < TM; ++i)                                     \
+            _Pragma("unroll") for (int j = 0; j < TN; ++j)                                     \
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ms][j], fa[ms][i],        \
+                                                                  acc[i][j], 0, 0, 0);         \
+            _Pragma("unroll") for (int t = 0; t < 6; ++t) {                                    \
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                               \
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                               \
+            }                                                                                  \
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                                 \
+          }                                                                                    \
+          __builtin_amdgcn_sched_barrier(0);                                                   \
+        }                                                                                      \
+        if (LNF && (FIRST)) {                                                                  \
+          ln_merge_dpp<kDppXor1>(lst);                                                         \
+          if ((tid & 1) == 0) rowst[par * BM + (tid >> 1)] = ln_factors(lst, p.ln_eps);        \
+        }                                                                                      \
+        buf ^= 1;                                                                              \
       }
-      const bool more = kt + 1 < nk, go = more || has_next;
-      const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0;
-      const int so = buf * STAGE;
-      // Opaque copies: keeps the per-quarter addresses from being hoisted out
-      // of the loop into registers.
-      int xl = pcx, pr = prow, ab[TM], bb[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) ab[i] = abase[i];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bb[j] = bbase[j];
-      asm volatile("" : "+v"(xl), "+v"(pr));
-#pragma unroll
-      for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(ab[i]));
-#pragma unroll
-      for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(bb[j]));
-#pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        if (go && kk < 3) {
-#pragma unroll
-          for (int t = (8 * kk + 2) / 3; t < (8 * (kk + 1) + 2) / 3; ++t)
-            load1(buf ^ 1, nr0, nkt, t, xl, pr);
-        }
-        const int kx = kk << 5;
-        bf16x8 af[TM], bf[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[i] = *reinterpret_cast<const bf16x8*>(smem + ((ab[i] + so) ^ kx));
-#pragma unroll
+      {
+        const int kt = 0;
+        ELASTO_PERS_STEP(true)
+      }
+  #pragma clang loop unroll(disable)
+      for (int kt = 1; kt < nk; ++kt) ELASTO_PERS_STEP(false)
+  #undef ELASTO_PERS_STEP
+      // The tile's last quarter.
+  #pragma unroll
+      for (int i = 0; i < TM; ++i)
+  #pragma unroll
         for (int j = 0; j < TN; ++j)
-          bf[j] = *reinterpret_cast<const bf16x8*>(smem + ((bb[j] + so) ^ kx));
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
-      }
-      if constexpr (LNF) {
-        // Published by a later barrier: the next step's, or the one below.
-        // rowst is double-buffered: a wave in the next tile has passed this
-        // tile's barriers, which every wave reaches after its epilogue.
-        if (kt == 0) {
-          lS += dpp_f<kDppXor1>(lS);
-          lQ += dpp_f<kDppXor1>(lQ);
-          if ((tid & 1) == 0) rowst[par * BM + (tid >> 1)] = ln_factors(lS, lQ, p.K, p.ln_eps);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[1][j], fa[1][i], acc[i][j], 0, 0, 0);
+    } else {
+      // The residual epilogue needs more registers than the fragment
+      // pipeline leaves: one quarter of fragments at a time.
+  #pragma clang loop unroll(disable)
+      for (int kt = 0; kt < nk; ++kt) {
+        // After an epilogue the wave's last 16 memory operations are its
+        // stores; everything issued before them (this step's loads) is done.
+        if (kt == 0 && stores_out) wait_vm_lds<16>();
+        else wait_vm_lds<0>();
+        __builtin_amdgcn_s_barrier();
+        // Next step of this tile, or the first step of the next tile, into the
+        // other stage (every wave finished reading it before the barrier).
+        // Folded LayerNorm: at the first step, two threads a row sum the row's
+        // segment statistics; the loads go out before this step's tile loads so
+        // that waiting for them does not wait for those.
+        LnStat lst{0.0f, 0.0f, 0.0f};
+        if constexpr (LNF) {
+          if (kt == 0)
+            ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, lst);
         }
+        const bool more = kt + 1 < nk, go = more || has_next;
+        const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0;
+        const int so = buf * STAGE;
+        // Opaque copies: keeps the per-quarter addresses from being hoisted out
+        // of the loop into registers.
+        int xl = pcx, pr = prow, ab[TM], bb[TN];
+  #pragma unroll
+        for (int i = 0; i < TM; ++i) ab[i] = abase[i];
+  #pragma unroll
+        for (int j = 0; j < TN; ++j) bb[j] = bbase[j];
+        asm volatile("" : "+v"(xl), "+v"(pr));
+  #pragma unroll
+        for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(ab[i]));
+  #pragma unroll
+        for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(bb[j]));
+  #pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+          if (go && kk < 3) {
+  #pragma unroll
+            for (int t = (8 * kk + 2) / 3; t < (8 * (kk + 1) + 2) / 3; ++t)
+              load1(buf ^ 1, nr0, nkt, t, xl, pr);
+          }
+          const int kx = kk << 5;
+          bf16x8 af[TM], bf[TN];
+  #pragma unroll
+          for (int i = 0; i < TM; ++i)
+            af[i] = *reinterpret_cast<const bf16x8*>(smem + ((ab[i] + so) ^ kx));
+  #pragma unroll
+          for (int j = 0; j < TN; ++j)
+            bf[j] = *reinterpret_cast<const bf16x8*>(smem + ((bb[j] + so) ^ kx));
+  #pragma unroll
+          for (int i = 0; i < TM; ++i)
+  #pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
+        }
+        if constexpr (LNF) {
+          // Published by a later barrier: the next step's, or the one below.
+          // rowst is double-buffered: a wave in the next tile has passed this
+          // tile's barriers, which every wave reaches after its epilogue.
+          if (kt == 0) {
+            ln_merge_dpp<kDppXor1>(lst);
+            if ((tid & 1) == 0) rowst[par * BM + (tid >> 1)] = ln_factors(lst, p.ln_eps);
+          }
+        }
+        buf ^= 1;
       }
-      buf ^= 1;
     }
     if constexpr (LNF) {
       if (nk == 1) {  // no later step barrier in this tile
@@ -870,18 +977,20 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     const int nrec = rows_valid * (int)p.ldc * 2;
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<uint16_t*>(p.C) + (int64_t)m0 * p.ldc, (short)0, nrec, kRsrcWord3);
-    // Bias of this lane's 32 columns (clamped into [0, N): the columns past N
-    // are computed from re-read rows and never stored).
-    f32x4 bv[TN][4], cs[TN][4];
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = min(n0 + wn * WTN + j * 32 + 8 * g + 4 * lg, p.N - 4);
-        bv[j][g] = *reinterpret_cast<const f32x4*>(p.bias + c);
-        if constexpr (LNF) cs[j][g] = *reinterpret_cast<const f32x4*>(p.ln_colsum + c);
-      }
+    // Bias (and, folded LayerNorm, column sums) of this lane's columns in
+    // 32-column block j, group g: columns n0 + wn*64 + j*32 + 8g + 4lg + 0..3,
+    // clamped into [0, N) (the columns past N are computed from re-read rows
+    // and never stored).
+    auto col_vec = [&](const float* v, int j, int g) {
+      const int c = min(n0 + wn * WTN + j * 32 + 8 * g + 4 * lg, p.N - 4);
+      return *reinterpret_cast<const f32x4*>(v + c);
+    };
     if constexpr (E == Epi::BiasResid) {
+      f32x4 bv[TN][4];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) bv[j][g] = col_vec(p.bias, j, g);
       // C = residual + acc + bias: fp32 staging of acc + bias, 16 columns per
       // pass (i, j, h); lane l then holds row r = l/2 of the 32-row block,
       // columns 8 (l%2) .. +7 of the pass.  The residual comes from res (or C
@@ -938,7 +1047,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         if (i + 1 < TM) load_res(i + 1, rz[(i + 1) & 1]);
         const int row = row_l0 + i * 32;
         const bool row_ok = row < p.M, cls = i == cls_i;
-        float ssum = 0.0f, ssq = 0.0f;
+        LnStat ls{0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -980,20 +1089,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
             const bool st = ok && (!cls || p.ln_out != nullptr);
             __builtin_amdgcn_raw_buffer_store_b128(
                 w, rc, st ? ((row - m0) * (int)p.ldc + col) * 2 : nrec, 0, 0);
-            if (ok) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                ssum += v[e];
-                ssq = fmaf(v[e], v[e], ssq);
-              }
-            }
+            const LnStat l8 = ln_of8(v, ok);
+            ln_merge(ls, l8.n, l8.mean, l8.m2);
             wait_lds();  // the slot is rewritten by the next pass
           }
         if (p.ln_out != nullptr) {  // this row's 64-column segment: lanes l and l ^ 1
-          ssum += dpp_f<kDppXor1>(ssum);
-          ssq += dpp_f<kDppXor1>(ssq);
+          ln_merge_dpp<kDppXor1>(ls);
           if ((lane & 1) == 0 && row_ok && 64 * seg < p.N)
-            p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(ssum, ssq);
+            p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(ls.n * ls.mean, ls.m2);
         }
       }
     } else {
@@ -1005,21 +1108,29 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       }
       const int lane_st = ((wm * WTM + (lane >> 2)) * (int)p.ldc + n0 + wn * WTN + (lane & 3) * 8) * 2;
       const int wofs = lr * ES + lg * 8, rofs = (lane >> 2) * ES + (lane & 3) * 16;
+      // Column blocks outermost, so only one block's bias and column sums
+      // are held at a time.
   #pragma unroll
-      for (int i = 0; i < TM; ++i) {
+      for (int j = 0; j < TN; ++j) {
+        f32x4 bv[4], cs[4];
+  #pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          bv[g] = col_vec(p.bias, j, g);
+          if constexpr (LNF) cs[g] = col_vec(p.ln_colsum, j, g);
+        }
+  #pragma unroll
+        for (int i = 0; i < TM; ++i) {
         int lst = lane_st, wo = wofs, ro = rofs;
         asm volatile("" : "+v"(lst), "+v"(wo), "+v"(ro));
-  #pragma unroll
-        for (int j = 0; j < TN; ++j) {
   #pragma unroll
           for (int g = 0; g < 4; ++g) {
             float t[4];
   #pragma unroll
             for (int e = 0; e < 4; ++e) {
               if constexpr (LNF)
-                t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[j][g][e], bv[j][g][e]));
+                t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[g][e], bv[g][e]));
               else
-                t[e] = acc[i][j][4 * g + e] + bv[j][g][e];
+                t[e] = acc[i][j][4 * g + e] + bv[g][e];
               if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
             }
             u32x2 w;
@@ -1050,6 +1161,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     stores_out = true;
     par ^= 1;
   }
+  // The last step issued loads into the idle stage: let them land before the
+  // wave ends.
+  wait_vm_lds<0>();
 }
 
 template <int BM, int BN, int WM, int WN, Epi E, bool CONV, int STAGES = 2>

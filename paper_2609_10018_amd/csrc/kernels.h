@@ -52,14 +52,16 @@ struct GemmArgs {
   int64_t c_split = 0;
   // LayerNorm folded into the GEMMs (bf16 path).
   // Producer (BiasResid, Patch): ln_out != nullptr also writes, for every
-  // output row r and every 64-column segment j of [0, N), the sum and the sum
-  // of squares of the row's values there (before their rounding to bf16) to
+  // output row r and every 64-column segment j of [0, N), the pair (sum of
+  // the row's values there, sum of their squared deviations from the
+  // segment's mean), of the values before their rounding to bf16, to
   // ln_out[r * ln_ld + j] (ln_ld even, >= ceil(N / 64); class-token rows:
   // of their fp32 values, which are then also stored rounded to bf16 in C).
   // Needs N % 8 == 0.
   // Consumer (Bias, BiasGelu): ln_in != nullptr treats A as the LayerNorm
   // input: with mean mu_r and rstd r_r of A's row r over its K columns
-  // (from the ceil(K / 64) segments of ln_in, same layout) the result is
+  // (the ceil(K / 64) segments of ln_in, same layout, merged pairwise; the
+  // last segment has K - 64 * (ceil(K / 64) - 1) columns) the result is
   // epi(r_r * (A W^T)[r][n] - r_r * mu_r * ln_colsum[n] + bias[n]), i.e.
   // LN(A) W^T + bias when W holds gamma (x) the weights, ln_colsum[n] the sum
   // of W's row n over its K columns and bias the original bias plus

@@ -22,7 +22,7 @@ c_i32, c_i64, c_f32, c_f64, c_vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_flo
                                      ctypes.c_double, ctypes.c_void_p)
 
 STATUS = {0: "OK", 1: "INVALID_ARG", 2: "BAD_CONFIG", 3: "BAD_TABLE", 4: "OUT_OF_MEMORY",
-          5: "HIP", 6: "MODE_RANGE", 7: "BATCH_RANGE"}
+          5: "HIP", 6: "MODE_RANGE", 7: "BATCH_RANGE", 8: "INFEASIBLE"}
 
 # Tensor ids (elasto_tensor_t).
 T_PATCH_W, T_PATCH_B, T_CLS, T_POS, T_NORM_G, T_NORM_B, T_HEAD_W, T_HEAD_B = range(8)
@@ -112,6 +112,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                 c_f32, c_vp],
         "elasto_op_linear": [c_i32, c_i32, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i32,
                              c_vp, c_i64, c_i32, c_i32, c_vp],
+        "elasto_op_linear_ln": [c_i32, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i32, c_vp,
+                                c_i64, c_i32, c_i32, c_vp, c_vp, c_i64, c_vp, c_f32, c_vp],
         "elasto_op_attention": [c_i32, c_vp, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32,
                                 c_f32, c_vp],
         "elasto_op_conv2d": [c_vp, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
@@ -311,6 +313,16 @@ def op_linear(dtype: int, epilogue: int, A, lda: int, W, ldw: int, C, ldc: int, 
                                           M, N, K, _stream_ptr(stream)))
 
 
+def op_linear_ln(epilogue: int, A, lda: int, W, ldw: int, C, ldc: int, bias, M: int, N: int,
+                 K: int, stats_ld: int, stats_out=None, stats_in=None, colsum=None,
+                 eps: float = 1e-6, C_cls=None, tokens: int = 1, stream=None) -> None:
+    check(load_library().elasto_op_linear_ln(epilogue, A.data_ptr(), lda, W.data_ptr(), ldw,
+                                             C.data_ptr(), ldc, _ptr(C_cls), tokens,
+                                             bias.data_ptr(), M, N, K, _ptr(stats_out),
+                                             _ptr(stats_in), stats_ld, _ptr(colsum), eps,
+                                             _stream_ptr(stream)))
+
+
 def op_attention(dtype: int, qkv, qkv_stride: int, o, o_stride: int, batch: int, tokens: int,
                  heads: int, head_dim: int, scale: float, stream=None) -> None:
     check(load_library().elasto_op_attention(dtype, qkv.data_ptr(), qkv_stride, o.data_ptr(),
@@ -463,5 +475,5 @@ def select_mode(flops, latency_ms, memory_bytes, accuracy=None, power_w=None,
 
 
 __all__ = ["ElasticViT", "ElasticResNet", "cnn_validate", "select_mode", "ElastoError", "load_library", "validate", "packed_bytes",
-           "packed_layout", "pack_weights", "op_layernorm", "op_linear", "op_attention",
+           "packed_layout", "pack_weights", "op_layernorm", "op_linear", "op_linear_ln", "op_attention",
            "KERNELS", "FP32", "BF16"]

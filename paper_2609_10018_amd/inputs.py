@@ -15,13 +15,16 @@ elastic forward pass computes.  It holds:
 * round-to-nearest-even fp32 -> bf16 rounding of host arrays, so the oracle
   can be fed exactly the values the bf16 path stores.
 
-In the paper the order comes from L1-norm saliency of trained weights
-(Section 4.1).  With random-init weights that order is arbitrary, so a seeded
-permutation stands in for it: it exercises the same permuted-prefix storage.
+The channel order is the paper's saliency order (Section 4.1, Eq. 4): rows
+ranked by their average absolute weight, most salient first, applied to the
+seeded weights.  Building a DN table is the design-time pruning step, not a
+step of the forward: the table is input data to the HIP path and to the
+oracle alike, and neither of them ranks anything.
 """
 from __future__ import annotations
 
 import dataclasses
+import functools
 from typing import Dict, List, Optional
 
 import numpy as np
@@ -33,7 +36,6 @@ WEIGHT_SEED = 0
 IMAGE_SEED = 1
 RATIO_SEED = 2
 SEQUENCE_SEED = 3
-ORDER_SEED = 4
 INIT_STD = 0.02
 
 
@@ -186,7 +188,39 @@ class DNTable:
         return int(self.n_heads.shape[1])
 
 
-def make_dn_table(cfg: ModelConfig, seed: int = ORDER_SEED) -> DNTable:
+def saliency_order(rows: np.ndarray) -> np.ndarray:
+    """Indices of the rows of `rows` ([n, ...]) by descending mean |value|
+    (Eq. 4's L1 row saliency); equal scores keep the lower index first."""
+    score = np.abs(np.asarray(rows, dtype=np.float64)).reshape(rows.shape[0], -1).mean(axis=1)
+    return np.argsort(-score, kind="stable").astype(np.int32)
+
+
+def _orders(cfg: ModelConfig, w: Dict[str, np.ndarray]):
+    d, hd, L = cfg.dim, cfg.head_dim, cfg.depth
+    # qkv_w rows t*d + i*hd + c (t = q, k, v) belong to head i.
+    head_order = np.stack([
+        saliency_order(w["qkv_w"][l].reshape(3, cfg.heads, hd, d).transpose(1, 0, 2, 3))
+        for l in range(L)])
+    mlp_order = np.stack([saliency_order(w["fc1_w"][l]) for l in range(L)])
+    return head_order, mlp_order, saliency_order(w["patch_w"])
+
+
+@functools.lru_cache(maxsize=None)
+def _seeded_orders(cfg: ModelConfig):
+    out = _orders(cfg, make_weights(cfg))
+    for a in out:
+        a.setflags(write=False)
+    return out
+
+
+def make_dn_table(cfg: ModelConfig, weights: Optional[Dict[str, np.ndarray]] = None) -> DNTable:
+    """DN table of a config: per-mode widths from MODE_CAPS (per-layer ratios
+    for LAYER_RATIO_CONFIGS) and per-layer channel orders by saliency of
+    `weights` (default: the config's seeded weights):
+    * heads: the mean |w| over the head's q, k and v rows of qkv_w;
+    * MLP units: the mean |w| of the unit's fc1_w row;
+    * embedding channels (one order for every layer): the mean |w| of the
+      channel's patch-embedding row."""
     caps = MODE_CAPS[cfg.name]
     L = cfg.depth
     n_heads = np.zeros((len(caps), L), dtype=np.int32)
@@ -200,10 +234,8 @@ def make_dn_table(cfg: ModelConfig, seed: int = ORDER_SEED) -> DNTable:
             else:
                 n_heads[k, l] = max(1, int(np.floor(hk * ratios[l] + 0.5)))
                 n_mlp[k, l] = max(1, int(np.floor(mk * ratios[l] + 0.5)))
-    rng = np.random.default_rng(seed)
-    head_order = np.stack([rng.permutation(cfg.heads) for _ in range(L)]).astype(np.int32)
-    mlp_order = np.stack([rng.permutation(cfg.mlp_hidden) for _ in range(L)]).astype(np.int32)
-    embed_order = rng.permutation(cfg.dim).astype(np.int32)
+    head_order, mlp_order, embed_order = (_orders(cfg, weights) if weights is not None
+                                          else _seeded_orders(cfg))
     n_embed = np.array([cap[2] if len(cap) > 2 else cfg.dim for cap in caps], dtype=np.int32)
     return DNTable(n_heads, n_mlp, head_order, mlp_order, n_embed, embed_order)
 

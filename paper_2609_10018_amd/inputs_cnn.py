@@ -13,7 +13,8 @@ computes nothing that the forward pass computes.  It holds:
   is scaled down (the usual small initial residual branch);
 * DN tables: each bottleneck's two inner widths (outputs of its 1x1 reduce and
   of its 3x3 convolution) are elastic, as prefixes of one filter order per
-  convolution (structured filter masks, Eq. 7; nested, Eq. 8).  The mode keep
+  convolution (structured filter masks, Eq. 7; nested, Eq. 8), the filters
+  ranked by saliency (mean absolute weight, most salient first).  The mode keep
   ratios are chosen so that the per-image MACs of ResNet-50's modes match the
   six DN levels the paper reports for it (Table 2).
 """
@@ -24,10 +25,9 @@ from typing import Dict, List, Optional, Tuple
 
 import numpy as np
 
-from .inputs import BF16, FP32, bf16_round  # noqa: F401  (shared dtype ids)
+from .inputs import BF16, FP32, bf16_round, saliency_order  # noqa: F401  (shared dtype ids)
 
 CNN_WEIGHT_SEED = 10
-CNN_ORDER_SEED = 14
 RESIDUAL_BRANCH_GAIN = 0.2
 
 
@@ -136,7 +136,10 @@ class CNNTable:
         return int(self.n_width.shape[0])
 
 
-def make_cnn_table(cfg: ResNetConfig, seed: int = CNN_ORDER_SEED) -> CNNTable:
+def make_cnn_table(cfg: ResNetConfig, weights: Optional[Dict[str, np.ndarray]] = None) -> CNNTable:
+    """Per-mode inner widths from CNN_MODE_RATIOS; each inner convolution's
+    filters ordered by descending mean |w| of the filter (Eq. 7's filter
+    saliency) of `weights` (default: the config's seeded weights)."""
     specs = cfg.block_specs()
     ratios = CNN_MODE_RATIOS[cfg.name]
     n = np.zeros((len(ratios), len(specs)), dtype=np.int32)
@@ -144,9 +147,9 @@ def make_cnn_table(cfg: ResNetConfig, seed: int = CNN_ORDER_SEED) -> CNNTable:
         for i, b in enumerate(specs):
             keep = int(np.floor(b["width"] * r / 8.0 + 0.5)) * 8
             n[k, i] = min(b["width"], max(8, keep))
-    rng = np.random.default_rng(seed)
-    order1 = [rng.permutation(b["width"]).astype(np.int32) for b in specs]
-    order2 = [rng.permutation(b["width"]).astype(np.int32) for b in specs]
+    w = weights if weights is not None else make_cnn_weights(cfg)
+    order1 = [saliency_order(w[f"b{i}_c1_w"]) for i in range(len(specs))]
+    order2 = [saliency_order(w[f"b{i}_c2_w"]) for i in range(len(specs))]
     return CNNTable(n, order1, order2)
 
 
@@ -158,8 +161,22 @@ def stored_cnn_weights(cfg: ResNetConfig, w: Dict[str, np.ndarray]) -> Dict[str,
     return {k: (bf16_round(v) if k.endswith("_w") else v) for k, v in w.items()}
 
 
+CNN_IMAGE_STATS_SEED = 5
+
+
 def make_cnn_images(cfg: ResNetConfig, batch: int, seed: int = 1) -> np.ndarray:
-    """N(0, 1) pixels, fp32, NCHW."""
+    """fp32 NCHW images with per-image statistics: pixel (b, c, y, x) =
+    offset[b, c] + contrast[b] * noise, noise N(0, 1) from `seed`, offsets
+    N(0, 1) from CNN_IMAGE_STATS_SEED and contrasts U[0.25, 2] from the seed
+    after it.  Like
+    normalised natural images, images differ in channel means and contrast;
+    white noise alone reaches the pooled features of a random network almost
+    only through its batch-common part."""
     rng = np.random.default_rng(seed)
-    return rng.standard_normal((batch, cfg.in_chans, cfg.img, cfg.img),
-                               dtype=np.float64).astype(np.float32)
+    noise = rng.standard_normal((batch, cfg.in_chans, cfg.img, cfg.img), dtype=np.float64)
+    # One generator per statistic, so that the first b images of a batch do
+    # not depend on the batch size.
+    offset = np.random.default_rng(CNN_IMAGE_STATS_SEED).standard_normal(
+        (batch, cfg.in_chans, 1, 1))
+    contrast = np.random.default_rng(CNN_IMAGE_STATS_SEED + 1).uniform(0.25, 2.0, (batch, 1, 1, 1))
+    return (offset + contrast * noise).astype(np.float32)

@@ -72,6 +72,8 @@ def classify(names):
             c = "ln"
         elif "MulFunctor" in n:
             c = "copy"
+        elif "reduce_kernel" in n:
+            c = "read"
         else:
             c = "other"
         out.append(c)
@@ -168,6 +170,12 @@ def summarize(out, cmds):
 
     rd, rd_scale, rd_copy = calibrated(fetch_n, fetch_c, "FETCH_SIZE")
     wr, wr_scale, wr_copy = calibrated(write_n, write_c, "WRITE_SIZE")
+    # Second calibration of the fetch counter: a read-only probe (a sum over
+    # the same 1 GiB), whose fetch is all it moves.
+    fc_ = classify(fetch_n)
+    reads = [sum(fetch_c[i]["FETCH_SIZE"] * 1024.0 for i in idx)
+             for c_, idx in launches(fc_) if c_ == "read"]
+    rd_read_scale = COPY_PROBE_BYTES / (sum(reads) / len(reads)) if reads else None
     mc = classify(mfma_n)
     busy = per_launch(mc, [v["SQ_VALU_MFMA_BUSY_CYCLES"] for v in mfma_c])
     # GRBM_GUI_ACTIVE comes summed over the 8 XCDs; each XCD counts the same cycles.
@@ -206,7 +214,8 @@ def summarize(out, cmds):
         "algorithmic_bytes_per_launch": table[dom]["algo_bytes"],
         "calibration": {"copy_bytes": COPY_PROBE_BYTES, "fetch_scale": rd_scale,
                         "write_scale": wr_scale, "fetch_copy_bytes_raw": rd_copy,
-                        "write_copy_bytes_raw": wr_copy},
+                        "write_copy_bytes_raw": wr_copy,
+                        "fetch_scale_read_probe": rd_read_scale},
         "classes": table,
         "commands": {k: _portable(v) for k, v in cmds.items()},
     }
@@ -231,7 +240,10 @@ def summarize(out, cmds):
         f"SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x {simds} SIMDs). Fetch / write = "
         f"FETCH_SIZE / WRITE_SIZE scaled by the copy probe (1 GiB read + 1 GiB written; "
         f"raw counters read {rd_copy / 2**30:.3f} GiB and {wr_copy / 2**30:.3f} GiB, "
-        f"scales {rd_scale:.3f} and {wr_scale:.3f}). Ratio = (fetch + write) / algorithmic bytes.",
+        f"scales {rd_scale:.3f} and {wr_scale:.3f}; a read-only probe, a sum over the same "
+        f"1 GiB, gives a fetch scale of "
+        + (f"{rd_read_scale:.3f}" if rd_read_scale else "n/a") +
+        "). Ratio = (fetch + write) / algorithmic bytes.",
         "",
         "| class | launches | avg µs | achieved (algorithmic FLOP) | algorithmic bytes / time "
         "| MFMA util | algorithmic MB | fetch MB | write MB | ratio |",

@@ -104,3 +104,75 @@ def test_bf16_round_is_rne():
     r = inputs.bf16_round(y)
     assert (r.view(np.uint32) & 0xFFFF == 0).all()
     assert np.max(np.abs(r - y) / np.abs(y)) <= 2 ** -8
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_emb", "vit_ti"])
+def test_channel_orders_follow_l1_saliency(name):
+    """Eq. 4's saliency, written out with loops: a head's score is the mean
+    |w| over its q, k and v rows, a unit's the mean |w| of its fc1 row, an
+    embedding channel's the mean |w| of its patch-embedding row; the order
+    lists them by descending score (equal scores: lower index first)."""
+    cfg = CONFIGS[name]
+    w = inputs.make_weights(cfg)
+    t = inputs.make_dn_table(cfg)
+    d, hd = cfg.dim, cfg.head_dim
+
+    def mean_abs(rows):
+        tot, n = 0.0, 0
+        for r in rows:
+            for v in np.asarray(r, dtype=np.float64).reshape(-1):
+                tot += abs(float(v))
+                n += 1
+        return tot / n
+
+    def check(order, scores):
+        assert sorted(order.tolist()) == list(range(len(scores)))
+        for a, b in zip(order[:-1], order[1:]):
+            assert scores[a] > scores[b] or (scores[a] == scores[b] and a < b)
+
+    for l in range(cfg.depth):
+        hs = [mean_abs([w["qkv_w"][l][q * d + i * hd + c] for q in range(3) for c in range(hd)])
+              for i in range(cfg.heads)]
+        check(t.head_order[l], hs)
+        us = [mean_abs([w["fc1_w"][l][j]]) for j in range(cfg.mlp_hidden)]
+        check(t.mlp_order[l], us)
+    es = [mean_abs([w["patch_w"][c]]) for c in range(d)]
+    check(t.embed_order, es)
+
+
+def test_saliency_order_ties_and_explicit_weights():
+    rows = np.array([[1.0, -1.0], [2.0, 0.0], [0.5, 0.5], [-3.0, 1.0], [0.0, 2.0]])
+    # scores 1, 1, 0.5, 2, 1: descending, equal scores by index
+    assert inputs.saliency_order(rows).tolist() == [3, 0, 1, 4, 2]
+    # Reversing layer 0's units (fc1 rows) reverses the index of every score,
+    # so the order maps j -> m - 1 - j; other layers keep theirs.
+    cfg = CONFIGS["tiny"]
+    w = inputs.make_weights(cfg)
+    w2 = {k: np.array(v, copy=True) for k, v in w.items()}
+    w2["fc1_w"][0] = w2["fc1_w"][0][::-1].copy()
+    t, t2 = inputs.make_dn_table(cfg), inputs.make_dn_table(cfg, w2)
+    m = cfg.mlp_hidden
+    assert np.unique(np.abs(w["fc1_w"][0]).mean(axis=1)).size == m
+    np.testing.assert_array_equal(t2.mlp_order[0], m - 1 - t.mlp_order[0])
+    np.testing.assert_array_equal(t2.mlp_order[1:], t.mlp_order[1:])
+    np.testing.assert_array_equal(t2.head_order, t.head_order)
+
+
+@pytest.mark.parametrize("name", ["tiny", "vit_ti", "vit_ti_emb"])
+def test_dense_model_bytes_count_the_extracted_model(name):
+    """cost.dense_model_bytes equals the sizes of the oracle's extracted
+    dense model (F3), matrices at 2 bytes and everything else at 4."""
+    cfg = CONFIGS[name]
+    w = inputs.make_weights(cfg)
+    t = inputs.make_dn_table(cfg)
+    mats = set(inputs.MATRIX_KEYS)
+    for k in range(t.num_modes):
+        p = oracle.extract_dense(w, cfg, t, k)
+        total = 0
+        for key, v in p.items():
+            if key == "layers":
+                for lp in v:
+                    total += sum(a.size * (2 if kk in mats else 4) for kk, a in lp.items())
+            elif isinstance(v, np.ndarray):
+                total += v.size * (2 if key in mats else 4)
+        assert cost.dense_model_bytes(cfg, t, k) == total, (name, k)

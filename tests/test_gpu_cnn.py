@@ -14,16 +14,23 @@ from paper_2609_10018_amd.inputs_cnn import (CNN_CONFIGS, make_cnn_images, make_
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
-from gpu_util import rel_err, top1_agreement  # noqa: E402
+from gpu_util import check_top1, rel_err  # noqa: E402
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 BF16_TOL = 2e-2
 # The image-dependent part of the logits (logits minus their batch mean) is
-# only 4-20% of their magnitude on these random networks (white-noise images
-# through random filters): bf16 rounding of the common part (2^-9 relative)
-# is then up to ~5% of it.  It is still checked on its own scale, at 0.1,
-# which a mix-up of images or channels would exceed many times over.
-CENTERED_TOL = 1e-1
+# checked on its own scale too, at the same bar: the images differ in
+# channel means and contrast (inputs_cnn.make_cnn_images), which makes that
+# part 0.39-0.44 of the logits' magnitude in every mode of both configs (with
+# white-noise images it was 0.04-0.2); `share` is printed and asserted to be
+# at least MIN_SHARE so that the centred check keeps its meaning.
+CENTERED_TOL = 2e-2
+MIN_SHARE = 0.35
+
+
+def share(ref):
+    r = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(r - r.mean(axis=0))) / np.max(np.abs(r)))
 
 
 def centered_err(got, ref):
@@ -75,8 +82,10 @@ def test_resnet_small_all_modes_match_oracle():
         got = n.run(k)
         ref = orn.elastic_forward(w, n.cfg, n.table, k, x)
         err, cerr = rel_err(got, ref), centered_err(got, ref)
-        print(f"resnet_small mode {k}: rel err {err:.3e}, centered {cerr:.3e}")
+        print(f"resnet_small mode {k}: rel err {err:.3e}, centered {cerr:.3e} "
+              f"(image-dependent share {share(ref):.3f})")
         assert np.isfinite(got).all()
+        assert share(ref) >= MIN_SHARE
         assert err <= BF16_TOL and cerr <= CENTERED_TOL
 
 
@@ -87,11 +96,12 @@ def test_resnet50_all_modes_match_golden():
     for k in range(n.table.num_modes):
         got = n.run(k)[:m]
         err, cerr = rel_err(got, gold[k]), centered_err(got, gold[k])
-        raw, tie = top1_agreement(got, gold[k])
-        print(f"resnet50 mode {k}: rel err {err:.3e}, centered {cerr:.3e}, top-1 {raw:.3f}/{tie:.3f}")
+        print(f"resnet50 mode {k}: rel err {err:.3e}, centered {cerr:.3e} "
+              f"(image-dependent share {share(gold[k]):.3f})")
         assert np.isfinite(got).all()
+        assert share(gold[k]) >= MIN_SHARE
         assert err <= BF16_TOL and cerr <= CENTERED_TOL
-        assert tie >= 0.995
+        check_top1(f"resnet50 mode {k}", got, gold[k])
 
 
 @pytest.mark.parametrize("batch", [1, 3])
