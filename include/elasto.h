@@ -157,6 +157,24 @@ elasto_status_t elasto_get_mode(elasto_handle_t h, int32_t* k);
 elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t batch,
                                float* logits, void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * forward as elasto_forward, with its activation scratch taken from one
+ * statically allocated array per GPU instead of the handle's buffers.  The
+ * array holds 64 MiB (ELASTO_STATIC_SCRATCH_BYTES), enough for ViT-B/16 at
+ * up to 20 images a call; each GPU the library runs on keeps its copy
+ * until the process ends.  Allocates nothing (the array's device address is
+ * looked up once per device, on the first call there); the caller still
+ * passes images and logits as for elasto_forward.
+ * Every call on one GPU shares that GPU's array, and a call reads only what
+ * it wrote there itself; calls that overlap on one GPU (several streams or
+ * several handles at once) race on it and must be serialised by the caller.
+ * BATCH_RANGE when batch is outside [1, max_batch] or the batch's
+ * activations exceed the array (the message gives both sizes). */
+#define ELASTO_STATIC_SCRATCH_BYTES (64LL << 20)
+elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int32_t batch,
+                                      float* logits, void* hip_stream);
+
 /* Thread-local message of the calling thread's last failing call ("" if none).
  * Returns a string, not a status. */
 const char* elasto_last_error(void);

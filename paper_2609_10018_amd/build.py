@@ -20,7 +20,7 @@ LIB_DIR = os.path.join(HERE, "_lib")
 LIB_PATH = os.path.join(LIB_DIR, "libelasto.so")
 
 SOURCES = ["gemm_bf16.hip", "gemm_f32.hip", "attention.hip", "attention_bwd.hip", "layernorm.hip",
-           "conv.hip", "growth_kernels.hip", "growth.cpp",
+           "conv.hip", "growth_kernels.hip", "static_scratch.hip", "growth.cpp",
            "api.cpp", "layout.cpp", "select.cpp", "cnn.cpp"]
 ARCH = "gfx950"
 

@@ -371,6 +371,29 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   return forward_impl(h, images, batch, logits, hip_stream, a);
 }
 
+elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int32_t batch,
+                                      float* logits, void* hip_stream) {
+  if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
+  if (batch < 1 || batch > h->cfg.max_batch)
+    return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
+  const int64_t need = scratch_layout(h->cfg, h->dims, h->lnseg, batch, nullptr, nullptr);
+  if (need > kStaticScratchBytes)
+    return fail(ELASTO_ERR_BATCH_RANGE,
+                "batch %d needs %lld bytes of activation scratch; the static scratch holds %lld",
+                batch, (long long)need, (long long)kStaticScratchBytes);
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device) {
+    if (hipSetDevice(h->device) != hipSuccess) return fail(ELASTO_ERR_HIP, "cannot select device %d", h->device);
+  }
+  void* base = nullptr;
+  int64_t have = 0;
+  const hipError_t e = static_scratch(&base, &have);
+  if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "static scratch: %s", hipGetErrorString(e));
+  Acts a;
+  scratch_layout(h->cfg, h->dims, h->lnseg, batch, static_cast<uint8_t*>(base), &a);
+  return forward_impl(h, images, batch, logits, hip_stream, a);
+}
+
 }  // extern "C"
 
 namespace {

@@ -194,4 +194,10 @@ hipError_t launch_max_pool_3x3_s2(const void* x, int batch, int H, int W, int C,
                                   hipStream_t s);
 hipError_t launch_avg_pool(const void* x, int batch, int HW, int C, void* y, hipStream_t s);
 
+// Statically allocated activation scratch (static_scratch.hip): its size, and
+// the device address of the current device's copy (looked up on the first
+// call per device; later calls return the cached address).
+constexpr int64_t kStaticScratchBytes = (int64_t)64 << 20;
+hipError_t static_scratch(void** ptr, int64_t* bytes);
+
 }  // namespace elasto

@@ -99,6 +99,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "elasto_set_mode": [c_vp, c_i32],
         "elasto_get_mode": [c_vp, P(c_i32)],
         "elasto_forward": [c_vp, c_vp, c_i32, c_vp, c_vp],
+        "elasto_forward_static": [c_vp, c_vp, c_i32, c_vp, c_vp],
         "elasto_mode_info": [c_vp, c_i32, P(c_f64), P(c_i64)],
         "elasto_memory_info": [c_vp, P(c_i64), P(c_i64)],
         "elasto_validate": [P(Config), P(Table)],
@@ -257,6 +258,14 @@ class ElasticViT:
             raise ValueError("images and logits must be contiguous")
         check(self.lib.elasto_forward(self.h, images.data_ptr(), int(images.shape[0]),
                                       logits.data_ptr(), _stream_ptr(stream)))
+
+    def forward_static(self, images, logits, stream=None) -> None:
+        """The forward with its activations in the library's static scratch
+        (elasto_forward_static: allocates nothing)."""
+        if not images.is_contiguous() or not logits.is_contiguous():
+            raise ValueError("images and logits must be contiguous")
+        check(self.lib.elasto_forward_static(self.h, images.data_ptr(), int(images.shape[0]),
+                                             logits.data_ptr(), _stream_ptr(stream)))
 
     def mode_info(self, k: int):
         f, b = c_f64(), c_i64()
