@@ -38,10 +38,12 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_vit_b_b256.json")
 
 
 def kernel_source_hash() -> str:
+    """Hash of the device code: every .hip source (kernels and their launch
+    planning) and the kernel headers; host-only sources are left out."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_10018_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h", ".cpp")):
+        if f.endswith(".hip") or f in ("kernels.h", "common.h"):
             h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -290,6 +292,9 @@ def main():
                     help="write the algorithmic work per kernel class (mode 0) to this JSON file")
     ap.add_argument("--no-next", action="store_true",
                     help="skip the widened rows (ResNet-50 forward, growth step)")
+    ap.add_argument("--profile-mode", type=int, default=None,
+                    help="profiling run: only warmup + --steps forwards of this DN mode, the "
+                         "--work-out file for it and the --copy-probe dispatches; no JSON line")
     ap.add_argument("--next-only", action="store_true",
                     help="measure only the widened rows and print them as one JSON line")
     args = ap.parse_args()
@@ -316,6 +321,10 @@ def main():
     xd = torch.from_numpy(x).to(torch.bfloat16).cuda().contiguous()
     logits = torch.empty((B, cfg.num_classes), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
+    if args.profile_mode is not None:
+        profile_run(torch, args, vit, cfg, table, xd, logits, stream)
+        vit.close()
+        return
 
     modes = list(range(table.num_modes)) if args.modes == "all" else \
         sorted({0} | {int(v) for v in args.modes.split(",")})
@@ -463,17 +472,55 @@ def main():
                   open(args.work_out, "w"), indent=1)
     vit.close()
     if args.copy_probe:
-        n = (1 << 30) // 4
-        src = torch.empty(n, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            torch.mul(src, 1.0, out=dst)
-        for _ in range(3):
-            torch.sum(src)
-        torch.cuda.synchronize()
-        del src, dst
-        log("copy probe done")
+        copy_probe(torch)
     print(json.dumps(result), flush=True)
+
+
+def copy_probe(torch):
+    """Three plain copies of 1 GiB (out = in * 1, fp32) and three sums over the
+    same 1 GiB (reads only): the calibration dispatches of the byte counters."""
+    n = (1 << 30) // 4
+    src = torch.empty(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    for _ in range(3):
+        torch.sum(src)
+    torch.cuda.synchronize()
+    del src, dst
+    log("copy probe done")
+
+
+def profile_run(torch, args, vit, cfg, table, xd, logits, stream):
+    """Forwards of one DN mode only, for a profiler: every library dispatch of
+    the run belongs to that mode."""
+    from paper_2609_10018_amd import ffi
+    k, B = args.profile_mode, cfg.batch
+    vit.set_mode(k)
+    for _ in range(max(1, args.warmup)):
+        vit.forward(xd, logits, stream)
+    class_ms = {}
+    for kc in ffi.KERNELS:
+        vit.kernel_timing(kc, 64)
+        vit.forward(xd, logits, stream)
+        class_ms[kc] = vit.kernel_timing_read()[0]
+    dominant = max(class_ms, key=class_ms.get)
+    vit.kernel_timing(dominant, args.steps * 64)
+    per, total_ms, _ = time_steps(torch, vit, k, xd, logits, args.steps, stream)
+    dom_ms, dom_n = vit.kernel_timing_read()
+    vit.kernel_timing(None, 0)
+    log(f"profile mode {k}: {total_ms / args.steps:.3f} ms per forward (events on {dominant})")
+    if args.work_out:
+        classes = {}
+        for kc in ffi.KERNELS:
+            f, b, n = vit.kernel_work(k, B, kc)
+            classes[kc] = {"flops_per_launch": f / n, "bytes_per_launch": b / n,
+                           "launches_per_forward": n}
+        json.dump({"mode": k, "classes": classes, "dominant": dominant,
+                   "dominant_avg_us": dom_ms / dom_n * 1e3, "class_ms": class_ms,
+                   "source_hash": kernel_source_hash()}, open(args.work_out, "w"), indent=1)
+    if args.copy_probe:
+        copy_probe(torch)
 
 
 if __name__ == "__main__":

@@ -146,7 +146,8 @@ extern "C" {
 
 elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t* w,
                               const elasto_dn_table_t* table, elasto_handle_t* out) {
-  if (!out) return fail(ELASTO_ERR_INVALID_ARG, "out is NULL");
+  if (!out || !cfg || !table)
+    return fail(ELASTO_ERR_INVALID_ARG, "%s is NULL", !out ? "out" : !cfg ? "config" : "DN table");
   if (!check_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
   if (!check_table(cfg, table)) return ELASTO_ERR_BAD_TABLE;
   if (!check_weights(w)) return ELASTO_ERR_INVALID_ARG;
@@ -675,7 +676,7 @@ elasto_status_t elasto_op_layernorm(int32_t dtype, const void* x, int64_t x_stri
   if (dtype == ELASTO_BF16) {
     if (d % 8 != 0 || x_stride % 8 != 0 || !aligned(x, 16) || !aligned(out, 16) ||
         !aligned(g, 16) || !aligned(b, 16))
-      return fail(ELASTO_ERR_INVALID_ARG, "bf16 layernorm needs d, stride % 8 == 0 and 16-byte aligned pointers");
+      return fail(ELASTO_ERR_INVALID_ARG, "bf16 layernorm needs d, stride %% 8 == 0 and 16-byte aligned pointers");
     e = launch_layernorm_bf16(x, x_stride, x_cls, tokens, out, rows, d, g, b, eps,
                               static_cast<hipStream_t>(hip_stream));
   } else if (dtype == ELASTO_FP32) {
@@ -695,7 +696,7 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
   if (C_cls && (epilogue != ELASTO_EPI_BIAS_RESID || dtype != ELASTO_BF16 || tokens < 1 ||
                 !aligned(C_cls, 16) || N % 4 != 0))
     return fail(ELASTO_ERR_INVALID_ARG,
-                "C_cls needs the bf16 residual epilogue, tokens >= 1, N % 4 == 0, 16-byte alignment");
+                "C_cls needs the bf16 residual epilogue, tokens >= 1, N %% 4 == 0, 16-byte alignment");
   if (M < 0 || M >= ((int64_t)1 << 31) || N < 1 || K < 1 || lda < K || ldw < K || ldc < N)
     return fail(ELASTO_ERR_INVALID_ARG, "bad linear sizes");
   if (epilogue < ELASTO_EPI_BIAS || epilogue > ELASTO_EPI_BIAS_F32OUT)
@@ -712,7 +713,7 @@ elasto_status_t elasto_op_linear(int32_t dtype, int32_t epilogue, const void* A,
     if (lda % 8 || ldw % 8 || ldc % cvec || !aligned(A, 16) || !aligned(Wt, 16) || !aligned(C, 16) ||
         !aligned(bias, 16))
       return fail(ELASTO_ERR_INVALID_ARG,
-                  "bf16 linear needs lda, ldw % 8 == 0, ldc a multiple of 16 bytes and 16-byte "
+                  "bf16 linear needs lda, ldw %% 8 == 0, ldc a multiple of 16 bytes and 16-byte "
                   "aligned A, W, C, bias");
     e = launch_gemm_bf16(epi, a, static_cast<hipStream_t>(hip_stream));
   } else if (dtype == ELASTO_FP32) {

@@ -135,6 +135,7 @@ struct elasto_cnn_s {
 extern "C" {
 
 elasto_status_t elasto_cnn_validate(const elasto_cnn_config_t* cfg, const elasto_cnn_table_t* t) {
+  if (!cfg || !t) return fail(ELASTO_ERR_INVALID_ARG, "%s is NULL", cfg ? "DN table" : "config");
   if (!check_cnn_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
   if (!check_cnn_table(cfg, t)) return ELASTO_ERR_BAD_TABLE;
   clear_error();
@@ -143,7 +144,8 @@ elasto_status_t elasto_cnn_validate(const elasto_cnn_config_t* cfg, const elasto
 
 elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_cnn_weights_t* w,
                                   const elasto_cnn_table_t* table, elasto_cnn_t* out) {
-  if (!out) return fail(ELASTO_ERR_INVALID_ARG, "out is NULL");
+  if (!out || !cfg || !table)
+    return fail(ELASTO_ERR_INVALID_ARG, "%s is NULL", !out ? "out" : !cfg ? "config" : "DN table");
   if (!check_cnn_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
   if (!check_cnn_table(cfg, table)) return ELASTO_ERR_BAD_TABLE;
   const std::vector<BlockSpec> bs = block_specs(*cfg);

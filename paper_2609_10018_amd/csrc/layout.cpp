@@ -319,6 +319,7 @@ extern "C" {
 const char* elasto_last_error(void) { return g_err.c_str(); }
 
 elasto_status_t elasto_validate(const elasto_config_t* cfg, const elasto_dn_table_t* table) {
+  if (!cfg || !table) return fail(ELASTO_ERR_INVALID_ARG, "%s is NULL", cfg ? "DN table" : "config");
   if (!check_config(cfg)) return ELASTO_ERR_BAD_CONFIG;
   if (!check_table(cfg, table)) return ELASTO_ERR_BAD_TABLE;
   clear_error();

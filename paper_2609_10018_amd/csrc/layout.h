@@ -42,9 +42,9 @@ bool check_weights(const elasto_weights_t* w);
 
 uint16_t f32_to_bf16_rne(float f);
 
-void set_error(const char* fmt, ...);
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();
-elasto_status_t fail(elasto_status_t st, const char* fmt, ...);
+elasto_status_t fail(elasto_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 // Per-image FLOPs of a mode (2 x MACs of every contraction) with per-layer
 // head / unit counts and embed active embedding channels.

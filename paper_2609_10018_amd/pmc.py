@@ -1,7 +1,7 @@
 """rocprofv3 runs and summaries for the elastic-ViT forward (ViT-B/16, bf16,
-batch 256, DN mode 0).
+batch 256, one DN mode, mode 0 by default).
 
-    python -m paper_2609_10018_amd.pmc --out gpurun_out/pmc
+    python -m paper_2609_10018_amd.pmc --out gpurun_out/pmc [--mode K]
 
 runs four profiled passes of ``bench.py`` (each a child process under its own
 time limit) and writes ``summary.md`` and ``traffic.json`` into ``--out``:
@@ -39,10 +39,12 @@ COPY_PROBE_BYTES = 1 << 30          # bench.py --copy-probe: reads and writes th
 EPI_CLASS = {"0": "qkv", "1": "fc1", "3": "head", "4": "patch"}  # Epi 2 (residual): proj or fc2
 CLASSES = ["patch", "ln", "qkv", "attn", "proj", "fc1", "fc2", "head"]
 
-TRACE_ARGS = ["--steps", "20", "--warmup", "3", "--no-cpu", "--no-latency", "--modes", "0",
-              "--copy-probe"]
-PMC_ARGS = ["--steps", "2", "--warmup", "1", "--no-cpu", "--no-latency", "--modes", "0",
-            "--copy-probe"]
+TRACE_ARGS = ["--steps", "20", "--warmup", "3", "--copy-probe"]
+PMC_ARGS = ["--steps", "2", "--warmup", "1", "--copy-probe"]
+# Published MI355X peaks the roofline column prices against: dense bf16 MFMA
+# and HBM3E bandwidth.
+PEAK_BF16_FLOPS = 2.5e15
+PEAK_HBM_BYTES = 8.0e12
 PASSES = {
     "fetch": ["FETCH_SIZE"],
     "write": ["WRITE_SIZE"],
@@ -144,11 +146,16 @@ def run_pass(out, tag, rocprof_args, bench_args, limit):
 
 
 def _portable(cmd):
-    """A command as text, with this checkout's absolute paths shown as <repo>."""
-    return " ".join(cmd).replace(ROOT, "<repo>")
+    """A command as text, with the checkout's absolute paths shown as <repo>
+    (the checkout the command ran in: the directory of its bench.py)."""
+    roots = {ROOT} | {os.path.dirname(a) for a in cmd if a.endswith("/bench.py")}
+    text = " ".join(cmd)
+    for r in sorted(roots, key=len, reverse=True):
+        text = text.replace(r, "<repo>")
+    return text
 
 
-def summarize(out, cmds):
+def summarize(out, cmds, mode):
     work = json.load(open(os.path.join(out, "work.json")))
     names, dur = read_trace(os.path.join(out, "trace"))
     cls = classify(names)
@@ -193,19 +200,25 @@ def summarize(out, cmds):
         e = {"launches": n, "avg_us": us, "flops": flops, "algo_bytes": algo_b,
              "tflops": flops / us * 1e-6 if flops else None, "gbs": algo_b / us * 1e-3,
              "fetch_bytes": rd.get(c, (0, None))[1], "write_bytes": wr.get(c, (0, None))[1],
-             "hbm_bytes": hbm, "mfma_util": util}
+             "hbm_bytes": hbm, "mfma_util": util,
+             # Roofline time: the larger of the FLOPs at the bf16 peak and the
+             # algorithmic bytes at the HBM peak; frac = that / measured time.
+             "roofline_frac": max(flops / PEAK_BF16_FLOPS, algo_b / PEAK_HBM_BYTES) / (us * 1e-6),
+             "roofline_bound": "mfma" if flops / PEAK_BF16_FLOPS >= algo_b / PEAK_HBM_BYTES
+             else "hbm"}
         table[c] = e
         rows.append(
             f"| {c} | {n} | {us:.1f} | "
             + (f"{e['tflops']:.0f} TF/s" if flops else "-") + f" | {e['gbs']:.0f} GB/s | "
             + (f"{100 * util:.1f}%" if util is not None else "-") + " | "
+            + f"{e['roofline_frac']:.2f} ({e['roofline_bound']}) | "
             + f"{algo_b / 1e6:.1f} | "
             + (f"{e['fetch_bytes'] / 1e6:.1f} | {e['write_bytes'] / 1e6:.1f} | {hbm / algo_b:.2f}"
                if hbm is not None else "- | - | -") + " |")
 
     dom = work["dominant"]
     traffic = {
-        "workload": "elastic ViT-B/16 forward, DN mode 0, batch 256, bf16",
+        "workload": f"elastic ViT-B/16 forward, DN mode {mode}, batch 256, bf16",
         "kernel_class": dom,
         "source_hash": work["source_hash"],
         "hbm_bytes_per_launch": table[dom]["hbm_bytes"],
@@ -222,11 +235,11 @@ def summarize(out, cmds):
     json.dump(traffic, open(os.path.join(out, "traffic.json"), "w"), indent=1)
 
     md = [
-        "# Kernel classes of the elastic ViT-B/16 forward — bf16, batch 256, DN mode 0",
+        f"# Kernel classes of the elastic ViT-B/16 forward — bf16, batch 256, DN mode {mode}",
         "",
         "Commands (GPU box, run from `/tmp` with `TMPDIR=/tmp`; committed files only):",
         "",
-        "    python -m paper_2609_10018_amd.pmc --out <repo>/gpurun_out/pmc",
+        f"    python -m paper_2609_10018_amd.pmc --out <repo>/gpurun_out/pmc --mode {mode}",
         "",
         "which runs:",
         "",
@@ -243,11 +256,12 @@ def summarize(out, cmds):
         f"scales {rd_scale:.3f} and {wr_scale:.3f}; a read-only probe, a sum over the same "
         f"1 GiB, gives a fetch scale of "
         + (f"{rd_read_scale:.3f}" if rd_read_scale else "n/a") +
-        "). Ratio = (fetch + write) / algorithmic bytes.",
+        "). Ratio = (fetch + write) / algorithmic bytes. Roofline frac = max(FLOPs / "
+        "2.5 PFLOP/s, algorithmic bytes / 8 TB/s) / time, with the bound that sets it.",
         "",
         "| class | launches | avg µs | achieved (algorithmic FLOP) | algorithmic bytes / time "
-        "| MFMA util | algorithmic MB | fetch MB | write MB | ratio |",
-        "|---|---|---|---|---|---|---|---|---|---|",
+        "| MFMA util | roofline frac | algorithmic MB | fetch MB | write MB | ratio |",
+        "|---|---|---|---|---|---|---|---|---|---|---|",
         *rows,
         "",
         f"Dominant class: **{dom}**, {table[dom]['avg_us']:.1f} µs per launch in the trace; "
@@ -274,20 +288,23 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "pmc"))
     ap.add_argument("--summarize-only", action="store_true")
+    ap.add_argument("--mode", type=int, default=0, help="DN mode to profile")
     args = ap.parse_args()
     out = os.path.abspath(args.out)
     os.makedirs(out, exist_ok=True)
     cmds = {}
     if not args.summarize_only:
         _, cmds["trace"] = run_pass(out, "trace", ["--kernel-trace", "--stats"],
-                                    TRACE_ARGS + ["--work-out", os.path.join(out, "work.json")],
+                                    TRACE_ARGS + ["--profile-mode", str(args.mode),
+                                                  "--work-out", os.path.join(out, "work.json")],
                                     300)
         for tag, counters in PASSES.items():
-            _, cmds[tag] = run_pass(out, tag, ["--pmc", *counters], PMC_ARGS, 180)
+            _, cmds[tag] = run_pass(out, tag, ["--pmc", *counters],
+                                    PMC_ARGS + ["--profile-mode", str(args.mode)], 180)
         json.dump(cmds, open(os.path.join(out, "commands.json"), "w"))
     else:
         cmds = json.load(open(os.path.join(out, "commands.json")))
-    summarize(out, cmds)
+    summarize(out, cmds, args.mode)
 
 
 if __name__ == "__main__":

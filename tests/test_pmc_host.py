@@ -101,8 +101,9 @@ def test_summarize_synthetic(tmp_path):
                    "launches_per_forward": 1} for c in pmc.CLASSES}
     json.dump({"classes": classes, "dominant": "fc1", "dominant_avg_us": 60.5,
                "class_ms_mode0": {}, "source_hash": "abc"}, open(os.path.join(out, "work.json"), "w"))
-    pmc.summarize(out, {"trace": ["x"], "fetch": ["y"]})
+    pmc.summarize(out, {"trace": ["x"], "fetch": ["y"]}, 3)
     tr = json.load(open(os.path.join(out, "traffic.json")))
+    assert "DN mode 3" in tr["workload"]
     assert tr["kernel_class"] == "fc1" and tr["source_hash"] == "abc"
     assert tr["calibration"]["fetch_scale"] == pytest.approx(2.0)
     assert tr["calibration"]["write_scale"] == pytest.approx(1.0)
@@ -113,4 +114,7 @@ def test_summarize_synthetic(tmp_path):
     fc1 = tr["classes"]["fc1"]
     assert fc1["avg_us"] == pytest.approx(60.0) and fc1["launches"] == 2
     assert fc1["mfma_util"] == pytest.approx(0.5)
+    # roofline: max(1e9 / 2.5e15, 4.096e6 / 8e12) s = 0.512 us over 60 us, memory-bound
+    assert fc1["roofline_frac"] == pytest.approx(4.096e6 / 8e12 / 60e-6)
+    assert fc1["roofline_bound"] == "hbm"
     assert "fc1" in open(os.path.join(out, "summary.md")).read()
