@@ -68,6 +68,8 @@ struct Acts {
   void *x = nullptr, *u = nullptr, *o = nullptr, *qkv = nullptr, *g = nullptr, *ucls = nullptr;
   float* xcls = nullptr;
   float2* lnpart = nullptr;
+  float* ws = nullptr;
+  int64_t ws_bytes = 0;
 };
 
 // Carves the activation buffers of a forward of up to `batch` images out of
@@ -75,9 +77,11 @@ struct Acts {
 // residual stream and u, o, qkv, g, ucls hold activations, all in the path's
 // dtype; on the bf16 path the class-token rows of the residual stream are
 // kept in fp32 in xcls (they alone decide the logits) and lnpart holds the
-// per-segment LayerNorm statistics of every row of x (lnseg float2 a row).
+// per-segment LayerNorm statistics of every row of x (lnseg float2 a row);
+// ws_bytes more (a multiple of 256) follow for the split-K workspace of the
+// small-batch GEMMs.
 int64_t scratch_layout(const elasto_config_t& cfg, const Dims& d, int lnseg, int64_t batch,
-                       uint8_t* base, Acts* a) {
+                       int64_t ws_bytes, uint8_t* base, Acts* a) {
   const int64_t eb = cfg.dtype == ELASTO_BF16 ? 2 : 4;
   const int64_t rows = batch * d.T, D = cfg.dim;
   auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
@@ -94,8 +98,11 @@ int64_t scratch_layout(const elasto_config_t& cfg, const Dims& d, int lnseg, int
     a->ucls = p; p += sz_cls;
     a->xcls = reinterpret_cast<float*>(p); p += sz_xcls;
     a->lnpart = lnseg > 0 ? reinterpret_cast<float2*>(p) : nullptr;
+    p += sz_ln;
+    a->ws = ws_bytes > 0 ? reinterpret_cast<float*>(p) : nullptr;
+    a->ws_bytes = ws_bytes;
   }
-  return 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls + sz_ln;
+  return 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls + sz_ln + ws_bytes;
 }
 
 elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
@@ -179,7 +186,8 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   auto al = [](int64_t v) { return (v + 255) / 256 * 256; };
   const bool bf = cfg->dtype == ELASTO_BF16;
   h->lnseg = bf ? (int)((D + 127) / 128 * 2) : 0;  // 64-column segments, rounded up to even
-  h->sbytes = scratch_layout(*cfg, h->dims, h->lnseg, cfg->max_batch, nullptr, nullptr);
+  const int64_t ws_bytes = bf ? kSplitWsBytes : 0;
+  h->sbytes = scratch_layout(*cfg, h->dims, h->lnseg, cfg->max_batch, ws_bytes, nullptr, nullptr);
   h->wbytes = h->lay.total;
   if (bf) {
     h->width_idx.resize((size_t)table->num_modes);
@@ -220,7 +228,7 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
     return fail(st, "create: %s", hipGetErrorString(e));
   }
   Acts a;
-  scratch_layout(*cfg, h->dims, h->lnseg, cfg->max_batch, h->ds, &a);
+  scratch_layout(*cfg, h->dims, h->lnseg, cfg->max_batch, ws_bytes, h->ds, &a);
   h->x = a.x;
   h->u = a.u;
   h->o = a.o;
@@ -229,6 +237,8 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   h->ucls = a.ucls;
   h->xcls = a.xcls;
   h->lnpart = a.lnpart;
+  h->ws = a.ws;
+  h->ws_bytes = a.ws_bytes;
   *out = h;
   clear_error();
   return ELASTO_OK;
@@ -368,7 +378,7 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
   Acts a;
   a.x = h->x; a.u = h->u; a.o = h->o; a.qkv = h->qkv; a.g = h->g; a.ucls = h->ucls;
-  a.xcls = h->xcls; a.lnpart = h->lnpart;
+  a.xcls = h->xcls; a.lnpart = h->lnpart; a.ws = h->ws; a.ws_bytes = h->ws_bytes;
   return forward_impl(h, images, batch, logits, hip_stream, a);
 }
 
@@ -377,7 +387,7 @@ elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int
   if (!h) return fail(ELASTO_ERR_INVALID_ARG, "handle is NULL");
   if (batch < 1 || batch > h->cfg.max_batch)
     return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
-  const int64_t need = scratch_layout(h->cfg, h->dims, h->lnseg, batch, nullptr, nullptr);
+  const int64_t need = scratch_layout(h->cfg, h->dims, h->lnseg, batch, 0, nullptr, nullptr);
   if (need > kStaticScratchBytes)
     return fail(ELASTO_ERR_BATCH_RANGE,
                 "batch %d needs %lld bytes of activation scratch; the static scratch holds %lld",
@@ -390,8 +400,11 @@ elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int
   int64_t have = 0;
   const hipError_t e = static_scratch(&base, &have);
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "static scratch: %s", hipGetErrorString(e));
+  // What the activations leave of the array serves as split-K workspace.
+  const int64_t ws_bytes = h->cfg.dtype == ELASTO_BF16
+                               ? std::min(kSplitWsBytes, (have - need) / 256 * 256) : 0;
   Acts a;
-  scratch_layout(h->cfg, h->dims, h->lnseg, batch, static_cast<uint8_t*>(base), &a);
+  scratch_layout(h->cfg, h->dims, h->lnseg, batch, ws_bytes, static_cast<uint8_t*>(base), &a);
   return forward_impl(h, images, batch, logits, hip_stream, a);
 }
 
@@ -482,6 +495,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       q.ln_colsum = reinterpret_cast<const float*>(fold_ptr(l, h->fold_sq)) + (int64_t)wi * 3 * D;
       q.ln_in = act.lnpart; q.ln_ld = h->lnseg; q.ln_eps = c.ln_eps;
     }
+    q.ws = act.ws; q.ws_bytes = act.ws_bytes;
     e = timed(h, ELASTO_K_QKV, s, [&] { return gemm(Epi::Bias, q, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "qkv layer %d: %s", l, hipGetErrorString(e));
     AttnArgs at;
@@ -501,6 +515,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
     if (fold) {
       pr.ln_out = act.lnpart; pr.ln_ld = h->lnseg;
     }
+    pr.ws = act.ws; pr.ws_bytes = act.ws_bytes;
     e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
     if (!fold) {
@@ -520,6 +535,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       f1.ln_colsum = reinterpret_cast<const float*>(fold_ptr(l, h->fold_s1)) + (int64_t)wi * Mh;
       f1.ln_in = act.lnpart; f1.ln_ld = h->lnseg; f1.ln_eps = c.ln_eps;
     }
+    f1.ws = act.ws; f1.ws_bytes = act.ws_bytes;
     e = timed(h, ELASTO_K_FC1, s, [&] { return gemm(Epi::BiasGelu, f1, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f2;
@@ -533,6 +549,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
     if (fold) {
       f2.ln_out = act.lnpart; f2.ln_ld = h->lnseg;
     }
+    f2.ws = act.ws; f2.ws_bytes = act.ws_bytes;
     e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
   }

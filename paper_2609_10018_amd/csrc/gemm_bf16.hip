@@ -1166,6 +1166,131 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   wait_vm_lds<0>();
 }
 
+// Split-K epilogue.  A GEMM whose tiles would occupy few of the CUs (small M:
+// batch-1 and batch-8 forwards) runs as ksplit K-chunks of the BiasF32 kernel
+// writing fp32 partial products, then this kernel sums each output's partials
+// in chunk order and applies the epilogue E: the folded-LayerNorm consumer
+// (Bias, BiasGelu) or the residual add with the LayerNorm-statistics producer
+// (BiasResid), with the same arithmetic as the tile epilogues.  One thread per
+// 8-column chunk of an output row; a row's chunks are padded to a multiple of
+// 8 threads, so the 8 lanes of an aligned group hold one 64-column segment.
+struct SplitEpi {
+  const float* part;   // ksplit slices of [M][ldp] fp32
+  int64_t ldp, slice;  // row stride of a slice (a multiple of 8), elements per slice
+  int ksplit, M, N, K, cpr;
+  void* C;
+  int64_t ldc;
+  const float* bias;
+  const uint16_t* res;  // BiasResid residual (nullptr: C)
+  int64_t ldres;
+  float* ccls;
+  int tokens;
+  float2* ln_out;
+  const float2* ln_in;
+  int64_t ln_ld;
+  const float* ln_colsum;
+  float ln_eps;
+};
+
+template <Epi E>
+__global__ __launch_bounds__(64) void splitk_epilogue_kernel(SplitEpi q) {
+  static_assert(E == Epi::Bias || E == Epi::BiasGelu || E == Epi::BiasResid, "split-K epilogues");
+  const int64_t g = (int64_t)blockIdx.x * 64 + threadIdx.x;
+  const int row = (int)(g / q.cpr), cc = (int)(g - (int64_t)row * q.cpr);
+  if (row >= q.M) return;  // whole 8-lane groups: cpr is a multiple of 8
+  const int col = cc * 8;
+  const bool col_in = col < q.N, full = col + 8 <= q.N;
+  float v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (col_in) {
+    const float* pp = q.part + (int64_t)row * q.ldp + col;
+    for (int c0 = 0; c0 < q.ksplit; c0 += 8) {
+      f32x4 t[8][2];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float* src = pp + (int64_t)min(c0 + u, q.ksplit - 1) * q.slice;
+        t[u][0] = *reinterpret_cast<const f32x4*>(src);
+        t[u][1] = *reinterpret_cast<const f32x4*>(src + 4);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (c0 + u < q.ksplit) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] += t[u][0][e];
+            v[4 + e] += t[u][1][e];
+          }
+        }
+    }
+  }
+  float bv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bv[e] = col + e < q.N ? q.bias[col + e] : 0.0f;
+  uint16_t* cp = static_cast<uint16_t*>(q.C) + (int64_t)row * q.ldc + col;
+  if constexpr (E == Epi::Bias || E == Epi::BiasGelu) {
+    if (!col_in) return;
+    if (q.ln_in != nullptr) {
+      LnStat st{0.0f, 0.0f, 0.0f};
+      ln_sums(q.ln_in + (int64_t)row * q.ln_ld, q.K, 0, 1, st);
+      const float2 rs = ln_factors(st, q.ln_eps);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float cs = col + e < q.N ? q.ln_colsum[col + e] : 0.0f;
+        v[e] = fmaf(v[e], rs.x, fmaf(rs.y, cs, bv[e]));
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += bv[e];
+    }
+    if constexpr (E == Epi::BiasGelu) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = gelu_poly(v[e]);
+    }
+    store_bf16x8(cp, v, full, q.N - col);
+  } else {
+    float st[8];
+    bool st_ok = false;
+    if (col_in) {
+      float* cls_row = nullptr;
+      if (q.ccls != nullptr) {
+        const int bi = row / q.tokens;
+        if (row == bi * q.tokens) cls_row = q.ccls + (int64_t)bi * q.N + col;
+      }
+      if (cls_row != nullptr) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = col + e < q.N ? cls_row[e] + (v[e] + bv[e]) : 0.0f;
+        store_f32x8(cls_row, v, full, q.N - col);
+        if (q.ln_out != nullptr) store_bf16x8(cp, v, full, q.N - col);
+      } else {
+        const uint16_t* rp = q.res != nullptr ? q.res + (int64_t)row * q.ldres + col : cp;
+        if (full) {
+          const u32x4 x = *reinterpret_cast<const u32x4*>(rp);
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16)) +
+                   (v[e] + bv[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            v[e] = col + e < q.N ? bf16_to_f32(rp[e]) + (v[e] + bv[e]) : 0.0f;
+        }
+        store_bf16x8(cp, v, full, q.N - col);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) st[e] = v[e];
+      st_ok = true;
+    }
+    if (q.ln_out != nullptr) {
+      LnStat ls = ln_of8(st, st_ok);
+      ln_merge_dpp<kDppXor1>(ls);
+      ln_merge_dpp<kDppXor2>(ls);
+      ln_merge_dpp<kDppHalfMirror>(ls);
+      const int seg = cc >> 3;
+      if ((cc & 7) == 0 && 64 * seg < q.N)
+        q.ln_out[(int64_t)row * q.ln_ld + seg] = make_float2(ls.n * ls.mean, ls.m2);
+    }
+  }
+}
+
 template <int BM, int BN, int WM, int WN, Epi E, bool CONV, int STAGES = 2>
 hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   Params p = p0;
@@ -1309,6 +1434,84 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
   }
 }
 
+// Split-K plan for launches whose 128x128 tiles would fill under half the
+// CUs: the K loop is then the critical path of every workgroup (about one
+// memory latency per K step).  Cutting it into chunks costs a second launch
+// and the fp32 partials' round trip, so the plan takes the chunk count with
+// the smallest estimated time, in microseconds, measured on MI355X at batch 1
+// and 8 of ViT-B/16:
+//   one launch:  3 + 1.1 nk,
+//   c chunks:   11 + 1.1 ceil(nk / c) + c M N 8 bytes / 3.5 TB/s,
+// with at least two K steps a chunk and at most one workgroup per CU.
+// Returns the chunk count (1: no split) and the chunk length.
+int split_plan(const Params& p, int64_t ws_bytes, int* kchunk) {
+  constexpr int kCUs = 256;
+  const int64_t tiles = (int64_t)((p.M + 127) / 128) * ((p.N + 127) / 128);
+  const int nk = (p.K + kBK - 1) / kBK;
+  if (tiles * 2 > kCUs || nk < 4) return 1;
+  const int64_t ldp = (p.N + 7) / 8 * 8;
+  const int most = (int)std::min<int64_t>(kCUs / tiles, nk / 2);
+  double best_t = 3.0 + 1.1 * nk - 1.0;  // a split must win by a microsecond
+  int best = 1;
+  for (int c = 2; c <= most; ++c) {
+    if ((int64_t)c * p.M * ldp * 4 > ws_bytes) break;
+    const int steps = (nk + c - 1) / c;
+    const double t = 11.0 + 1.1 * steps + (double)c * p.M * ldp * 8.0 / 3.5e6;
+    if (t < best_t) { best_t = t; best = c; }
+  }
+  if (best < 2) return 1;
+  const int steps = (nk + best - 1) / best;
+  *kchunk = steps * kBK;
+  return (nk + steps - 1) / steps;
+}
+
+template <Epi E>
+hipError_t launch_split(const Params& p, float* ws, int ksplit, int kchunk, hipStream_t s) {
+  Params pp = p;
+  const int64_t ldp = (p.N + 7) / 8 * 8;
+  pp.C = ws;
+  pp.ldc = ldp;
+  pp.bias = nullptr;
+  pp.ccls = nullptr;
+  pp.res = nullptr;
+  pp.aux = nullptr;
+  pp.ln_out = nullptr;
+  pp.ln_in = nullptr;
+  pp.relu = 0;
+  pp.ksplit = ksplit;
+  pp.kchunk = kchunk;
+  pp.c_split = (int64_t)p.M * ldp;
+  hipError_t e = (p.K % kBK == 0 && kchunk / kBK >= 4)
+                     ? launch_cfg<128, 128, 2, 2, Epi::BiasF32, false, 4>(pp, 0, s)
+                     : launch_cfg<128, 128, 2, 2, Epi::BiasF32, false>(pp, 0, s);
+  if (e != hipSuccess) return e;
+  SplitEpi q;
+  q.part = ws;
+  q.ldp = ldp;
+  q.slice = pp.c_split;
+  q.ksplit = ksplit;
+  q.M = p.M;
+  q.N = p.N;
+  q.K = p.K;
+  q.cpr = (int)((p.N + 63) / 64 * 8);
+  q.C = p.C;
+  q.ldc = p.ldc;
+  q.bias = p.bias;
+  q.res = p.res;
+  q.ldres = p.ldres;
+  q.ccls = p.ccls;
+  q.tokens = p.tokens;
+  q.ln_out = p.ln_out;
+  q.ln_in = p.ln_in;
+  q.ln_ld = p.ln_ld;
+  q.ln_colsum = p.ln_colsum;
+  q.ln_eps = p.ln_eps;
+  const int64_t threads = (int64_t)p.M * q.cpr;
+  hipLaunchKernelGGL(splitk_epilogue_kernel<E>, dim3((unsigned)((threads + 63) / 64)), dim3(64),
+                     0, s, q);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
@@ -1363,6 +1566,19 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   if (a.res != nullptr && (a.ldres < a.N || a.ldres % 8 != 0)) return hipErrorInvalidValue;
   if (a.aux != nullptr && epi == Epi::BiasGelu && (a.ldaux < a.N || a.ldaux % 8 != 0))
     return hipErrorInvalidValue;
+  // Small M: split K over more workgroups when the caller gave a workspace.
+  if (a.ws != nullptr && a.ksplit <= 1 && !a.relu && a.aux == nullptr && p.bias != nullptr &&
+      (epi == Epi::Bias || epi == Epi::BiasGelu || epi == Epi::BiasResid)) {
+    int kchunk = 0;
+    const int ksplit = split_plan(p, a.ws_bytes, &kchunk);
+    if (ksplit > 1) {
+      switch (epi) {
+        case Epi::Bias: return launch_split<Epi::Bias>(p, a.ws, ksplit, kchunk, s);
+        case Epi::BiasGelu: return launch_split<Epi::BiasGelu>(p, a.ws, ksplit, kchunk, s);
+        default: return launch_split<Epi::BiasResid>(p, a.ws, ksplit, kchunk, s);
+      }
+    }
+  }
   switch (epi) {
     case Epi::Bias: return launch_epi<Epi::Bias>(p, s);
     case Epi::BiasGelu: return launch_epi<Epi::BiasGelu>(p, s);

@@ -34,6 +34,8 @@ struct elasto_handle_s {
   std::vector<int32_t> widths;     // distinct active embedding widths
   std::vector<int32_t> width_idx;  // [num_modes] index into widths
   float2* lnpart = nullptr;        // [max_batch * T][lnseg] per-segment LayerNorm statistics
+  float* ws = nullptr;             // split-K workspace of small-batch GEMMs (bf16 path)
+  int64_t ws_bytes = 0;
   int lnseg = 0;                   // 64-column segments of d, rounded up to even
   // kernel timing
   int timed_class = -1;

@@ -71,7 +71,19 @@ struct GemmArgs {
   int64_t ln_ld = 0;
   const float* ln_colsum = nullptr;
   float ln_eps = 0.0f;
+  // Bias, BiasGelu, BiasResid (bf16, no relu / aux): a device workspace of
+  // ws_bytes (256-byte aligned) lets a launch whose 128x128 tiles would fill
+  // under half the CUs split K into chunks whose fp32 partial products go
+  // there, summed by a second kernel that applies the epilogue.  At most
+  // kSplitWsBytes is ever used.
+  float* ws = nullptr;
+  int64_t ws_bytes = 0;
 };
+
+// Largest split-K workspace the planner uses: chunks are limited to the CU
+// count over the 128x128 tile count, so chunks x M x N stays below
+// 256 x 128 x 128 fp32 values.
+constexpr int64_t kSplitWsBytes = (int64_t)256 * 128 * 128 * 4;
 
 hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s);
 

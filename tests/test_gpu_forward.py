@@ -132,10 +132,11 @@ def test_vit_b_partial_batches(batch):
 
 
 @pytest.mark.parametrize("name,batches", [("vit_ti", (1, 2, 5)), ("vit_s", (1, 3, 8)),
-                                          ("vit_b_emb", (1, 8))])
+                                          ("vit_b", (1, 2, 8)), ("vit_b_emb", (1, 8))])
 def test_small_batches(name, batches):
-    """Batch 1-8 (few tiles per GEMM, ragged K on ViT-S): every mode matches
-    the oracle, and repeated calls are identical."""
+    """Batch 1-8 (few tiles per GEMM, so the GEMMs split K over more
+    workgroups; ragged K on ViT-S and in narrow modes): every mode matches the
+    oracle, and repeated calls are identical."""
     m = model(name)
     gold = golden(name)
     for batch in batches:
@@ -227,6 +228,22 @@ def test_prefix_read_nan_poison(name, k):
     poisoned.vit.close()
     assert np.isfinite(got).all()
     np.testing.assert_array_equal(got, ref)
+
+
+@pytest.mark.parametrize("name,k,batch", [("vit_s", 4, 1), ("vit_b", 4, 1), ("vit_b", 3, 8),
+                                          ("vit_ti_emb", 3, 1)])
+def test_prefix_read_nan_poison_small_batch(name, k, batch):
+    """The split-K path of small batches (each K chunk a slice of the prefix,
+    the last one ragged) reads no weight outside mode k's prefix either."""
+    clean = model(name)
+    ref = clean.run(k, batch)
+    poisoned = Model(name, max_batch=batch,
+                     weights=_poison_outside(clean.w, clean.cfg, clean.table, k))
+    poisoned.xd = clean.xd[:batch].contiguous()  # the same images
+    got = poisoned.run(k, batch)
+    poisoned.vit.close()
+    assert np.isfinite(got).all()
+    np.testing.assert_allclose(got, ref, rtol=0, atol=0)
 
 
 def test_error_paths_on_device():
