@@ -26,9 +26,12 @@ from gpu_util import dev, rel_err  # noqa: E402
 
 # The bf16 parity bar (R11: max |error| over a slice / max |expected| of that
 # slice).  bf16 activations, weights and backward intermediates through 12
-# layers each round at 2^-9 relative; the per-slice errors measured are below
-# 1%.  Slices whose exact gradient vanishes (the key bias: softmax ignores a
-# shift shared by all keys) are measured against 1e-3 of the step's largest
+# layers each round at 2^-9 relative; with the oracle fed the same
+# bf16-rounded images, the worst slice errors measured are 1.87e-2 (ViT-Ti,
+# mode 0), 1.35e-2 (ViT-Ti, mode 2), 1.58e-2 (ViT-S, mode 1) and 1.28e-2
+# (ViT-B, mode 0), so the bar sits just above them (the step is deterministic).
+# Slices whose exact gradient vanishes (the key bias: softmax ignores a shift
+# shared by all keys) are measured against 1e-3 of the step's largest
 # gradient entry instead.
 GRAD_TOL = 2e-2
 LOSS_TOL = 1e-2
