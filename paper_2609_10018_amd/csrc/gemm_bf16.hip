@@ -79,6 +79,8 @@ struct Params {
   // elements of the step); tap / KW = (tap * kwinv) >> 16.
   int cv_H, cv_W, cv_Cs, cv_Ca, cv_KW, cv_T, cv_stride, cv_pad, cv_Ho, cv_Wo, cv_wseg, cv_nc;
   int cv_tps, cv_cshift, cv_kwinv;
+  int cv_ncinv;     // K step / nc = (step * cv_ncinv) >> 16 (exact for every step)
+  int patch_shift;  // Patch: log2(patch) when patch is a power of two, else -1
   int a_bytes, w_bytes;
   // BiasResid residual source (nullptr: C itself); BiasGelu pre-activation
   // output / GeluBwd pre-activation input (nullptr: none).
@@ -260,7 +262,14 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int ABLK = BM / kRowsPerBlock, BBLK = BN / kRowsPerBlock;
   constexpr int PER_WAVE = (ABLK + BBLK) / NW;
-  static_assert((ABLK + BBLK) % NW == 0, "blocks must split evenly over waves");
+  // Gathering loaders (convolutions, patches): load i of wave w brings block
+  // i * NW + w, so loads i < APW are A blocks and the rest W blocks for every
+  // wave, and whether a load gathers is known at compile time (no branch on
+  // the wave index in the K loop).  Plain GEMMs keep contiguous blocks per
+  // wave (block w * PER_WAVE + i), measured faster for them.
+  constexpr bool GATHER = CONV || E == Epi::Patch;
+  constexpr int APW = ABLK / NW;
+  static_assert(ABLK % NW == 0 && BBLK % NW == 0, "blocks must split evenly over waves");
   constexpr int STAGE = (BM + BN) * kRowBytes;
   constexpr int EPI_BYTES = (BM > 128 ? 128 : BM) * (BN + 8) * 4;
   constexpr int SMEM_MAIN = STAGES * STAGE > EPI_BYTES ? STAGES * STAGE : EPI_BYTES;
@@ -301,13 +310,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   int chunk[PER_WAVE];
   int ldsoff[PER_WAVE];
   // CONV: element offset of the row's tap-0 pixel (A) or of the weight row
-  // (W), and the tap-0 input coordinates (A).
-  int cbase[PER_WAVE], cih[PER_WAVE], ciw[PER_WAVE];
+  // (W), and (A) the taps that fall inside the image: bit t of tmask is set
+  // when tap t (kernel row t / KW, column t % KW) of the row's output pixel
+  // reads an input pixel, so a K step tests one bit instead of two ranges.
+  int cbase[PER_WAVE];
+  uint64_t tmask[PER_WAVE];
   const int prow = lane >> 3, pc = lane & 7;
 #pragma unroll
   for (int i = 0; i < PER_WAVE; ++i) {
-    const int blk = wave * PER_WAVE + i;
-    if (blk < ABLK) {
+    const int blk = GATHER ? i * NW + wave : wave * PER_WAVE + i;
+    if (GATHER ? i < APW : blk < ABLK) {
       const int r = blk * kRowsPerBlock + prow;
       const int gm = min(m0 + r, p.M - 1);
       chunk[i] = pc ^ swz(r);
@@ -315,9 +327,19 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       if constexpr (CONV) {
         const int hw = p.cv_Ho * p.cv_Wo, im = gm / hw, rem = gm - im * hw;
         const int oh = rem / p.cv_Wo, ow = rem - oh * p.cv_Wo;
-        cih[i] = oh * p.cv_stride - p.cv_pad;
-        ciw[i] = ow * p.cv_stride - p.cv_pad;
-        cbase[i] = ((im * p.cv_H + cih[i]) * p.cv_W + ciw[i]) * p.cv_Cs;
+        const int ih = oh * p.cv_stride - p.cv_pad, iw = ow * p.cv_stride - p.cv_pad;
+        cbase[i] = ((im * p.cv_H + ih) * p.cv_W + iw) * p.cv_Cs;
+        // Keep the product itself in a register: folding the tap offset into
+        // its factors would put a multiply into every load of the K loop.
+        asm volatile("" : "+v"(cbase[i]));
+        uint64_t m = 0;
+        for (int t = 0; t < p.cv_T; ++t) {
+          const int ti = (t * p.cv_kwinv) >> 16, tj = t - ti * p.cv_KW;
+          const bool in = ((unsigned)(ih + ti) < (unsigned)p.cv_H) &
+                          ((unsigned)(iw + tj) < (unsigned)p.cv_W);
+          m |= (uint64_t)in << t;
+        }
+        tmask[i] = m;
         src[i] = nullptr;
       } else if constexpr (E == Epi::Patch) {
         const int bi = gm / p.tokens, t = gm - bi * p.tokens;
@@ -334,16 +356,40 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       src[i] = p.W + (int64_t)min(n0 + r, p.N - 1) * p.ldw;
       if constexpr (CONV) {
         cbase[i] = min(n0 + r, p.N - 1) * (int)p.ldw;
-        cih[i] = ciw[i] = 0;
+        tmask[i] = 0;
       }
     }
   }
+  // Patch rows with a power-of-two patch of at least 8: a K step (64 values)
+  // stays in one channel and covers whole patch rows, so the im2col offset
+  // of (step kt, chunk q) splits into a per-step part, the same for every
+  // lane, and a per-chunk part fixed for the row block (plofs).
+  int plofs[PER_WAVE];
+  if constexpr (E == Epi::Patch) {
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int q = chunk[i] * 8, sh = p.patch_shift > 0 ? p.patch_shift : 0;
+      plofs[i] = (q >> sh) * p.img_size + (q & (p.patch - 1));
+    }
+  }
+  const bool patch_fast = E == Epi::Patch && p.patch_shift >= 3;
   // Element offset of k-index k within a source row (im2col for patches).
   auto koff = [&](int i, int k) -> int64_t {
     if constexpr (E == Epi::Patch) {
-      if (wave * PER_WAVE + i < ABLK) {
-        const int pp = p.patch * p.patch;
-        const int c = k / pp, rem = k - c * pp, ii = rem / p.patch, jj = rem - ii * p.patch;
+      if (i < APW) {
+        int c, ii, jj;
+        if (p.patch_shift >= 0) {
+          const int sh = p.patch_shift, msk = p.patch - 1;
+          c = k >> (2 * sh);
+          ii = (k >> sh) & msk;
+          jj = k & msk;
+        } else {
+          const int pp = p.patch * p.patch;
+          c = k / pp;
+          const int rem = k - c * pp;
+          ii = rem / p.patch;
+          jj = rem - ii * p.patch;
+        }
         return ((int64_t)c * p.img_size + ii) * p.img_size + jj;
       }
     }
@@ -370,11 +416,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         for (int i = 0; i < PER_WAVE; ++i) {
           if (i < lo || i >= hi) continue;
           const int q = chunk[i] * 8, t = t0 + (q >> p.cv_cshift), ch = q & cmask;
-          const bool tap_ok = t < p.cv_T && ch < p.cv_Ca;
+          const bool tap_ok = (t < p.cv_T) & (ch < p.cv_Ca);
           const int ti = (t * p.cv_kwinv) >> 16, tj = t - ti * p.cv_KW;
-          if (wave * PER_WAVE + i < ABLK) {
-            const bool ok = tap_ok && (unsigned)(cih[i] + ti) < (unsigned)p.cv_H &&
-                            (unsigned)(ciw[i] + tj) < (unsigned)p.cv_W;
+          if (i < APW) {
+            const bool ok = tap_ok & (bool)((tmask[i] >> (t & 63)) & 1u);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rs_a, (lds_void*)(base + ldsoff[i]), 16,
                 ok ? (unsigned)(cbase[i] + (ti * p.cv_W + tj) * p.cv_Cs + ch) * 2u : kOutOfRange,
@@ -387,16 +432,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         }
         return;
       }
-      const int t = kt / p.cv_nc, c0 = (kt - t * p.cv_nc) * kBK;
-      const int ti = t / p.cv_KW, tj = t - ti * p.cv_KW;
+      const int t = (kt * p.cv_ncinv) >> 16, c0 = (kt - t * p.cv_nc) * kBK;
+      const int ti = (t * p.cv_kwinv) >> 16, tj = t - ti * p.cv_KW;
       const int tap = (ti * p.cv_W + tj) * p.cv_Cs, wtap = t * p.cv_wseg;
 #pragma unroll
       for (int i = 0; i < PER_WAVE; ++i) {
         if (i < lo || i >= hi) continue;
         const int ch = c0 + chunk[i] * 8;
-        if (wave * PER_WAVE + i < ABLK) {
-          const bool ok = ch < p.cv_Ca && (unsigned)(cih[i] + ti) < (unsigned)p.cv_H &&
-                          (unsigned)(ciw[i] + tj) < (unsigned)p.cv_W;
+        if (i < APW) {
+          const bool ok = (ch < p.cv_Ca) & (bool)((tmask[i] >> t) & 1u);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
               rs_a, (lds_void*)(base + ldsoff[i]), 16,
               ok ? (unsigned)(cbase[i] + tap + ch) * 2u : kOutOfRange, 0, 0, 0);
@@ -407,11 +451,22 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
         }
       }
     } else if (kt < nk_full) {
+      // Patch rows, fast form: offset of step kt's channel and patch row.
+      int64_t patch_step = 0;
+      if constexpr (E == Epi::Patch) {
+        if (patch_fast) {
+          const int k0 = kt * kBK, sh = p.patch_shift;
+          patch_step = (int64_t)(k0 >> (2 * sh)) * p.img_size * p.img_size +
+                       (int64_t)((k0 & (p.patch * p.patch - 1)) >> sh) * p.img_size;
+        }
+      }
 #pragma unroll
       for (int i = 0; i < PER_WAVE; ++i)
         if (i >= lo && i < hi)
         __builtin_amdgcn_global_load_lds(
-            (global_void*)(src[i] + koff(i, kt * kBK + chunk[i] * 8)),
+            (global_void*)(src[i] + ((E == Epi::Patch && i < APW && patch_fast)
+                                         ? patch_step + plofs[i]
+                                         : koff(i, kt * kBK + chunk[i] * 8))),
             (lds_void*)(base + ldsoff[i]), 16, 0, 0);
     } else {
       // Ragged last step: masked loads through registers.
@@ -1531,6 +1586,9 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.img = static_cast<const uint16_t*>(a.img);
   p.img_size = a.img_size;
   p.patch = a.patch;
+  p.patch_shift = -1;
+  for (int sh = 0; sh < 16; ++sh)
+    if (a.patch == (1 << sh)) p.patch_shift = sh;
   p.chans = a.chans;
   p.grid = a.grid;
   p.tokens = a.tokens;
@@ -1623,6 +1681,9 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
   const int kwinv = 65536 / a.KW + 1;
   for (int t = 0; t < T + tps; ++t)  // the division by multiplication is exact here
     if ((t * kwinv) >> 16 != t / a.KW) return hipErrorInvalidValue;
+  const int nc = (a.Ca + kBK - 1) / kBK, ncinv = 65536 / nc + 1;
+  for (int kt = 0; kt <= T * nc; ++kt)
+    if ((kt * ncinv) >> 16 != kt / nc) return hipErrorInvalidValue;
   // The range checks take 32-bit offsets: run the batch in runs of images
   // whose input stays below 2 GiB.
   const int per = (int)std::min<int64_t>(a.batch, limit / img_bytes);
@@ -1642,7 +1703,7 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
     p.cv_H = a.H; p.cv_W = a.W; p.cv_Cs = a.Cs; p.cv_Ca = a.Ca; p.cv_KW = a.KW; p.cv_T = T;
     p.cv_stride = a.stride; p.cv_pad = a.pad; p.cv_Ho = Ho; p.cv_Wo = Wo; p.cv_wseg = (int)a.wseg;
     p.cv_nc = (a.Ca + kBK - 1) / kBK;
-    p.cv_tps = tps; p.cv_cshift = cshift; p.cv_kwinv = kwinv;
+    p.cv_tps = tps; p.cv_cshift = cshift; p.cv_kwinv = kwinv; p.cv_ncinv = ncinv;
     p.a_bytes = (int)(nb * img_bytes);
     p.w_bytes = (int)w_bytes;
     const hipError_t e = launch_epi<Epi::Bias, true>(p, s);
