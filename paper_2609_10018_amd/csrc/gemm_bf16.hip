@@ -80,6 +80,7 @@ struct Params {
   int cv_H, cv_W, cv_Cs, cv_Ca, cv_KW, cv_T, cv_stride, cv_pad, cv_Ho, cv_Wo, cv_wseg, cv_nc;
   int cv_tps, cv_cshift, cv_kwinv;
   int cv_ncinv;     // K step / nc = (step * cv_ncinv) >> 16 (exact for every step)
+  int cv_rowb, cv_pixb;  // bytes of one input row (W * Cs * 2) and one pixel (Cs * 2)
   int patch_shift;  // Patch: log2(patch) when patch is a power of two, else -1
   int a_bytes, w_bytes;
   // BiasResid residual source (nullptr: C itself); BiasGelu pre-activation
@@ -275,7 +276,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   constexpr int SMEM_MAIN = STAGES * STAGE > EPI_BYTES ? STAGES * STAGE : EPI_BYTES;
   constexpr bool LN_CONSUMER = E == Epi::Bias || E == Epi::BiasGelu;
   constexpr bool LN_PRODUCER = E == Epi::BiasResid || E == Epi::Patch;
-  constexpr int SMEM = SMEM_MAIN + (LN_CONSUMER ? BM * 8 : 0);  // + per-row LN factors
+  // + per-row LN factors (LayerNorm consumers; convolutions never fold one)
+  constexpr int SMEM = SMEM_MAIN + (LN_CONSUMER && !CONV ? BM * 8 : 0);
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -315,6 +317,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   // reads an input pixel, so a K step tests one bit instead of two ranges.
   int cbase[PER_WAVE];
   uint64_t tmask[PER_WAVE];
+  // CONV with several taps per K step (cv_tps > 1): the lane's tap within a
+  // step (dtap), and its byte offset without the tap term: A, the tap-0
+  // pixel plus the channel; W, the weight row plus the tap's segment and the
+  // channel.  A chunk past the active channels clears the row's tap mask
+  // (A) or wok (W).
+  int dtap[PER_WAVE], boff[PER_WAVE];
+  bool wok[PER_WAVE];
   const int prow = lane >> 3, pc = lane & 7;
 #pragma unroll
   for (int i = 0; i < PER_WAVE; ++i) {
@@ -340,6 +349,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           m |= (uint64_t)in << t;
         }
         tmask[i] = m;
+        if (p.cv_tps > 1) {
+          const int q = chunk[i] * 8, ch = q & ((1 << p.cv_cshift) - 1);
+          dtap[i] = q >> p.cv_cshift;
+          boff[i] = (cbase[i] + ch) * 2;
+          if (ch >= p.cv_Ca) tmask[i] = 0;
+          wok[i] = false;
+        }
         src[i] = nullptr;
       } else if constexpr (E == Epi::Patch) {
         const int bi = gm / p.tokens, t = gm - bi * p.tokens;
@@ -357,6 +373,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       if constexpr (CONV) {
         cbase[i] = min(n0 + r, p.N - 1) * (int)p.ldw;
         tmask[i] = 0;
+        if (p.cv_tps > 1) {
+          const int q = chunk[i] * 8, ch = q & ((1 << p.cv_cshift) - 1);
+          dtap[i] = q >> p.cv_cshift;
+          boff[i] = (cbase[i] + dtap[i] * p.cv_wseg + ch) * 2;
+          wok[i] = ch < p.cv_Ca;
+        }
       }
     }
   }
@@ -410,24 +432,28 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
     char* base = smem + stage * STAGE;
     if constexpr (CONV) {
       if (p.cv_tps > 1) {
-        // Several taps per step: this lane's chunk belongs to tap t0 + d.
-        const int t0 = kt * p.cv_tps, cmask = (1 << p.cv_cshift) - 1;
+        // Several taps per step: this lane's chunk belongs to tap t0 + dtap.
+        // The host guarantees that every tap offset and every t * kwinv fit
+        // 24 bits, so the tap's pixel offset takes 24-bit multiplies.
+        const int t0 = kt * p.cv_tps;
 #pragma unroll
         for (int i = 0; i < PER_WAVE; ++i) {
           if (i < lo || i >= hi) continue;
-          const int q = chunk[i] * 8, t = t0 + (q >> p.cv_cshift), ch = q & cmask;
-          const bool tap_ok = (t < p.cv_T) & (ch < p.cv_Ca);
-          const int ti = (t * p.cv_kwinv) >> 16, tj = t - ti * p.cv_KW;
+          const int t = t0 + dtap[i];
           if (i < APW) {
-            const bool ok = tap_ok & (bool)((tmask[i] >> (t & 63)) & 1u);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rs_a, (lds_void*)(base + ldsoff[i]), 16,
-                ok ? (unsigned)(cbase[i] + (ti * p.cv_W + tj) * p.cv_Cs + ch) * 2u : kOutOfRange,
-                0, 0, 0);
+            const int ti = (int)(__umul24((unsigned)t, (unsigned)p.cv_kwinv) >> 16);
+            const int tj = t - (int)__umul24((unsigned)ti, (unsigned)p.cv_KW);
+            const int toff = (int)(__umul24((unsigned)ti, (unsigned)p.cv_rowb) +
+                                   __umul24((unsigned)tj, (unsigned)p.cv_pixb));
+            const bool ok = (t < p.cv_T) & (bool)((tmask[i] >> (t & 63)) & 1u);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_a, (lds_void*)(base + ldsoff[i]), 16,
+                                                     ok ? (unsigned)(boff[i] + toff) : kOutOfRange,
+                                                     0, 0, 0);
           } else {
+            const bool ok = (t < p.cv_T) & wok[i];
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rs_w, (lds_void*)(base + ldsoff[i]), 16,
-                tap_ok ? (unsigned)(cbase[i] + t * p.cv_wseg + ch) * 2u : kOutOfRange, 0, 0, 0);
+                ok ? (unsigned)(boff[i] + t0 * p.cv_wseg * 2) : kOutOfRange, 0, 0, 0);
           }
         }
         return;
@@ -575,7 +601,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   // (rstd, -rstd * mean) of the tile's rows into LDS.
   float cs[8];
   float2* rowst = reinterpret_cast<float2*>(smem + SMEM_MAIN);
-  if constexpr (LN_CONSUMER) {
+  if constexpr (LN_CONSUMER && !CONV) {
     if (p.ln_in != nullptr) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) cs[e] = col + e < p.N ? p.ln_colsum[col + e] : 0.0f;
@@ -653,7 +679,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
       if constexpr (LN_CONSUMER) {
         // Pre-activation: acc + bias, or with a folded LayerNorm
         // rstd * acc - rstd * mean * colsum + bias.
-        if (p.ln_in != nullptr) {
+        if (!CONV && p.ln_in != nullptr) {
           const float2 rs = rowst[pass * SR + rl];
 #pragma unroll
           for (int e = 0; e < 8; ++e) v[e] = fmaf(v[e], rs.x, fmaf(rs.y, cs[e], bv[e]));
@@ -1673,8 +1699,11 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
   if (w_bytes > limit || img_bytes > limit) return hipErrorInvalidValue;
   // K steps: Ca > 32 takes ceil(Ca / 64) steps per tap; otherwise taps
   // share a step, each spanning Cp = the next power of two >= Ca.
+  // (Several taps a step need their pixel offsets, ((KH - 1) * W + KW - 1) *
+  // Cs * 2 bytes at most, to fit 24 bits; otherwise one tap a step.)
   int tps = 1, cshift = 0;
-  if (a.Ca <= 32) {
+  const int64_t max_tap_bytes = ((int64_t)(a.KH - 1) * a.W + (a.KW - 1)) * a.Cs * 2;
+  if (a.Ca <= 32 && max_tap_bytes < (1 << 24) && (int64_t)a.W * a.Cs * 2 < (1 << 24)) {
     cshift = a.Ca <= 8 ? 3 : a.Ca <= 16 ? 4 : 5;
     tps = kBK >> cshift;
   }
@@ -1704,6 +1733,7 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
     p.cv_stride = a.stride; p.cv_pad = a.pad; p.cv_Ho = Ho; p.cv_Wo = Wo; p.cv_wseg = (int)a.wseg;
     p.cv_nc = (a.Ca + kBK - 1) / kBK;
     p.cv_tps = tps; p.cv_cshift = cshift; p.cv_kwinv = kwinv; p.cv_ncinv = ncinv;
+    p.cv_rowb = a.W * a.Cs * 2; p.cv_pixb = a.Cs * 2;
     p.a_bytes = (int)(nb * img_bytes);
     p.w_bytes = (int)w_bytes;
     const hipError_t e = launch_epi<Epi::Bias, true>(p, s);
