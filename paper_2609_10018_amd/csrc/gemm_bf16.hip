@@ -276,9 +276,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   constexpr int SMEM_MAIN = STAGES * STAGE > EPI_BYTES ? STAGES * STAGE : EPI_BYTES;
   constexpr bool LN_CONSUMER = E == Epi::Bias || E == Epi::BiasGelu;
   constexpr bool LN_PRODUCER = E == Epi::BiasResid || E == Epi::Patch;
-  // + per-row LN factors (LayerNorm consumers; convolutions never fold one)
-  constexpr int SMEM = SMEM_MAIN + (LN_CONSUMER && !CONV ? BM * 8 : 0);
+  constexpr int SMEM = SMEM_MAIN;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  // Per-row LayerNorm factors of a folded LayerNorm (BM float2): dynamic LDS
+  // that the launch adds only when the GEMM consumes one, so plain GEMMs keep
+  // their occupancy.
+  extern __shared__ __attribute__((aligned(16))) char smem_ln[];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -600,7 +603,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
   // Folded LayerNorm (consumer): column sums of this thread's 8 columns, and
   // (rstd, -rstd * mean) of the tile's rows into LDS.
   float cs[8];
-  float2* rowst = reinterpret_cast<float2*>(smem + SMEM_MAIN);
+  float2* rowst = reinterpret_cast<float2*>(smem_ln);
   if constexpr (LN_CONSUMER && !CONV) {
     if (p.ln_in != nullptr) {
 #pragma unroll
@@ -1383,9 +1386,10 @@ hipError_t launch_cfg(const Params& p0, int row0, hipStream_t s) {
   p.group_m = p.K >= 2048 ? 2 : 4;
   const int64_t blocks = tm * tn;
   if (blocks <= 0) return hipSuccess;
+  const bool ln_consumer = (E == Epi::Bias || E == Epi::BiasGelu) && !CONV && p.ln_in != nullptr;
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, E, CONV, STAGES>),
                      dim3((unsigned)blocks, (unsigned)(p.ksplit > 1 ? p.ksplit : 1)),
-                     dim3(64 * WM * WN), 0, s, p);
+                     dim3(64 * WM * WN), ln_consumer ? BM * 8 : 0, s, p);
   return hipGetLastError();
 }
 
