@@ -63,6 +63,11 @@ int64_t al256(int64_t v) { return (v + 255) / 256 * 256; }
 // Packed stem filter row: 7 kernel rows x (8 pixels x 4 channels).
 constexpr int kStemLdw = 7 * 32;
 
+// The stem and the max pool run as one kernel for 32 or 64 stem channels
+// (launch_stem_pool); other widths take the padded-input convolution and a
+// separate pool.
+static bool stem_pool_fused(const elasto_cnn_config_t& c) { return c.stem == 32 || c.stem == 64; }
+
 bool check_cnn_config(const elasto_cnn_config_t* c) {
   if (!c) { set_error("config is NULL"); return false; }
   if (c->dtype != ELASTO_BF16) { set_error("the CNN path is bf16 only"); return false; }
@@ -263,7 +268,11 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
     t1 = std::max(t1, B * hi * hi * b.width);
     t2 = std::max(t2, B * ho * ho * b.width);
   }
-  const int64_t sz_col = al256(col * 2), sz_stem = al256(B * hs * hs * cfg->stem * 2),
+  // The fused stem + max pool (32 or 64 stem channels) needs neither the
+  // padded NHWC input nor the full-resolution stem output.
+  const bool fused = stem_pool_fused(*cfg);
+  const int64_t sz_col = fused ? 0 : al256(col * 2),
+                sz_stem = fused ? 0 : al256(B * hs * hs * cfg->stem * 2),
                 sz_io = al256(io * 2), sz_t1 = al256(t1 * 2), sz_t2 = al256(t2 * 2),
                 sz_feat = al256(B * F * 2);
   h->sbytes = sz_col + sz_stem + 2 * sz_io + sz_t1 + sz_t2 + sz_feat;
@@ -393,8 +402,13 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
   } while (0)
 
   const int hs = c.img / 2;
-  ELASTO_TRY(launch_pad_nhwc4(images, batch, c.in_chans, c.img, c.img, 3, h->col, s), "stem input");
-  {
+  if (stem_pool_fused(c)) {
+    ELASTO_TRY(launch_stem_pool(images, batch, c.in_chans, c.img, Wp(h->stem_w), kStemLdw,
+                                Fp(h->stem_b), c.stem, h->x, s),
+               "stem + max pool");
+  } else {
+    ELASTO_TRY(launch_pad_nhwc4(images, batch, c.in_chans, c.img, c.img, 3, h->col, s),
+               "stem input");
     ConvArgs a;
     a.x = h->col; a.batch = batch; a.H = c.img + 6; a.W = c.img + 6; a.Cs = 4; a.Ca = 32;
     a.KH = 7; a.KW = 1; a.stride = 2; a.pad = 0; a.row_window = 7;
@@ -404,8 +418,8 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
     a.N = c.stem;
     a.relu = true;
     ELASTO_TRY(launch_conv_bf16(a, s), "stem");
+    ELASTO_TRY(launch_max_pool_3x3_s2(h->stem_out, batch, hs, hs, c.stem, h->x, s), "max pool");
   }
-  ELASTO_TRY(launch_max_pool_3x3_s2(h->stem_out, batch, hs, hs, c.stem, h->x, s), "max pool");
   void* cur = h->x;
   void* other = h->d;
   for (size_t bi = 0; bi < h->blocks.size(); ++bi) {

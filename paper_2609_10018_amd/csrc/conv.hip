@@ -9,6 +9,12 @@
 // * max_pool_3x3_s2: 3x3 window, stride 2, padding 1, NHWC, 8 channels per
 //   thread.
 // * avg_pool: mean over all pixels of each image, fp32 sums, bf16 out.
+// * stem_pool: the stem (7x7 stride-2 convolution + bias + ReLU) and the 3x3
+//   stride-2 max pool in one kernel, reading the NCHW images directly: a
+//   workgroup stages the input patch of an 8x8 block of pooled outputs
+//   (39x40 pixels, 4 channels) and the filters in LDS, computes the 17x17
+//   stem outputs the block's pooling windows cover with MFMAs, rounds them to
+//   bf16 as the separate stem would store them, and pools them in LDS.
 #include "common.h"
 #include "kernels.h"
 
@@ -92,7 +98,151 @@ __global__ __launch_bounds__(256) void avg_pool_kernel(const uint16_t* __restric
   *reinterpret_cast<u32x4*>(y + (int64_t)n * C + c8 * 8) = w;
 }
 
+// Fused stem + max pool (see the file comment).  One workgroup of 10 waves
+// per (image, 8x8 block of pooled outputs).  Stem output (sh, sw) is
+// relu(bias + sum over kernel row i, column j < 7, channel c < 4 of
+// x[c][2sh - 3 + i][2sw - 3 + j] * w[n][i*32 + j*4 + c]) with x zero outside
+// the image (and for c >= C); the packed filter row's 8th column and 4th
+// channel hold zeros.  Pooled output (ph, pw) is the max of the stem outputs
+// (2ph - 1 + di, 2pw - 1 + dj), di, dj < 3, inside the stem output.
+constexpr int kStemPT = 8;                  // pooled outputs per block side
+constexpr int kStemSR = 2 * kStemPT + 1;    // stem outputs per block side (17)
+constexpr int kStemM = kStemSR * kStemSR;   // 289 stem outputs
+constexpr int kStemMB = (kStemM + 31) / 32; // 10 row blocks of 32 (one per wave)
+constexpr int kStemIR = 2 * kStemSR + 5;    // 39 input rows
+constexpr int kStemIC = 2 * kStemSR + 6;    // 40 input columns (incl. the 8th tap column)
+constexpr int kStemK = 7 * 32;              // 224 filter entries
+constexpr int kStemWS = kStemK * 2 + 16;    // LDS row stride of a staged filter (bytes)
+constexpr int kStemThreads = 64 * kStemMB;
+
+template <int N>
+__global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
+    const uint16_t* __restrict__ img, int C, int S, const uint16_t* __restrict__ w, int ldw,
+    const float* __restrict__ bias, uint16_t* __restrict__ out) {
+  static_assert(N % 32 == 0 && N <= 64, "stem channels");
+  constexpr int IN_BYTES = kStemIR * kStemIC * 8;
+  constexpr int W_OFF = (IN_BYTES + 255) / 256 * 256;
+  constexpr int GEMM_BYTES = W_OFF + N * kStemWS;
+  constexpr int POOL_BYTES = kStemM * N * 2;
+  __shared__ __attribute__((aligned(16))) char smem[GEMM_BYTES > POOL_BYTES ? GEMM_BYTES : POOL_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int S2 = S / 2, S4 = S / 4, tiles = S4 / kStemPT;
+  const int b = blockIdx.x / (tiles * tiles), t = blockIdx.x - b * tiles * tiles;
+  const int ph0 = (t / tiles) * kStemPT, pw0 = (t - (t / tiles) * tiles) * kStemPT;
+  const int y0 = 4 * ph0 - 5, x0 = 4 * pw0 - 5;  // image coordinates of the patch origin
+
+  // Filters: N rows of 28 16-byte chunks.
+  for (int q = tid; q < N * (kStemK / 8); q += kStemThreads) {
+    const int n = q / (kStemK / 8), kc = q - n * (kStemK / 8);
+    *reinterpret_cast<u32x4*>(smem + W_OFF + n * kStemWS + kc * 16) =
+        *reinterpret_cast<const u32x4*>(w + (int64_t)n * ldw + kc * 8);
+  }
+  // Input patch, NHWC with 4 channels, zero outside the image.
+  for (int q = tid; q < kStemIR * kStemIC; q += kStemThreads) {
+    const int lr = q / kStemIC, lc = q - lr * kStemIC, y = y0 + lr, x = x0 + lc;
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+    if ((unsigned)y < (unsigned)S && (unsigned)x < (unsigned)S) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (c < C) h[c] = img[(((int64_t)b * C + c) * S + y) * S + x];
+    }
+    *reinterpret_cast<u32x2*>(smem + q * 8) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+  }
+  __syncthreads();
+
+  // D^T = W A^T per 32x32 block: wave = row block of stem outputs; lane l
+  // holds stem output m = 32 wave + l % 32 and channels 8(e/4) + 4(l/32) + e%4.
+  const int lr = lane & 31, lg = lane >> 5;
+  const int m = min(wave * 32 + lr, kStemM - 1);
+  const int r = m / kStemSR, c = m - r * kStemSR;
+  f32x16 acc[N / 32];
+#pragma unroll
+  for (int nb = 0; nb < N / 32; ++nb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[nb][e] = 0.0f;
+#pragma unroll
+  for (int kb = 0; kb < kStemK / 16; ++kb) {
+    const int k8 = kb * 16 + lg * 8, i = k8 >> 5, q = (k8 & 31) >> 3;
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(smem + ((2 * r + i) * kStemIC + 2 * c + 2 * q) * 8);
+#pragma unroll
+    for (int nb = 0; nb < N / 32; ++nb) {
+      const bf16x8 wf = *reinterpret_cast<const bf16x8*>(smem + W_OFF + (nb * 32 + lr) * kStemWS + k8 * 2);
+      acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, a, acc[nb], 0, 0, 0);
+    }
+  }
+  __syncthreads();  // every wave is done with the staged patch and filters
+
+  // bias + ReLU, rounded to bf16; stem outputs outside the image hold 0
+  // (a pooling window always has an output inside, and every output >= 0).
+  const int mo = wave * 32 + lr;
+  const int sh = 2 * ph0 - 1 + r, sw = 2 * pw0 - 1 + c;
+  const bool inside = (unsigned)sh < (unsigned)S2 && (unsigned)sw < (unsigned)S2;
+  if (mo < kStemM) {
+#pragma unroll
+    for (int nb = 0; nb < N / 32; ++nb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n0 = nb * 32 + 8 * g + 4 * lg;
+        uint32_t h[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          h[e] = inside ? f32_to_bf16(fmaxf(acc[nb][4 * g + e] + bias[n0 + e], 0.0f)) : 0u;
+        *reinterpret_cast<u32x2*>(smem + (mo * N + n0) * 2) =
+            u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+      }
+  }
+  __syncthreads();
+
+  // Pool: one thread per (pooled output, 8 channels).
+  constexpr int C8 = N / 8;
+  if (tid < kStemPT * kStemPT * C8) {
+    const int pix = tid / C8, c8 = tid - pix * C8;
+    const int pr = pix / kStemPT, pc = pix - pr * kStemPT;
+    float mx[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) mx[e] = 0.0f;
+#pragma unroll
+    for (int di = 0; di < 3; ++di)
+#pragma unroll
+      for (int dj = 0; dj < 3; ++dj) {
+        const int sm = (2 * pr + di) * kStemSR + 2 * pc + dj;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(smem + (sm * N + c8 * 8) * 2);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          mx[e] = fmaxf(mx[e], __uint_as_float((e & 1) ? (v[e >> 1] & 0xffff0000u)
+                                                        : (v[e >> 1] << 16)));
+      }
+    u32x4 o;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      o[h] = (uint32_t)f32_to_bf16(mx[2 * h]) | ((uint32_t)f32_to_bf16(mx[2 * h + 1]) << 16);
+    const int ph = ph0 + pr, pw = pw0 + pc;
+    *reinterpret_cast<u32x4*>(out + ((((int64_t)b * S4 + ph) * S4 + pw) * N + c8 * 8)) = o;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_stem_pool(const void* img, int batch, int C, int S, const void* w, int ldw,
+                            const float* bias, int N, void* out, hipStream_t s) {
+  if (C < 1 || C > 4 || S < 32 || S % 32 != 0 || (N != 32 && N != 64) || ldw < kStemK ||
+      ldw % 8 != 0)
+    return hipErrorInvalidValue;
+  if (batch <= 0) return hipSuccess;
+  const int tiles = S / 4 / kStemPT;
+  const int64_t blocks = (int64_t)batch * tiles * tiles;
+  if (blocks > INT32_MAX) return hipErrorInvalidValue;
+  if (N == 64)
+    hipLaunchKernelGGL(stem_pool_kernel<64>, dim3((unsigned)blocks), dim3(kStemThreads), 0, s,
+                       static_cast<const uint16_t*>(img), C, S, static_cast<const uint16_t*>(w),
+                       ldw, bias, static_cast<uint16_t*>(out));
+  else
+    hipLaunchKernelGGL(stem_pool_kernel<32>, dim3((unsigned)blocks), dim3(kStemThreads), 0, s,
+                       static_cast<const uint16_t*>(img), C, S, static_cast<const uint16_t*>(w),
+                       ldw, bias, static_cast<uint16_t*>(out));
+  return hipGetLastError();
+}
 
 hipError_t launch_pad_nhwc4(const void* img, int batch, int C, int H, int W, int pad, void* out,
                             hipStream_t s) {

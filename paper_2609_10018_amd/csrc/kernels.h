@@ -202,6 +202,13 @@ constexpr int kAttnMaxTokens = 240;
 // Elastic bottleneck-ResNet data movement (conv.hip).  NHWC bf16.
 hipError_t launch_pad_nhwc4(const void* img, int batch, int C, int H, int W, int pad, void* out,
                             hipStream_t s);
+// Stem + max pool of the bottleneck ResNet in one launch: NCHW bf16 images
+// (C <= 4 channels, S x S, S % 32 == 0), packed stem filters [N][ldw] bf16
+// (kernel row i, column j < 8, channel c < 4 at i*32 + j*4 + c; column 7
+// and channels >= C zero), fp32 bias, out NHWC [batch][S/4][S/4][N] bf16.
+// N is 32 or 64.
+hipError_t launch_stem_pool(const void* img, int batch, int C, int S, const void* w, int ldw,
+                            const float* bias, int N, void* out, hipStream_t s);
 hipError_t launch_max_pool_3x3_s2(const void* x, int batch, int H, int W, int C, void* y,
                                   hipStream_t s);
 hipError_t launch_avg_pool(const void* x, int batch, int HW, int C, void* y, hipStream_t s);

@@ -180,6 +180,10 @@ hipError_t launch_max_pool_3x3_s2(const void*, int, int, int, int, void*, hipStr
   return launch();
 }
 hipError_t launch_avg_pool(const void*, int, int, int, void*, hipStream_t) { return launch(); }
+hipError_t launch_stem_pool(const void*, int, int, int, const void*, int, const float*, int, void*,
+                            hipStream_t) {
+  return launch();
+}
 
 hipError_t static_scratch(void** ptr, int64_t* bytes) {
   tick();
