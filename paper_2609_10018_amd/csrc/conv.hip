@@ -21,6 +21,23 @@
 namespace elasto {
 namespace {
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef int16_t i16x2 __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+
+// Two bf16 values packed in a 32-bit word.  Per 16-bit half: max with 0 as a
+// signed integer (zero for a set sign bit), and max as an unsigned integer
+// (the float max for non-negative values).
+__device__ __forceinline__ uint32_t pk_relu_bf16(uint32_t a) {
+  return __builtin_bit_cast(uint32_t,
+                            __builtin_elementwise_max(__builtin_bit_cast(i16x2, a), (i16x2){0, 0}));
+}
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
+                                                                __builtin_bit_cast(u16x2, b)));
+}
+
 inline unsigned grid_for(int64_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
 // One thread per padded output pixel: 4 channels (8 bytes), zero in the
@@ -115,6 +132,14 @@ constexpr int kStemK = 7 * 32;              // 224 filter entries
 constexpr int kStemWS = kStemK * 2 + 16;    // LDS row stride of a staged filter (bytes)
 constexpr int kStemThreads = 64 * kStemMB;
 
+// Byte offset of stem output m, channel n in the block's LDS copy: rows of N
+// bf16, their 16-byte units permuted by (m mod 8) so that the 32 rows a
+// wave's epilogue writes at once spread over the banks.
+template <int N>
+__device__ __forceinline__ int stem_slot(int m, int n) {
+  return m * (N * 2) + ((((n >> 3) ^ m) & (N / 8 - 1)) << 4) + (n & 7) * 2;
+}
+
 template <int N>
 __global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
     const uint16_t* __restrict__ img, int C, int S, const uint16_t* __restrict__ w, int ldw,
@@ -138,16 +163,31 @@ __global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
     *reinterpret_cast<u32x4*>(smem + W_OFF + n * kStemWS + kc * 16) =
         *reinterpret_cast<const u32x4*>(w + (int64_t)n * ldw + kc * 8);
   }
-  // Input patch, NHWC with 4 channels, zero outside the image.
-  for (int q = tid; q < kStemIR * kStemIC; q += kStemThreads) {
-    const int lr = q / kStemIC, lc = q - lr * kStemIC, y = y0 + lr, x = x0 + lc;
-    uint32_t h[4] = {0u, 0u, 0u, 0u};
-    if ((unsigned)y < (unsigned)S && (unsigned)x < (unsigned)S) {
+  // Input patch, NHWC with 4 channels, zero outside the image: every load of
+  // the thread's pixels is issued before the first LDS store.
+  {
+    constexpr int kIn = kStemIR * kStemIC, kSlots = (kIn + kStemThreads - 1) / kStemThreads;
+    const uint16_t* const ib = img + (int64_t)b * C * S * S;
+    uint32_t h[kSlots][4];
+#pragma unroll
+    for (int sl = 0; sl < kSlots; ++sl) {
+      const int q = tid + sl * kStemThreads;
+      const int lr = q / kStemIC, lc = q - lr * kStemIC, y = y0 + lr, x = x0 + lc;
+      const bool ok = q < kIn && (unsigned)y < (unsigned)S && (unsigned)x < (unsigned)S;
+      const uint32_t off = (uint32_t)(y * S + x) * 2u;  // bytes within a channel plane
 #pragma unroll
       for (int c = 0; c < 4; ++c)
-        if (c < C) h[c] = img[(((int64_t)b * C + c) * S + y) * S + x];
+        h[sl][c] = (ok && c < C) ? (uint32_t)*reinterpret_cast<const uint16_t*>(
+                                       reinterpret_cast<const char*>(ib + (int64_t)c * S * S) + off)
+                                 : 0u;
     }
-    *reinterpret_cast<u32x2*>(smem + q * 8) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+#pragma unroll
+    for (int sl = 0; sl < kSlots; ++sl) {
+      const int q = tid + sl * kStemThreads;
+      if (q < kIn)
+        *reinterpret_cast<u32x2*>(smem + q * 8) =
+            u32x2{h[sl][0] | (h[sl][1] << 16), h[sl][2] | (h[sl][3] << 16)};
+    }
   }
   __syncthreads();
 
@@ -173,8 +213,11 @@ __global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
   }
   __syncthreads();  // every wave is done with the staged patch and filters
 
-  // bias + ReLU, rounded to bf16; stem outputs outside the image hold 0
-  // (a pooling window always has an output inside, and every output >= 0).
+  // bias, rounded to bf16, then ReLU on the bf16 bits (a negative value's
+  // sign bit makes it negative as a 16-bit integer; the same result as
+  // rounding max(v, 0) for every finite v); stem outputs outside the image
+  // hold 0 (a pooling window always has an output inside, and every output
+  // is >= 0).
   const int mo = wave * 32 + lr;
   const int sh = 2 * ph0 - 1 + r, sw = 2 * pw0 - 1 + c;
   const bool inside = (unsigned)sh < (unsigned)S2 && (unsigned)sw < (unsigned)S2;
@@ -184,39 +227,36 @@ __global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int n0 = nb * 32 + 8 * g + 4 * lg;
-        uint32_t h[4];
+        const f32x4 bz = *reinterpret_cast<const f32x4*>(bias + n0);
+        uint32_t h[2];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          h[e] = inside ? f32_to_bf16(fmaxf(acc[nb][4 * g + e] + bias[n0 + e], 0.0f)) : 0u;
-        *reinterpret_cast<u32x2*>(smem + (mo * N + n0) * 2) =
-            u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        for (int e = 0; e < 2; ++e) {
+          const bf16x2 v = __builtin_convertvector(
+              (f32x2){acc[nb][4 * g + 2 * e] + bz[2 * e], acc[nb][4 * g + 2 * e + 1] + bz[2 * e + 1]},
+              bf16x2);
+          h[e] = inside ? pk_relu_bf16(__builtin_bit_cast(uint32_t, v)) : 0u;
+        }
+        *reinterpret_cast<u32x2*>(smem + stem_slot<N>(mo, n0)) = u32x2{h[0], h[1]};
       }
   }
   __syncthreads();
 
-  // Pool: one thread per (pooled output, 8 channels).
+  // Pool: one thread per (pooled output, 8 channels).  The stem outputs are
+  // non-negative bf16, ordered as 16-bit unsigned integers.
   constexpr int C8 = N / 8;
   if (tid < kStemPT * kStemPT * C8) {
     const int pix = tid / C8, c8 = tid - pix * C8;
     const int pr = pix / kStemPT, pc = pix - pr * kStemPT;
-    float mx[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) mx[e] = 0.0f;
+    u32x4 o = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int di = 0; di < 3; ++di)
 #pragma unroll
       for (int dj = 0; dj < 3; ++dj) {
         const int sm = (2 * pr + di) * kStemSR + 2 * pc + dj;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(smem + (sm * N + c8 * 8) * 2);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(smem + stem_slot<N>(sm, c8 * 8));
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          mx[e] = fmaxf(mx[e], __uint_as_float((e & 1) ? (v[e >> 1] & 0xffff0000u)
-                                                        : (v[e >> 1] << 16)));
+        for (int h = 0; h < 4; ++h) o[h] = pk_max_u16(o[h], v[h]);
       }
-    u32x4 o;
-#pragma unroll
-    for (int h = 0; h < 4; ++h)
-      o[h] = (uint32_t)f32_to_bf16(mx[2 * h]) | ((uint32_t)f32_to_bf16(mx[2 * h + 1]) << 16);
     const int ph = ph0 + pr, pw = pw0 + pc;
     *reinterpret_cast<u32x4*>(out + ((((int64_t)b * S4 + ph) * S4 + pw) * N + c8 * 8)) = o;
   }
@@ -227,7 +267,7 @@ __global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
 hipError_t launch_stem_pool(const void* img, int batch, int C, int S, const void* w, int ldw,
                             const float* bias, int N, void* out, hipStream_t s) {
   if (C < 1 || C > 4 || S < 32 || S % 32 != 0 || (N != 32 && N != 64) || ldw < kStemK ||
-      ldw % 8 != 0)
+      ldw % 8 != 0 || reinterpret_cast<uintptr_t>(bias) % 16 != 0)
     return hipErrorInvalidValue;
   if (batch <= 0) return hipSuccess;
   const int tiles = S / 4 / kStemPT;
