@@ -189,8 +189,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     const int q = q0 + lq;
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
-      const u32x2 w = {(uint32_t)f32_to_bf16(o[n][0] * inv) | ((uint32_t)f32_to_bf16(o[n][1] * inv) << 16),
-                       (uint32_t)f32_to_bf16(o[n][2] * inv) | ((uint32_t)f32_to_bf16(o[n][3] * inv) << 16)};
+      const u32x2 w = {pack_bf16x2(o[n][0] * inv, o[n][1] * inv),
+                       pack_bf16x2(o[n][2] * inv, o[n][3] * inv)};
       __builtin_amdgcn_raw_buffer_store_b64(w, ro, q < T ? (q * (int)p.os + 16 * n + 4 * lg) * 2 : nrec,
                                             0, 0);
     }

@@ -21,8 +21,6 @@
 namespace elasto {
 namespace {
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef int16_t i16x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
@@ -88,7 +86,7 @@ __global__ __launch_bounds__(256) void max_pool_kernel(const uint16_t* __restric
   u32x4 w;
 #pragma unroll
   for (int h = 0; h < 4; ++h)
-    w[h] = (uint32_t)f32_to_bf16(mx[2 * h]) | ((uint32_t)f32_to_bf16(mx[2 * h + 1]) << 16);
+    w[h] = pack_bf16x2(mx[2 * h], mx[2 * h + 1]);
   *reinterpret_cast<u32x4*>(y + m * (int64_t)C + c8 * 8) = w;
 }
 
@@ -111,7 +109,7 @@ __global__ __launch_bounds__(256) void avg_pool_kernel(const uint16_t* __restric
   u32x4 w;
 #pragma unroll
   for (int h = 0; h < 4; ++h)
-    w[h] = (uint32_t)f32_to_bf16(s[2 * h] * inv) | ((uint32_t)f32_to_bf16(s[2 * h + 1] * inv) << 16);
+    w[h] = pack_bf16x2(s[2 * h] * inv, s[2 * h + 1] * inv);
   *reinterpret_cast<u32x4*>(y + (int64_t)n * C + c8 * 8) = w;
 }
 
@@ -231,10 +229,9 @@ __global__ __launch_bounds__(kStemThreads) void stem_pool_kernel(
         uint32_t h[2];
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-          const bf16x2 v = __builtin_convertvector(
-              (f32x2){acc[nb][4 * g + 2 * e] + bz[2 * e], acc[nb][4 * g + 2 * e + 1] + bz[2 * e + 1]},
-              bf16x2);
-          h[e] = inside ? pk_relu_bf16(__builtin_bit_cast(uint32_t, v)) : 0u;
+          const uint32_t v =
+              pack_bf16x2(acc[nb][4 * g + 2 * e] + bz[2 * e], acc[nb][4 * g + 2 * e + 1] + bz[2 * e + 1]);
+          h[e] = inside ? pk_relu_bf16(v) : 0u;
         }
         *reinterpret_cast<u32x2*>(smem + stem_slot<N>(mo, n0)) = u32x2{h[0], h[1]};
       }

@@ -230,7 +230,7 @@ __device__ __forceinline__ void store_bf16x8(uint16_t* cp, const float* v, bool 
     u32x4 w;
 #pragma unroll
     for (int h = 0; h < 4; ++h)
-      w[h] = (uint32_t)f32_to_bf16(v[2 * h]) | ((uint32_t)f32_to_bf16(v[2 * h + 1]) << 16);
+      w[h] = pack_bf16x2(v[2 * h], v[2 * h + 1]);
     *reinterpret_cast<u32x4*>(cp) = w;
   } else {
 #pragma unroll
@@ -1169,7 +1169,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
             u32x4 w;
 #pragma unroll
             for (int q2 = 0; q2 < 4; ++q2)
-              w[q2] = (uint32_t)f32_to_bf16(v[2 * q2]) | ((uint32_t)f32_to_bf16(v[2 * q2 + 1]) << 16);
+              w[q2] = pack_bf16x2(v[2 * q2], v[2 * q2 + 1]);
             const bool st = ok && (!cls || p.ln_out != nullptr);
             __builtin_amdgcn_raw_buffer_store_b128(
                 w, rc, st ? ((row - m0) * (int)p.ldc + col) * 2 : nrec, 0, 0);
@@ -1218,8 +1218,8 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
               if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
             }
             u32x2 w;
-            w[0] = (uint32_t)f32_to_bf16(t[0]) | ((uint32_t)f32_to_bf16(t[1]) << 16);
-            w[1] = (uint32_t)f32_to_bf16(t[2]) | ((uint32_t)f32_to_bf16(t[3]) << 16);
+            w[0] = pack_bf16x2(t[0], t[1]);
+            w[1] = pack_bf16x2(t[2], t[3]);
             *reinterpret_cast<u32x2*>(slot + wo + g * 16) = w;
           }
           wait_lds();

@@ -100,10 +100,8 @@ __global__ __launch_bounds__(256) void layernorm_bf16_kernel(const uint16_t* __r
       u32x4 w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint16_t lo = f32_to_bf16((v[i][2 * e] - mean) * rstd * gv[2 * e] + bv[2 * e]);
-        const uint16_t hi =
-            f32_to_bf16((v[i][2 * e + 1] - mean) * rstd * gv[2 * e + 1] + bv[2 * e + 1]);
-        w[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+        w[e] = pack_bf16x2((v[i][2 * e] - mean) * rstd * gv[2 * e] + bv[2 * e],
+                           (v[i][2 * e + 1] - mean) * rstd * gv[2 * e + 1] + bv[2 * e + 1]);
       }
       *reinterpret_cast<u32x4*>(orow + 8 * ci) = w;
     }
