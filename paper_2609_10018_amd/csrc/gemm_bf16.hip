@@ -140,6 +140,20 @@ __device__ __forceinline__ void ln_merge_dpp(LnStat& a) {
   ln_merge(a, nb, mb, m2b);
 }
 
+// The same update for two sets of equal size (n_b = n_a, a power of two):
+// d n_b / n = d / 2 and n_a n_b / n = n_a / 2, with no reciprocal.
+__device__ __forceinline__ void ln_merge_equal(LnStat& a, float mb, float m2b) {
+  const float d = mb - a.mean;
+  a.mean = fmaf(d, 0.5f, a.mean);
+  a.m2 += fmaf(d * d, a.n * 0.5f, m2b);
+  a.n += a.n;
+}
+template <int CTRL>
+__device__ __forceinline__ void ln_merge_dpp_equal(LnStat& a) {
+  ln_merge_equal(a, dpp_f<CTRL>(a.mean), dpp_f<CTRL>(a.m2));
+}
+
+
 // Statistics of 8 values (all of them valid, or none).
 __device__ __forceinline__ LnStat ln_of8(const float* v, bool valid) {
   LnStat s{0.0f, 0.0f, 0.0f};
@@ -154,6 +168,23 @@ __device__ __forceinline__ LnStat ln_of8(const float* v, bool valid) {
     s = LnStat{8.0f, m, q};
   }
   return s;
+}
+
+// Segment statistics from the 8-value chunks held by the 8 lanes of an
+// aligned group.  When N is a multiple of 64 the chunks of a segment inside
+// [0, N) are all whole, so the three merges are of equal sizes.
+__device__ __forceinline__ LnStat ln_of_group8(const float* v, bool valid, bool whole_segments) {
+  LnStat ls = ln_of8(v, valid);
+  if (whole_segments) {
+    ln_merge_dpp_equal<kDppXor1>(ls);
+    ln_merge_dpp_equal<kDppXor2>(ls);
+    ln_merge_dpp_equal<kDppHalfMirror>(ls);
+  } else {
+    ln_merge_dpp<kDppXor1>(ls);
+    ln_merge_dpp<kDppXor2>(ls);
+    ln_merge_dpp<kDppHalfMirror>(ls);
+  }
+  return ls;
 }
 
 // Merges, in segment order, the segments of a row (stored row-major: segment j
@@ -786,10 +817,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
           // Statistics of each 64-column segment: the 8 lanes of an aligned
           // group hold its 8 chunks (N % 8 == 0, so a chunk is whole or
           // absent); three DPP merges give every lane the group's total.
-          LnStat ls = ln_of8(st, st_ok);
-          ln_merge_dpp<kDppXor1>(ls);
-          ln_merge_dpp<kDppXor2>(ls);
-          ln_merge_dpp<kDppHalfMirror>(ls);
+          const LnStat ls = ln_of_group8(st, st_ok, (p.N & 63) == 0);
           const int seg = (n0 >> 6) + (cc >> 3);
           if ((cc & 7) == 0 && 64 * seg < p.N)
             p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(ls.n * ls.mean, ls.m2);
@@ -1131,7 +1159,12 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         if (i + 1 < TM) load_res(i + 1, rz[(i + 1) & 1]);
         const int row = row_l0 + i * 32;
         const bool row_ok = row < p.M, cls = i == cls_i;
-        LnStat ls{0.0f, 0.0f, 0.0f};
+        // Statistics of the lane's four chunks of the segment: pairwise
+        // merges of equal sizes when N is a multiple of 64 (every chunk of a
+        // segment inside [0, N) whole), else one at a time.
+        static_assert(TN == 2, "segment = two 32-column blocks");
+        const bool whole = (p.N & 63) == 0;
+        LnStat ls{0.0f, 0.0f, 0.0f}, lj{0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -1174,11 +1207,26 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
             __builtin_amdgcn_raw_buffer_store_b128(
                 w, rc, st ? ((row - m0) * (int)p.ldc + col) * 2 : nrec, 0, 0);
             const LnStat l8 = ln_of8(v, ok);
-            ln_merge(ls, l8.n, l8.mean, l8.m2);
+            if (whole) {
+              if (h == 0) {
+                lj = l8;
+              } else {
+                ln_merge_equal(lj, l8.mean, l8.m2);
+                if (j == 0)
+                  ls = lj;
+                else
+                  ln_merge_equal(ls, lj.mean, lj.m2);
+              }
+            } else {
+              ln_merge(ls, l8.n, l8.mean, l8.m2);
+            }
             wait_lds();  // the slot is rewritten by the next pass
           }
         if (p.ln_out != nullptr) {  // this row's 64-column segment: lanes l and l ^ 1
-          ln_merge_dpp<kDppXor1>(ls);
+          if (whole)
+            ln_merge_dpp_equal<kDppXor1>(ls);
+          else
+            ln_merge_dpp<kDppXor1>(ls);
           if ((lane & 1) == 0 && row_ok && 64 * seg < p.N)
             p.ln_out[(int64_t)row * p.ln_ld + seg] = make_float2(ls.n * ls.mean, ls.m2);
         }
@@ -1364,10 +1412,7 @@ __global__ __launch_bounds__(64) void splitk_epilogue_kernel(SplitEpi q) {
       st_ok = true;
     }
     if (q.ln_out != nullptr) {
-      LnStat ls = ln_of8(st, st_ok);
-      ln_merge_dpp<kDppXor1>(ls);
-      ln_merge_dpp<kDppXor2>(ls);
-      ln_merge_dpp<kDppHalfMirror>(ls);
+      const LnStat ls = ln_of_group8(st, st_ok, (q.N & 63) == 0);
       const int seg = cc >> 3;
       if ((cc & 7) == 0 && 64 * seg < q.N)
         q.ln_out[(int64_t)row * q.ln_ld + seg] = make_float2(ls.n * ls.mean, ls.m2);
