@@ -16,6 +16,14 @@
 //     1x1 expand: GEMM over t2, K = n, + shortcut, ReLU, in place into the
 //          shortcut buffer (which becomes cur)
 //   global average pool -> classifier GEMM (fp32 logits)
+//
+// Tile plans: at create, for batches of max_batch >= kTuneMinBatch, every
+// convolution and GEMM of the forward of every mode (a "site") is timed once
+// with each tile plan that can run it (kernels.h, kTilePlans) and keeps the
+// fastest, or the planner's own choice unless another plan is at least 3%
+// faster.  None of these GEMMs has LayerNorm work, so every plan gives
+// bit-identical outputs: the choice changes the speed only.  Forwards of
+// more than half of max_batch images use the plans; smaller ones the planner.
 #include <hip/hip_runtime.h>
 #include <string.h>
 
@@ -38,6 +46,40 @@ struct BlockSpec {
 struct BlockOff {
   int64_t c1w, c1b, c2w, c2b, c3w, c3b, dnw, dnb;
 };
+
+constexpr int kTuneMinBatch = 32;  // smaller max_batch: no tuning
+constexpr int kTuneReps = 3;       // timed launches per plan (the fastest counts)
+
+// Times `launch(plan)` for every tile plan at one site and stores the choice
+// in `plan` (see the file comment).  launch returns hipErrorNotSupported for
+// a plan that cannot run the site's arguments.
+template <class F>
+hipError_t tune_site(F&& launch, uint8_t& plan, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  float t0 = 0.0f, best_t = 0.0f;
+  int best = 0;
+  for (int c = 0; c < kTilePlans; ++c) {
+    hipError_t e = launch(c);  // also the warm-up
+    if (e == hipErrorNotSupported) continue;
+    if (e != hipSuccess) return e;
+    float t = 0.0f;
+    for (int r = 0; r < kTuneReps; ++r) {
+      if ((e = hipEventRecord(e0, s)) != hipSuccess || (e = launch(c)) != hipSuccess ||
+          (e = hipEventRecord(e1, s)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess)
+        return e;
+      float ms = 0.0f;
+      if ((e = hipEventElapsedTime(&ms, e0, e1)) != hipSuccess) return e;
+      t = r == 0 ? ms : std::min(t, ms);
+    }
+    if (c == 0) {
+      t0 = best_t = t;
+    } else if (t < best_t) {
+      best_t = t;
+      best = c;
+    }
+  }
+  plan = (uint8_t)(best != 0 && best_t < 0.97f * t0 ? best : 0);
+  return hipSuccess;
+}
 
 std::vector<BlockSpec> block_specs(const elasto_cnn_config_t& c) {
   std::vector<BlockSpec> out;
@@ -135,7 +177,17 @@ struct elasto_cnn_s {
   std::vector<BlockOff> boff;
   void *col = nullptr, *stem_out = nullptr, *x = nullptr, *d = nullptr, *t1 = nullptr,
        *t2 = nullptr, *feat = nullptr;
+  int64_t sz_io = 0, sz_t1 = 0;
+  // Tile plan per (mode, site), sites in forward order: per block reduce,
+  // 3x3, projection (if any), expand; then the classifier.  Empty: none.
+  int nsites = 0;
+  std::vector<uint8_t> plans;
 };
+
+namespace {
+elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float* logits,
+                        hipStream_t s, hipEvent_t tune0, hipEvent_t tune1);
+}
 
 extern "C" {
 
@@ -297,6 +349,41 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
   h->t1 = p; p += sz_t1;
   h->t2 = p; p += sz_t2;
   h->feat = p;
+  h->sz_io = sz_io;
+  h->sz_t1 = sz_t1;
+  h->nsites = 1;
+  for (const BlockSpec& b : bs) h->nsites += b.down ? 4 : 3;
+
+  // Tile plans (file comment): the tuning forwards read their images from
+  // the projection buffer d (overwritten only after the stem has read them)
+  // and write their logits to t1 (free by then); their values do not matter.
+  if (B >= kTuneMinBatch && B * C * cfg->img * cfg->img * 2 <= sz_io &&
+      B * cfg->num_classes * 4 <= sz_t1) {
+    elasto_status_t st = ELASTO_OK;
+    try {
+      h->plans.assign((size_t)h->num_modes * h->nsites, 0);
+    } catch (...) {
+      st = fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (st == ELASTO_OK && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
+      st = fail(ELASTO_ERR_HIP, "cnn create: cannot create events");
+    for (int m = 0; st == ELASTO_OK && m < h->num_modes; ++m) {
+      h->mode = m;
+      st = cnn_run(h, h->d, (int32_t)B, static_cast<float*>(h->t1), nullptr, e0, e1);
+    }
+    if (st == ELASTO_OK && hipDeviceSynchronize() != hipSuccess)
+      st = fail(ELASTO_ERR_HIP, "cnn create: tuning forward failed");
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    h->mode = 0;
+    if (st != ELASTO_OK) {
+      (void)hipFree(h->dw);
+      (void)hipFree(h->ds);
+      delete h;
+      return st;
+    }
+  }
   *out = h;
   clear_error();
   return ELASTO_OK;
@@ -364,14 +451,23 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
   if (hipGetDevice(&cur_dev) != hipSuccess || cur_dev != h->device) {
     if (hipSetDevice(h->device) != hipSuccess) return fail(ELASTO_ERR_HIP, "cannot select device %d", h->device);
   }
-  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  return cnn_run(h, images, batch, logits, static_cast<hipStream_t>(hip_stream), nullptr, nullptr);
+}
+
+}  // extern "C"
+
+namespace {
+// One forward (the file comment); tuning forwards (tune0 != nullptr) time
+// every tile plan at each site and record the choices.
+elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float* logits,
+                        hipStream_t s, hipEvent_t tune0, hipEvent_t tune1) {
   const elasto_cnn_config_t& c = h->cfg;
   const int k = h->mode;
   const int64_t B = batch;
   auto Wp = [&](int64_t o) { return static_cast<const void*>(h->dw + o); };
   auto Fp = [&](int64_t o) { return reinterpret_cast<const float*>(h->dw + o); };
   auto gemm = [&](Epi epi, const void* A, int64_t lda, int64_t wo, int64_t ldw, void* C, int64_t ldc,
-                  int64_t bo, int64_t M, int N, int K, bool relu) {
+                  int64_t bo, int64_t M, int N, int K, bool relu, int plan) {
     GemmArgs a;
     a.A = A; a.lda = lda;
     a.W = Wp(wo); a.ldw = ldw;
@@ -379,11 +475,13 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
     a.bias = Fp(bo);
     a.M = M; a.N = N; a.K = K;
     a.relu = relu;
+    a.plan = plan;
     return launch_gemm_bf16(epi, a, s);
   };
   // Square input (hw x hw, channel stride cs, first ca channels), ks x ks taps.
   auto conv = [&](const void* x, int hw, int cs, int ca, int ks, int stride, int pad, int64_t wo,
-                  int64_t ldw, int64_t wseg, void* C, int64_t ldc, int64_t bo, int N, bool relu) {
+                  int64_t ldw, int64_t wseg, void* C, int64_t ldc, int64_t bo, int N, bool relu,
+                  int plan) {
     ConvArgs a;
     a.x = x; a.batch = batch; a.H = hw; a.W = hw; a.Cs = cs; a.Ca = ca;
     a.KH = ks; a.KW = ks; a.stride = stride; a.pad = pad;
@@ -392,7 +490,18 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
     a.bias = Fp(bo);
     a.N = N;
     a.relu = relu;
+    a.plan = plan;
     return launch_conv_bf16(a, s);
+  };
+  // Site: launch(plan) with this forward's plan for the next site, or (tuning
+  // forwards) every plan, timed.
+  const bool tune = tune0 != nullptr;
+  const bool use_plans = !h->plans.empty() && 2 * (int64_t)batch > c.max_batch;
+  int site = 0;
+  auto at_site = [&](auto&& launch) -> hipError_t {
+    const size_t i = (size_t)k * h->nsites + site++;
+    if (tune) return tune_site(launch, h->plans[i], s, tune0, tune1);
+    return launch(use_plans ? (int)h->plans[i] : 0);
   };
   hipError_t e;
 #define ELASTO_TRY(call, what)                                                       \
@@ -428,22 +537,29 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
     const int n = h->n_width[(size_t)k * h->blocks.size() + bi];
     const int hi = b.hw_in, ho = b.hw_in / b.stride;
     const int64_t mi = B * hi * hi, mo = B * ho * ho;
-    ELASTO_TRY(gemm(Epi::Bias, cur, b.c_in, o.c1w, b.c_in, h->t1, b.width, o.c1b, mi, n, b.c_in, true),
-               "1x1 reduce");
-    ELASTO_TRY(conv(h->t1, hi, b.width, n, 3, b.stride, 1, o.c2w, 9 * b.width, b.width, h->t2,
-                    b.width, o.c2b, n, true), "3x3");
+    ELASTO_TRY(at_site([&](int pl) {
+                 return gemm(Epi::Bias, cur, b.c_in, o.c1w, b.c_in, h->t1, b.width, o.c1b, mi, n,
+                             b.c_in, true, pl);
+               }), "1x1 reduce");
+    ELASTO_TRY(at_site([&](int pl) {
+                 return conv(h->t1, hi, b.width, n, 3, b.stride, 1, o.c2w, 9 * b.width, b.width,
+                             h->t2, b.width, o.c2b, n, true, pl);
+               }), "3x3");
     void* shortcut = cur;
     if (b.down) {
-      if (b.stride > 1)
-        ELASTO_TRY(conv(cur, hi, b.c_in, b.c_in, 1, b.stride, 0, o.dnw, b.c_in, b.c_in, other,
-                        b.c_out, o.dnb, b.c_out, false), "projection");
-      else
-        ELASTO_TRY(gemm(Epi::Bias, cur, b.c_in, o.dnw, b.c_in, other, b.c_out, o.dnb, mo, b.c_out,
-                        b.c_in, false), "projection");
+      ELASTO_TRY(at_site([&](int pl) {
+                   return b.stride > 1
+                              ? conv(cur, hi, b.c_in, b.c_in, 1, b.stride, 0, o.dnw, b.c_in, b.c_in,
+                                     other, b.c_out, o.dnb, b.c_out, false, pl)
+                              : gemm(Epi::Bias, cur, b.c_in, o.dnw, b.c_in, other, b.c_out, o.dnb,
+                                     mo, b.c_out, b.c_in, false, pl);
+                 }), "projection");
       shortcut = other;
     }
-    ELASTO_TRY(gemm(Epi::BiasResid, h->t2, b.width, o.c3w, b.width, shortcut, b.c_out, o.c3b, mo,
-                    b.c_out, n, true), "1x1 expand");
+    ELASTO_TRY(at_site([&](int pl) {
+                 return gemm(Epi::BiasResid, h->t2, b.width, o.c3w, b.width, shortcut, b.c_out,
+                             o.c3b, mo, b.c_out, n, true, pl);
+               }), "1x1 expand");
     if (b.down) {
       other = cur;
       cur = shortcut;
@@ -452,10 +568,11 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
   const BlockSpec& last = h->blocks.back();
   const int hf = last.hw_in / last.stride;
   ELASTO_TRY(launch_avg_pool(cur, batch, hf * hf, last.c_out, h->feat, s), "average pool");
-  ELASTO_TRY(gemm(Epi::BiasF32, h->feat, last.c_out, h->fc_w, last.c_out, logits, c.num_classes,
-                  h->fc_b, B, c.num_classes, last.c_out, false), "classifier");
+  ELASTO_TRY(at_site([&](int pl) {
+               return gemm(Epi::BiasF32, h->feat, last.c_out, h->fc_w, last.c_out, logits,
+                           c.num_classes, h->fc_b, B, c.num_classes, last.c_out, false, pl);
+             }), "classifier");
 #undef ELASTO_TRY
   return ELASTO_OK;
 }
-
-}  // extern "C"
+}  // namespace

@@ -71,6 +71,7 @@ struct Params {
   int tiles_n;
   int group_m;  // row panels per rasterisation group
   int relu;     // Bias / BiasResid: clamp the bf16 result at 0 (convolution blocks)
+  int plan;     // forced tile plan (GemmArgs::plan), 0: the planner
   // Implicit convolution: input [*, H, W, Cs] (first Ca channels active),
   // KH x KW taps (row-major), stride, zero padding, output Ho x Wo; weights
   // stride wseg elements per tap; nc = 64-channel steps per tap; buffer
@@ -1498,8 +1499,31 @@ hipError_t launch_persistent(const Params& p0, int rows, hipStream_t s) {
   }
 }
 
+// One launch of the tile plan p.plan (see kTilePlans).
+template <Epi E, bool CONV>
+hipError_t launch_forced(const Params& p, hipStream_t s) {
+  switch (p.plan) {
+    case 1: return launch_cfg<256, 256, 2, 4, E, CONV>(p, 0, s);
+    case 2: return launch_cfg<256, 128, 2, 2, E, CONV>(p, 0, s);
+    case 3: return launch_cfg<128, 128, 2, 2, E, CONV>(p, 0, s);
+    case 4: return launch_cfg<256, 64, 4, 1, E, CONV>(p, 0, s);
+    case 5:
+      if constexpr (!CONV && (E == Epi::Bias || E == Epi::BiasGelu || E == Epi::BiasResid)) {
+        if (p.K % kBK == 0 && p.K / kBK >= 4) return launch_cfg<128, 128, 2, 2, E, CONV, 4>(p, 0, s);
+      }
+      return hipErrorNotSupported;
+    case 6:
+      if constexpr (!CONV) {
+        if (persistent_ok<E>(p)) return launch_persistent<E>(p, p.M, s);
+      }
+      return hipErrorNotSupported;
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <Epi E, bool CONV = false>
 hipError_t launch_epi(const Params& p, hipStream_t s) {
+  if (p.plan != 0) return launch_forced<E, CONV>(p, s);
   // Pick the launch plan that keeps the chip busiest.  Estimated time is the
   // number of rounds of concurrent workgroups (one per CU) times the relative
   // cost of one tile.  Besides single launches of one tile shape there is a
@@ -1672,6 +1696,7 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   p.ldpos = a.ldpos > 0 ? a.ldpos : a.N;
   p.ccls = a.ccls;
   p.relu = a.relu ? 1 : 0;
+  p.plan = a.plan;
   p.res = static_cast<const uint16_t*>(a.res);
   p.ldres = a.ldres;
   p.aux = static_cast<uint16_t*>(a.aux);
@@ -1697,6 +1722,7 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   if (epi == Epi::GeluBwd && (a.aux == nullptr || a.ldaux < a.N || a.ldaux % 8 != 0))
     return hipErrorInvalidValue;
   if (a.res != nullptr && (a.ldres < a.N || a.ldres % 8 != 0)) return hipErrorInvalidValue;
+  if (a.plan < 0 || a.plan >= kTilePlans) return hipErrorInvalidValue;
   if (a.aux != nullptr && epi == Epi::BiasGelu && (a.ldaux < a.N || a.ldaux % 8 != 0))
     return hipErrorInvalidValue;
   // Small M: split K over more workgroups when the caller gave a workspace.
@@ -1705,6 +1731,7 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
     int kchunk = 0;
     const int ksplit = split_plan(p, a.ws_bytes, &kchunk);
     if (ksplit > 1) {
+      if (a.plan != 0) return hipErrorNotSupported;  // split K sums in another order
       switch (epi) {
         case Epi::Bias: return launch_split<Epi::Bias>(p, a.ws, ksplit, kchunk, s);
         case Epi::BiasGelu: return launch_split<Epi::BiasGelu>(p, a.ws, ksplit, kchunk, s);
@@ -1732,7 +1759,7 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
   if (a.batch < 0 || a.H < 1 || a.W < 1 || a.KH < 1 || a.KW < 1 || a.stride < 1 || a.pad < 0 ||
       a.N < 1 || a.Ca < 8 || (a.Ca & 7) != 0 || a.Cs < 1 || a.wseg < a.Ca || (a.wseg & 7) != 0 ||
       a.ldw < (int64_t)T * a.wseg || (a.ldw & 7) != 0 || a.ldc < a.N || (a.ldc & 7) != 0 ||
-      T > 64)
+      T > 64 || a.plan < 0 || a.plan >= kTilePlans)
     return hipErrorInvalidValue;
   if (win ? (a.KW != 1 || a.pad != 0 || (a.Cs & 3) != 0 || (a.stride * a.Cs) % 8 != 0 ||
              (a.W * a.Cs) % 8 != 0 || a.Ca < a.row_window * a.Cs)
@@ -1778,6 +1805,7 @@ hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s) {
     p.N = a.N;
     p.K = T * a.Ca;
     p.relu = a.relu ? 1 : 0;
+    p.plan = a.plan;
     p.cv_H = a.H; p.cv_W = a.W; p.cv_Cs = a.Cs; p.cv_Ca = a.Ca; p.cv_KW = a.KW; p.cv_T = T;
     p.cv_stride = a.stride; p.cv_pad = a.pad; p.cv_Ho = Ho; p.cv_Wo = Wo; p.cv_wseg = (int)a.wseg;
     p.cv_nc = (a.Ca + kBK - 1) / kBK;

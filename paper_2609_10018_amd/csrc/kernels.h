@@ -78,7 +78,20 @@ struct GemmArgs {
   // kSplitWsBytes is ever used.
   float* ws = nullptr;
   int64_t ws_bytes = 0;
+  // Tile plan (see kTilePlans): 0 lets the planner choose; another value
+  // runs that one configuration, or returns hipErrorNotSupported where it
+  // cannot take these arguments (or where the planner would split K).
+  int plan = 0;
 };
+
+// Tile plans a caller may force (GemmArgs::plan, ConvArgs::plan): 1 256x256,
+// 2 256x128, 3 128x128, 4 256x64, 5 128x128 with four LDS stages (bf16
+// Bias / BiasGelu / BiasResid, no implicit convolution, K a multiple of 64
+// and >= 256), 6 the persistent 256x256 kernel (where the planner may use
+// it).  Every plan walks K in the same order with the same MFMA
+// instruction, so for a GEMM with no LayerNorm work (ln_in, ln_out) and no
+// class-token rows (ccls) the outputs are bit-identical whatever the plan.
+constexpr int kTilePlans = 7;
 
 // Largest split-K workspace the planner uses: chunks are limited to the CU
 // count over the 128x128 tile count, so chunks x M x N stays below
@@ -107,6 +120,7 @@ struct ConvArgs {
   int N = 0;
   bool relu = false;
   int row_window = 0;
+  int plan = 0;  // as GemmArgs::plan (the persistent and four-stage plans do not apply)
 };
 hipError_t launch_conv_bf16(const ConvArgs& a, hipStream_t s);
 hipError_t launch_gemm_f32(Epi epi, const GemmArgs& a, hipStream_t s);

@@ -26,6 +26,8 @@ long g_fail_at = -1;  // hipMalloc call index (0-based, counted from arming) tha
 long g_armed_mallocs = 0;
 std::map<void*, size_t> g_live;
 uint8_t* g_static = nullptr;
+int g_elapsed_decreasing = 0;
+float g_elapsed = 1000.0f;
 
 void tick() { ++g_api_calls; }
 hipError_t api() {
@@ -44,6 +46,10 @@ long hipstub_launches(void) { return g_launches; }
 long hipstub_mallocs(void) { return g_mallocs; }
 long hipstub_live_allocations(void) { return (long)g_live.size(); }
 void hipstub_reset_counts(void) { g_api_calls = g_launches = g_mallocs = 0; }
+void hipstub_elapsed_decreasing(int on) {
+  g_elapsed_decreasing = on;
+  g_elapsed = 1000.0f;
+}
 void hipstub_fail_malloc_at(long n) {
   g_fail_at = n;
   g_armed_mallocs = 0;
@@ -118,7 +124,7 @@ hipError_t hipEventRecord(hipEvent_t, hipStream_t) { return api(); }
 hipError_t hipEventSynchronize(hipEvent_t) { return api(); }
 hipError_t hipEventElapsedTime(float* ms, hipEvent_t, hipEvent_t) {
   tick();
-  *ms = 0.25f;
+  *ms = g_elapsed_decreasing ? (g_elapsed *= 0.99f) : 0.25f;
   return hipSuccess;
 }
 

@@ -12,6 +12,9 @@ long hipstub_live_allocations(void);  // hipMalloc'd blocks not yet freed
 void hipstub_reset_counts(void);
 void hipstub_fail_malloc_at(long n);  // the n-th hipMalloc from now fails (n >= 0)
 void hipstub_release_static(void);
+// hipEventElapsedTime: 0.25 ms (off), or a value that falls with every call
+// (on), so that each timed candidate looks faster than the one before.
+void hipstub_elapsed_decreasing(int on);
 #ifdef __cplusplus
 }
 #endif

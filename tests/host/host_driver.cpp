@@ -600,6 +600,28 @@ void test_cnn() {
         ELASTO_ERR_BATCH_RANGE);
   CHECK(elasto_cnn_destroy(h) == ELASTO_OK);
   CHECK(hipstub_live_allocations() == live0);
+  {
+    // max_batch 32: create times every tile plan of every site (each timing
+    // here smaller than the last, so plans other than the planner's are
+    // kept); forwards of more than 16 images then use them.
+    Cnn t;
+    t.c.max_batch = 32;
+    hipstub_elapsed_decreasing(1);
+    hipstub_reset_counts();
+    elasto_cnn_t ht = nullptr;
+    CHECK(elasto_cnn_create(&t.c, &t.w, &t.t, &ht) == ELASTO_OK && ht);
+    CHECK(hipstub_launches() > 2 * 7 * 9);  // two modes, seven plans, nine sites
+    std::vector<uint8_t> im((size_t)32 * 3 * 64 * 64 * 2, 0);
+    std::vector<float> lg((size_t)32 * 10);
+    for (int b : {32, 16, 1}) {
+      hipstub_reset_counts();
+      CHECK(elasto_cnn_forward(ht, im.data(), b, lg.data(), nullptr) == ELASTO_OK);
+      CHECK(hipstub_launches() > 0 && hipstub_mallocs() == 0);
+    }
+    CHECK(elasto_cnn_destroy(ht) == ELASTO_OK);
+    CHECK(hipstub_live_allocations() == live0);
+    hipstub_elapsed_decreasing(0);
+  }
   for (long i = 0; i < mallocs; ++i) {
     hipstub_fail_malloc_at(i);
     elasto_cnn_t h2 = nullptr;

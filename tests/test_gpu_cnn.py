@@ -114,6 +114,18 @@ def test_resnet50_small_batches(batch):
         np.testing.assert_array_equal(n.run(k, batch), got)
 
 
+def test_resnet50_tile_plans_do_not_change_outputs():
+    """The handle (max_batch 256) chose its tile plans by timing them at
+    create; a batch of 256 runs with them, one of 128 with the planner's
+    choices.  Every plan walks K in the same order, so the logits of the
+    shared images are bit-identical."""
+    n = net("resnet50")
+    for k in (0, 3, 5):
+        full = n.run(k)
+        half = n.run(k, n.max_batch // 2)
+        np.testing.assert_array_equal(full[: n.max_batch // 2], half)
+
+
 def test_cnn_mode_info_matches_cost_model():
     from paper_2609_10018_amd import cost
     n = net("resnet50")
