@@ -1,7 +1,7 @@
 """rocprofv3 runs and summaries for the elastic-ViT forward (ViT-B/16, bf16,
 batch 256, one DN mode, mode 0 by default).
 
-    python -m paper_2609_10018_amd.pmc --out gpurun_out/pmc [--mode K]
+    PYTHONPATH=<repo> python -m paper_2609_10018_amd.pmc --out gpurun_out/pmc [--mode K]
 
 runs four profiled passes of ``bench.py`` (each a child process under its own
 time limit) and writes ``summary.md`` and ``traffic.json`` into ``--out``:
@@ -145,10 +145,10 @@ def run_pass(out, tag, rocprof_args, bench_args, limit):
     return d, cmd
 
 
-def _portable(cmd):
+def _portable(cmd, extra_roots=()):
     """A command as text, with the checkout's absolute paths shown as <repo>
     (the checkout the command ran in: the directory of its bench.py)."""
-    roots = {ROOT} | {os.path.dirname(a) for a in cmd if a.endswith("/bench.py")}
+    roots = {ROOT} | set(extra_roots) | {os.path.dirname(a) for a in cmd if a.endswith("/bench.py")}
     text = " ".join(cmd)
     for r in sorted(roots, key=len, reverse=True):
         text = text.replace(r, "<repo>")
@@ -239,7 +239,9 @@ def summarize(out, cmds, mode):
         "",
         "Commands (GPU box, run from `/tmp` with `TMPDIR=/tmp`; committed files only):",
         "",
-        f"    python -m paper_2609_10018_amd.pmc --out <repo>/gpurun_out/pmc --mode {mode}",
+        "    PYTHONPATH=<repo> " + _portable(
+            ["python", "-m", "paper_2609_10018_amd.pmc", "--out", out, "--mode", str(mode)],
+            {os.path.dirname(a) for c in cmds.values() for a in c if a.endswith("/bench.py")}),
         "",
         "which runs:",
         "",
