@@ -130,6 +130,12 @@ typedef struct {
  * rounded to nearest even on the BF16 path), makes one device allocation for
  * the weights and one for max_batch activation scratch, and copies.  The
  * current device at call time owns the handle.  Mode 0 is selected.
+ * BF16 with max_batch >= 32: also runs one forward per DN mode on the
+ * default stream in which every GEMM is timed with each tile plan the GEMM
+ * kernels offer, and keeps the fastest per GEMM shape (a fraction of a
+ * second; synchronises the device).  Forwards of more than max_batch / 2
+ * images use those plans; a handle's outputs are deterministic, two handles
+ * may differ within fp32 rounding.
  * *out receives the handle (unchanged on error). */
 elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t* w,
                               const elasto_dn_table_t* table, elasto_handle_t* out);
@@ -515,10 +521,15 @@ typedef struct {
 /* Host-only validation (no HIP call). */
 elasto_status_t elasto_cnn_validate(const elasto_cnn_config_t* cfg, const elasto_cnn_table_t* t);
 
-/* As elasto_create: validates, packs (bf16 filters with the input channels
- * of each 3x3 ordered channel-major, c * 9 + tap, so a narrower mode's
- * channels are a prefix of every filter row), one weight and one scratch
- * allocation sized for max_batch, mode 0 selected. */
+/* As elasto_create: validates, packs (bf16; a 3x3 filter row holds its 9
+ * taps one after another, each tap's input channels in order1 order over the
+ * block's full width, so a narrower mode's channels are a prefix of every
+ * tap's segment), one weight and one scratch allocation sized for max_batch,
+ * mode 0 selected.  With max_batch >= 32 it also times every tile plan of
+ * each convolution of every DN mode once (one forward per mode on the
+ * default stream, about a second for ResNet-50 at 256 images; synchronises
+ * the device) and keeps the fastest; forwards of more than max_batch / 2
+ * images use them.  The plans give bit-identical outputs. */
 elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_cnn_weights_t* w,
                                   const elasto_cnn_table_t* table, elasto_cnn_t* out);
 elasto_status_t elasto_cnn_destroy(elasto_cnn_t h);

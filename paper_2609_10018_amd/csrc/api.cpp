@@ -25,6 +25,7 @@
 #include "handle.h"
 #include "kernels.h"
 #include "layout.h"
+#include "plans.h"
 
 using namespace elasto;
 
@@ -105,8 +106,20 @@ int64_t scratch_layout(const elasto_config_t& cfg, const Dims& d, int lnseg, int
   return 3 * sz_x + sz_qkv + sz_g + sz_cls + sz_xcls + sz_ln + ws_bytes;
 }
 
+// Create-time tuning of the GEMM tile plans (plans.h): events for the
+// timings, and the plan chosen for each GEMM shape already timed (the layers
+// of a mode, and often several modes, share shapes).
+struct PlanTuning {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  struct Seen {
+    int64_t key[9];
+    uint8_t plan;
+  };
+  std::vector<Seen> seen;
+};
+
 elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
-                             void* hip_stream, const Acts& act);
+                             void* hip_stream, const Acts& act, PlanTuning* tune = nullptr);
 
 }  // namespace
 
@@ -239,6 +252,45 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   h->lnpart = a.lnpart;
   h->ws = a.ws;
   h->ws_bytes = a.ws_bytes;
+  h->nsites = 2 + 4 * cfg->depth;
+
+  // Tile plans (handle.h, plans.h): one tuning forward per mode, images read
+  // from the q/k/v buffer (overwritten only after the patch embedding has
+  // read them), logits written to the fc1 buffer (free by then); their
+  // values do not matter.
+  const int64_t B = cfg->max_batch;
+  const int64_t img_bytes = B * cfg->in_chans * cfg->img * cfg->img * 2;
+  const int64_t qkv_bytes = B * h->dims.T * 3 * (int64_t)cfg->dim * 2;
+  const int64_t g_bytes = B * h->dims.T * (int64_t)cfg->mlp_hidden * 2;
+  if (bf && B >= kTuneMinBatch && img_bytes <= qkv_bytes && B * cfg->num_classes * 4 <= g_bytes) {
+    elasto_status_t st = ELASTO_OK;
+    PlanTuning tn;
+    try {
+      h->plans.assign((size_t)h->num_modes * h->nsites, 0);
+      tn.seen.reserve(64);
+    } catch (...) {
+      st = fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
+    }
+    if (st == ELASTO_OK &&
+        (hipEventCreate(&tn.e0) != hipSuccess || hipEventCreate(&tn.e1) != hipSuccess))
+      st = fail(ELASTO_ERR_HIP, "create: cannot create events");
+    for (int m = 0; st == ELASTO_OK && m < h->num_modes; ++m) {
+      h->mode = m;
+      st = forward_impl(h, h->qkv, (int32_t)B, static_cast<float*>(h->g), nullptr, a, &tn);
+    }
+    if (st == ELASTO_OK && hipDeviceSynchronize() != hipSuccess)
+      st = fail(ELASTO_ERR_HIP, "create: tuning forward failed");
+    if (tn.e0) (void)hipEventDestroy(tn.e0);
+    if (tn.e1) (void)hipEventDestroy(tn.e1);
+    h->mode = 0;
+    if (st != ELASTO_OK) {
+      (void)hipFree(h->dw);
+      (void)hipFree(h->ds);
+      if (h->dfold) (void)hipFree(h->dfold);
+      delete h;
+      return st;
+    }
+  }
   *out = h;
   clear_error();
   return ELASTO_OK;
@@ -413,7 +465,7 @@ elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int
 namespace {
 
 elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
-                             void* hip_stream, const Acts& act) {
+                             void* hip_stream, const Acts& act, PlanTuning* tune) {
   if (!images || !logits) return fail(ELASTO_ERR_INVALID_ARG, "images / logits is NULL");
   if (batch < 1 || batch > h->cfg.max_batch)
     return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
@@ -447,6 +499,36 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
   const bool fold = h->dfold != nullptr;
   const int wi = fold ? h->width_idx[(size_t)k] : 0;
   auto fold_ptr = [&](int l, int64_t off) { return h->dfold + (int64_t)l * h->fold_stride + off; };
+  // GEMM sites (handle.h): the tuned plan of the next site for batches of more
+  // than half of max_batch; in the tuning forwards, every plan timed (once
+  // per distinct shape) and the choice recorded.
+  const bool use_plans = !h->plans.empty() && 2 * (int64_t)batch > c.max_batch;
+  int site = 0;
+  auto run = [&](int kc, Epi epi, GemmArgs& a) -> hipError_t {
+    const size_t i = (size_t)k * h->nsites + site++;
+    if (tune) {
+      const int64_t key[9] = {(int64_t)epi, a.M, a.N, a.K, a.lda, a.ldc, a.ln_in != nullptr,
+                              a.ln_out != nullptr, a.ccls != nullptr};
+      for (const PlanTuning::Seen& sn : tune->seen)
+        if (std::equal(key, key + 9, sn.key)) {
+          h->plans[i] = sn.plan;
+          return hipSuccess;
+        }
+      const hipError_t te = time_plans(
+          [&](int pl) {
+            a.plan = pl;
+            return gemm(epi, a, s);
+          },
+          s, tune->e0, tune->e1, &h->plans[i]);
+      PlanTuning::Seen sn;
+      std::copy(key, key + 9, sn.key);
+      sn.plan = h->plans[i];
+      tune->seen.push_back(sn);
+      return te;
+    }
+    a.plan = use_plans ? (int)h->plans[i] : 0;
+    return timed(h, kc, s, [&] { return gemm(epi, a, s); });
+  };
 
   hipError_t e;
   {
@@ -473,7 +555,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       a.ln_out = act.lnpart;
       a.ln_ld = h->lnseg;
     }
-    e = timed(h, ELASTO_K_PATCH, s, [&] { return gemm(Epi::Patch, a, s); });
+    e = run(ELASTO_K_PATCH, Epi::Patch, a);
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "patch embedding: %s", hipGetErrorString(e));
   }
   for (int l = 0; l < L; ++l) {
@@ -496,7 +578,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       q.ln_in = act.lnpart; q.ln_ld = h->lnseg; q.ln_eps = c.ln_eps;
     }
     q.ws = act.ws; q.ws_bytes = act.ws_bytes;
-    e = timed(h, ELASTO_K_QKV, s, [&] { return gemm(Epi::Bias, q, s); });
+    e = run(ELASTO_K_QKV, Epi::Bias, q);
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "qkv layer %d: %s", l, hipGetErrorString(e));
     AttnArgs at;
     at.qkv = act.qkv; at.qkv_stride = 3 * D;
@@ -516,7 +598,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       pr.ln_out = act.lnpart; pr.ln_ld = h->lnseg;
     }
     pr.ws = act.ws; pr.ws_bytes = act.ws_bytes;
-    e = timed(h, ELASTO_K_PROJ, s, [&] { return gemm(Epi::BiasResid, pr, s); });
+    e = run(ELASTO_K_PROJ, Epi::BiasResid, pr);
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "proj layer %d: %s", l, hipGetErrorString(e));
     if (!fold) {
       e = timed(h, ELASTO_K_LN, s, [&] { return ln(F(h, ELASTO_T_LN2_G, l), F(h, ELASTO_T_LN2_B, l)); });
@@ -536,7 +618,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       f1.ln_in = act.lnpart; f1.ln_ld = h->lnseg; f1.ln_eps = c.ln_eps;
     }
     f1.ws = act.ws; f1.ws_bytes = act.ws_bytes;
-    e = timed(h, ELASTO_K_FC1, s, [&] { return gemm(Epi::BiasGelu, f1, s); });
+    e = run(ELASTO_K_FC1, Epi::BiasGelu, f1);
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc1 layer %d: %s", l, hipGetErrorString(e));
     GemmArgs f2;
     f2.A = act.g; f2.lda = Mh;
@@ -550,7 +632,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       f2.ln_out = act.lnpart; f2.ln_ld = h->lnseg;
     }
     f2.ws = act.ws; f2.ws_bytes = act.ws_bytes;
-    e = timed(h, ELASTO_K_FC2, s, [&] { return gemm(Epi::BiasResid, f2, s); });
+    e = run(ELASTO_K_FC2, Epi::BiasResid, f2);
     if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "fc2 layer %d: %s", l, hipGetErrorString(e));
   }
   // Final norm on the class-token rows only.
@@ -567,7 +649,7 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
   hg.C = logits; hg.ldc = c.num_classes;
   hg.bias = F(h, ELASTO_T_HEAD_B);
   hg.M = batch; hg.N = c.num_classes; hg.K = E;
-  e = timed(h, ELASTO_K_HEAD, s, [&] { return gemm(Epi::BiasF32, hg, s); });
+  e = run(ELASTO_K_HEAD, Epi::BiasF32, hg);
   if (e != hipSuccess) return fail(ELASTO_ERR_HIP, "head: %s", hipGetErrorString(e));
   return ELASTO_OK;
 }

@@ -33,6 +33,7 @@
 
 #include "kernels.h"
 #include "layout.h"
+#include "plans.h"
 
 using namespace elasto;
 
@@ -47,39 +48,6 @@ struct BlockOff {
   int64_t c1w, c1b, c2w, c2b, c3w, c3b, dnw, dnb;
 };
 
-constexpr int kTuneMinBatch = 32;  // smaller max_batch: no tuning
-constexpr int kTuneReps = 3;       // timed launches per plan (the fastest counts)
-
-// Times `launch(plan)` for every tile plan at one site and stores the choice
-// in `plan` (see the file comment).  launch returns hipErrorNotSupported for
-// a plan that cannot run the site's arguments.
-template <class F>
-hipError_t tune_site(F&& launch, uint8_t& plan, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  float t0 = 0.0f, best_t = 0.0f;
-  int best = 0;
-  for (int c = 0; c < kTilePlans; ++c) {
-    hipError_t e = launch(c);  // also the warm-up
-    if (e == hipErrorNotSupported) continue;
-    if (e != hipSuccess) return e;
-    float t = 0.0f;
-    for (int r = 0; r < kTuneReps; ++r) {
-      if ((e = hipEventRecord(e0, s)) != hipSuccess || (e = launch(c)) != hipSuccess ||
-          (e = hipEventRecord(e1, s)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess)
-        return e;
-      float ms = 0.0f;
-      if ((e = hipEventElapsedTime(&ms, e0, e1)) != hipSuccess) return e;
-      t = r == 0 ? ms : std::min(t, ms);
-    }
-    if (c == 0) {
-      t0 = best_t = t;
-    } else if (t < best_t) {
-      best_t = t;
-      best = c;
-    }
-  }
-  plan = (uint8_t)(best != 0 && best_t < 0.97f * t0 ? best : 0);
-  return hipSuccess;
-}
 
 std::vector<BlockSpec> block_specs(const elasto_cnn_config_t& c) {
   std::vector<BlockSpec> out;
@@ -500,7 +468,7 @@ elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float
   int site = 0;
   auto at_site = [&](auto&& launch) -> hipError_t {
     const size_t i = (size_t)k * h->nsites + site++;
-    if (tune) return tune_site(launch, h->plans[i], s, tune0, tune1);
+    if (tune) return time_plans(launch, s, tune0, tune1, &h->plans[i]);
     return launch(use_plans ? (int)h->plans[i] : 0);
   };
   hipError_t e;

@@ -37,6 +37,11 @@ struct elasto_handle_s {
   float* ws = nullptr;             // split-K workspace of small-batch GEMMs (bf16 path)
   int64_t ws_bytes = 0;
   int lnseg = 0;                   // 64-column segments of d, rounded up to even
+  // bf16: tile plan per (mode, GEMM site), sites in forward order: patch
+  // embedding, per layer q/k/v, projection, fc1, fc2, then the head; chosen
+  // at create by timing (plans.h).  Empty: the planner everywhere.
+  int nsites = 0;
+  std::vector<uint8_t> plans;
   // kernel timing
   int timed_class = -1;
   std::vector<hipEvent_t> events;

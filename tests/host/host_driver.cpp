@@ -645,6 +645,36 @@ void test_null_handles() {
 
 }  // namespace
 
+// bf16 handles of max_batch >= 32 time every GEMM tile plan at create (each
+// stand-in timing smaller than the last, so plans other than the planner's
+// are kept); forwards of more than half of max_batch images use them.
+void test_tuned_plans(bool embed) {
+  elasto_config_t c = vit_config(ELASTO_BF16);
+  c.max_batch = 32;
+  VitWeights w(c);
+  VitTable tab(c, 3, embed);
+  const long live0 = hipstub_live_allocations();
+  hipstub_elapsed_decreasing(1);
+  hipstub_reset_counts();
+  elasto_handle_t h = nullptr;
+  CHECK(elasto_create(&c, &w.w, &tab.t, &h) == ELASTO_OK && h);
+  if (!h) return;
+  CHECK(hipstub_launches() > 7 * 6);  // at least every plan of the distinct GEMM shapes
+  std::vector<uint8_t> images((size_t)c.max_batch * c.in_chans * c.img * c.img * 2, 0);
+  std::vector<float> logits((size_t)c.max_batch * c.num_classes);
+  for (int k = 0; k < 3; ++k)
+    for (int b : {32, 16, 1}) {
+      CHECK(elasto_set_mode(h, k) == ELASTO_OK);
+      hipstub_reset_counts();
+      CHECK(elasto_forward(h, images.data(), b, logits.data(), nullptr) == ELASTO_OK);
+      CHECK(elasto_forward_static(h, images.data(), b, logits.data(), nullptr) == ELASTO_OK);
+      CHECK(hipstub_launches() > 0 && hipstub_mallocs() == 0);
+    }
+  CHECK(elasto_destroy(h) == ELASTO_OK);
+  CHECK(hipstub_live_allocations() == live0);
+  hipstub_elapsed_decreasing(0);
+}
+
 int main() {
   test_validation(ELASTO_FP32);
   test_validation(ELASTO_BF16);
@@ -654,6 +684,8 @@ int main() {
   test_lifecycle(ELASTO_FP32, true);
   test_lifecycle(ELASTO_BF16, false);
   test_lifecycle(ELASTO_BF16, true);
+  test_tuned_plans(false);
+  test_tuned_plans(true);
   test_growth();
   test_ops();
   test_select();
