@@ -205,9 +205,14 @@ def next_rows(torch, ffi, inputs, stream, with_cpu, steps=20, warmup=3):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / gsteps
+    gflop = cost.growth_step_flops(cfg, t, 0) / 1e9
     gres = {"workload": "ViT-B/16 growth step (mode 0 from mode 1), batch 64, bf16 with fp32 "
                         "masters", "steps": gsteps, "ms_per_step": ms,
-            "images_per_s": GB * 1e3 / ms}
+            "images_per_s": GB * 1e3 / ms, "gflop_per_image": gflop,
+            "tflops": gflop * GB / ms, "mfu": gflop * GB / ms / BF16_PEAK_TFLOPS,
+            "flops_note": "cost.growth_step_flops: forward, activation gradients, attention "
+                          "backward as five T x T contractions per head, weight gradients of "
+                          "the re-introduced slices"}
     gc.close()
     vit.close()
     log(f"growth step b64: {ms:.2f} ms")

@@ -51,6 +51,25 @@ def flops_per_image(cfg: ModelConfig, table, k: int) -> float:
     return float(sum(gemm_flops(cfg, table, k).values()))
 
 
+def growth_step_flops(cfg: ModelConfig, table, k: int) -> float:
+    """Per-image FLOPs of one growth step of mode k from mode k + 1 (Eq. 9)
+    as the bf16 path runs it: the mode-k forward (gemm_flops); the
+    activation-gradient contractions of the head and of every layer's fc2,
+    fc1, projection and q/k/v over mode k's widths; the attention backward
+    counted as five T x T x head_dim contractions per head (the scores once
+    recomputed, dP, dV, dQ, dK); and the weight-gradient contractions over
+    the re-introduced slices only (mode k's widths minus mode k + 1's).  The
+    patch embedding is not differentiated."""
+    T, d, hd = cfg.tokens, embed_width(cfg, table, k), cfg.head_dim
+    h, m = layer_widths(table, k)
+    hp, mp = layer_widths(table, k + 1)
+    act = 2.0 * T * (d * m + m * d + d * hd * h + 3 * hd * h * d)
+    attn = 5 * 2.0 * T * T * hd * h
+    wgrad = 2.0 * T * (d * (m - mp) + (m - mp) * d + d * hd * (h - hp) + 3 * hd * (h - hp) * d)
+    return (flops_per_image(cfg, table, k) + 2.0 * d * cfg.num_classes
+            + float(np.sum(act + attn + wgrad)))
+
+
 def paper_macs(cfg: ModelConfig, table, k: int) -> float:
     f = gemm_flops(cfg, table, k)
     return (f["patch"] + f["qkv"] + f["proj"] + f["fc1"] + f["fc2"] + f["head"]) / 2.0

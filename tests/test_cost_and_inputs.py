@@ -176,3 +176,25 @@ def test_dense_model_bytes_count_the_extracted_model(name):
             elif isinstance(v, np.ndarray):
                 total += v.size * (2 if key in mats else 4)
         assert cost.dense_model_bytes(cfg, t, k) == total, (name, k)
+
+
+def test_growth_step_flops_decomposition():
+    """The growth step's count = forward + head backward + activation
+    gradients (the forward's layer contractions once more) + attention
+    backward (2.5x the forward's QK^T and PV) + weight gradients of the
+    re-introduced slices: none when mode k + 1 equals mode k, all of the
+    layer contractions once more when mode k + 1 keeps nothing."""
+    from types import SimpleNamespace
+    cfg = inputs.CONFIGS["vit_b"]
+    L = cfg.depth
+    h0, m0 = np.full(L, cfg.heads), np.full(L, cfg.mlp_hidden)
+    f = cost.gemm_flops(cfg, SimpleNamespace(n_heads=[h0], n_mlp=[m0]), 0)
+    layers = f["qkv"] + f["proj"] + f["fc1"] + f["fc2"]
+    base = sum(f.values()) + 2.0 * cfg.dim * cfg.num_classes + layers + 2.5 * f["attn"]
+    same = SimpleNamespace(n_heads=[h0, h0], n_mlp=[m0, m0])
+    none = SimpleNamespace(n_heads=[h0, 0 * h0], n_mlp=[m0, 0 * m0])
+    assert cost.growth_step_flops(cfg, same, 0) == pytest.approx(base, rel=1e-12)
+    assert cost.growth_step_flops(cfg, none, 0) == pytest.approx(base + layers, rel=1e-12)
+    t = inputs.make_dn_table(cfg)
+    assert (cost.growth_step_flops(cfg, same, 0) < cost.growth_step_flops(cfg, t, 0)
+            < cost.growth_step_flops(cfg, none, 0))
