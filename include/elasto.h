@@ -130,12 +130,18 @@ typedef struct {
  * rounded to nearest even on the BF16 path), makes one device allocation for
  * the weights and one for max_batch activation scratch, and copies.  The
  * current device at call time owns the handle.  Mode 0 is selected.
- * BF16 with max_batch >= 32: also runs one forward per DN mode on the
- * default stream in which every GEMM is timed with each tile plan the GEMM
- * kernels offer, and keeps the fastest per GEMM shape (a fraction of a
- * second; synchronises the device).  Forwards of more than max_batch / 2
- * images use those plans; a handle's outputs are deterministic, two handles
- * may differ within fp32 rounding.
+ * BF16 with max_batch >= 32: also tunes, per DN mode, on the default
+ * stream (about a second at ViT-B batch 256; synchronises the device): every
+ * GEMM is timed with each tile plan the GEMM kernels offer, for forwards of
+ * max_batch and of half as many images, and the whole forward is timed
+ * against two half-batch forwards of which the second runs on a stream the
+ * handle owns (forked from and joined back into the caller's stream with
+ * events, so a captured graph captures both).  A forward of more than
+ * max_batch / 2 images then runs as chosen.  The choices are kept per
+ * process: a later handle of the same configuration, DN widths, max_batch
+ * and device takes them without timing.  A handle's outputs are
+ * deterministic; handles of different processes may differ within fp32
+ * rounding (the plans of the LayerNorm-folded GEMMs round differently).
  * *out receives the handle (unchanged on error). */
 elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t* w,
                               const elasto_dn_table_t* table, elasto_handle_t* out);
@@ -525,11 +531,13 @@ elasto_status_t elasto_cnn_validate(const elasto_cnn_config_t* cfg, const elasto
  * taps one after another, each tap's input channels in order1 order over the
  * block's full width, so a narrower mode's channels are a prefix of every
  * tap's segment), one weight and one scratch allocation sized for max_batch,
- * mode 0 selected.  With max_batch >= 32 it also times every tile plan of
- * each convolution of every DN mode once (one forward per mode on the
- * default stream, about a second for ResNet-50 at 256 images; synchronises
- * the device) and keeps the fastest; forwards of more than max_batch / 2
- * images use them.  The plans give bit-identical outputs. */
+ * mode 0 selected.  With max_batch >= 32 it also tunes as elasto_create
+ * does: tile plans of each convolution of every DN mode, for whole and
+ * half-batch forwards, and whether a mode runs as two half-batch forwards on
+ * two streams (about two seconds for ResNet-50 at 256 images; synchronises
+ * the device), kept per process for handles of the same shapes; forwards of
+ * more than max_batch / 2 images run as chosen.  Every choice gives
+ * bit-identical outputs. */
 elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_cnn_weights_t* w,
                                   const elasto_cnn_table_t* table, elasto_cnn_t* out);
 elasto_status_t elasto_cnn_destroy(elasto_cnn_t h);

@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(LIB_DIR, "libelasto.so")
 
 SOURCES = ["gemm_bf16.hip", "gemm_f32.hip", "attention.hip", "attention_bwd.hip", "layernorm.hip",
            "conv.hip", "growth_kernels.hip", "static_scratch.hip", "growth.cpp",
-           "api.cpp", "layout.cpp", "select.cpp", "cnn.cpp"]
+           "api.cpp", "layout.cpp", "select.cpp", "cnn.cpp", "plans.cpp"]
 ARCH = "gfx950"
 
 

@@ -64,6 +64,14 @@ hipError_t timed(elasto_handle_s* h, int kc, hipStream_t s, Fn&& fn) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+void release_streams(elasto_handle_s* h) {
+  if (h->side) (void)hipStreamDestroy(h->side);
+  if (h->fork) (void)hipEventDestroy(h->fork);
+  if (h->join) (void)hipEventDestroy(h->join);
+  h->side = nullptr;
+  h->fork = h->join = nullptr;
+}
+
 // Activation buffers of one forward.
 struct Acts {
   void *x = nullptr, *u = nullptr, *o = nullptr, *qkv = nullptr, *g = nullptr, *ucls = nullptr;
@@ -107,10 +115,12 @@ int64_t scratch_layout(const elasto_config_t& cfg, const Dims& d, int lnseg, int
 }
 
 // Create-time tuning of the GEMM tile plans (plans.h): events for the
-// timings, and the plan chosen for each GEMM shape already timed (the layers
-// of a mode, and often several modes, share shapes).
+// timings, where the choices of the forward being tuned go ([nsites]), and
+// the plan chosen for each GEMM shape already timed (the layers of a mode,
+// and often several modes, share shapes).
 struct PlanTuning {
   hipEvent_t e0 = nullptr, e1 = nullptr;
+  uint8_t* target = nullptr;
   struct Seen {
     int64_t key[9];
     uint8_t plan;
@@ -118,8 +128,18 @@ struct PlanTuning {
   std::vector<Seen> seen;
 };
 
+// One forward over the activation buffers `act`, with a tile plan per GEMM
+// site (`plans`, [nsites]; nullptr: the planner), or timing them (`tune`).
 elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
-                             void* hip_stream, const Acts& act, PlanTuning* tune = nullptr);
+                             void* hip_stream, const Acts& act, const uint8_t* plans,
+                             PlanTuning* tune = nullptr);
+
+// A forward as the handle's tuning chose for the current mode: for more than
+// max_batch / 2 images with its tile plans, whole or as two halves on the
+// caller's stream and the side stream; smaller batches (and forwards whose
+// kernel launches are being timed) whole with the planner.
+elasto_status_t forward_parts(elasto_handle_t h, const void* images, int32_t batch, float* logits,
+                              void* hip_stream, const Acts& act);
 
 }  // namespace
 
@@ -254,10 +274,12 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   h->ws_bytes = a.ws_bytes;
   h->nsites = 2 + 4 * cfg->depth;
 
-  // Tile plans (handle.h, plans.h): one tuning forward per mode, images read
-  // from the q/k/v buffer (overwritten only after the patch embedding has
-  // read them), logits written to the fc1 buffer (free by then); their
-  // values do not matter.
+  // Tile plans and split (handle.h, plans.h): per mode a tuning forward of
+  // max_batch images and one of half as many, then the whole forward timed
+  // against the two-stream split; or the choices an earlier handle of the
+  // same shapes made in this process.  Images are read from the q/k/v buffer
+  // (overwritten only after the patch embedding has read them) and logits
+  // written to the fc1 buffer; their values do not matter.
   const int64_t B = cfg->max_batch;
   const int64_t img_bytes = B * cfg->in_chans * cfg->img * cfg->img * 2;
   const int64_t qkv_bytes = B * h->dims.T * 3 * (int64_t)cfg->dim * 2;
@@ -265,25 +287,82 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   if (bf && B >= kTuneMinBatch && img_bytes <= qkv_bytes && B * cfg->num_classes * 4 <= g_bytes) {
     elasto_status_t st = ELASTO_OK;
     PlanTuning tn;
+    std::vector<int64_t> key;
+    bool cached = false;
     try {
-      h->plans.assign((size_t)h->num_modes * h->nsites, 0);
-      tn.seen.reserve(64);
+      key = {0, h->device, cfg->img, cfg->patch, cfg->in_chans, cfg->dim, cfg->depth, cfg->heads,
+             cfg->mlp_hidden, cfg->num_classes, cfg->max_batch, cfg->dtype, h->num_modes};
+      key.insert(key.end(), h->n_heads.begin(), h->n_heads.end());
+      key.insert(key.end(), h->n_mlp.begin(), h->n_mlp.end());
+      key.insert(key.end(), h->n_embed.begin(), h->n_embed.end());
+      TunedPlans tp;
+      cached = tuned_lookup(key, &tp);
+      if (cached) {
+        h->plans = tp.plans;
+        h->plans_half = tp.plans_half;
+        h->split = tp.split;
+      } else {
+        h->plans.assign((size_t)h->num_modes * h->nsites, 0);
+        h->plans_half.assign((size_t)h->num_modes * h->nsites, 0);
+        h->split.assign((size_t)h->num_modes, 0);
+        tn.seen.reserve(64);
+      }
     } catch (...) {
       st = fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
     }
     if (st == ELASTO_OK &&
-        (hipEventCreate(&tn.e0) != hipSuccess || hipEventCreate(&tn.e1) != hipSuccess))
-      st = fail(ELASTO_ERR_HIP, "create: cannot create events");
-    for (int m = 0; st == ELASTO_OK && m < h->num_modes; ++m) {
+        (hipEventCreate(&tn.e0) != hipSuccess || hipEventCreate(&tn.e1) != hipSuccess ||
+         hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) != hipSuccess ||
+         hipEventCreateWithFlags(&h->fork, hipEventDisableTiming) != hipSuccess ||
+         hipEventCreateWithFlags(&h->join, hipEventDisableTiming) != hipSuccess))
+      st = fail(ELASTO_ERR_HIP, "create: cannot create streams / events");
+    Acts half = a;
+    half.ws = nullptr;
+    half.ws_bytes = 0;
+    float* lg = static_cast<float*>(h->g);
+    // Whole forwards and two-stream splits of the mode, alternately (round 0
+    // untimed), and whether the split is faster by the margin.
+    auto choose_split = [&](size_t m) -> elasto_status_t {
+      float t[2] = {0.0f, 0.0f};
+      for (int r = 0; r <= kTuneReps; ++r)
+        for (int sp = 0; sp < 2; ++sp) {
+          h->split[m] = (uint8_t)sp;
+          if (hipEventRecord(tn.e0, nullptr) != hipSuccess) return fail(ELASTO_ERR_HIP, "create: event");
+          const elasto_status_t fs = forward_parts(h, h->qkv, (int32_t)B, lg, nullptr, a);
+          if (fs != ELASTO_OK) return fs;
+          float ms = 0.0f;
+          if (hipEventRecord(tn.e1, nullptr) != hipSuccess || hipEventSynchronize(tn.e1) != hipSuccess ||
+              hipEventElapsedTime(&ms, tn.e0, tn.e1) != hipSuccess)
+            return fail(ELASTO_ERR_HIP, "create: timing failed");
+          if (r == 1 || (r > 1 && ms < t[sp])) t[sp] = ms;
+        }
+      h->split[m] = t[1] < kTuneMargin * t[0] ? 1 : 0;
+      return ELASTO_OK;
+    };
+    for (int m = 0; st == ELASTO_OK && !cached && m < h->num_modes; ++m) {
       h->mode = m;
-      st = forward_impl(h, h->qkv, (int32_t)B, static_cast<float*>(h->g), nullptr, a, &tn);
+      const size_t o = (size_t)m * h->nsites;
+      tn.target = h->plans.data() + o;
+      st = forward_impl(h, h->qkv, (int32_t)B, lg, nullptr, a, nullptr, &tn);
+      tn.target = h->plans_half.data() + o;
+      if (st == ELASTO_OK)
+        st = forward_impl(h, h->qkv, (int32_t)((B + 1) / 2), lg, nullptr, half, nullptr, &tn);
+      if (st == ELASTO_OK) st = choose_split((size_t)m);
     }
     if (st == ELASTO_OK && hipDeviceSynchronize() != hipSuccess)
       st = fail(ELASTO_ERR_HIP, "create: tuning forward failed");
+    if (st == ELASTO_OK && !cached) {
+      try {
+        tuned_store(key, TunedPlans{h->plans, h->plans_half, h->split});
+      } catch (...) {
+        st = fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
+      }
+    }
     if (tn.e0) (void)hipEventDestroy(tn.e0);
     if (tn.e1) (void)hipEventDestroy(tn.e1);
     h->mode = 0;
     if (st != ELASTO_OK) {
+      release_streams(h);
       (void)hipFree(h->dw);
       (void)hipFree(h->ds);
       if (h->dfold) (void)hipFree(h->dfold);
@@ -299,6 +378,7 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
 elasto_status_t elasto_destroy(elasto_handle_t h) {
   if (!h) return ELASTO_OK;
   destroy_events(h);
+  release_streams(h);
   hipError_t e1 = hipSuccess, e2 = hipSuccess;
   if (h->dw) e1 = hipFree(h->dw);
   if (h->ds) e2 = hipFree(h->ds);
@@ -431,7 +511,7 @@ elasto_status_t elasto_forward(elasto_handle_t h, const void* images, int32_t ba
   Acts a;
   a.x = h->x; a.u = h->u; a.o = h->o; a.qkv = h->qkv; a.g = h->g; a.ucls = h->ucls;
   a.xcls = h->xcls; a.lnpart = h->lnpart; a.ws = h->ws; a.ws_bytes = h->ws_bytes;
-  return forward_impl(h, images, batch, logits, hip_stream, a);
+  return forward_parts(h, images, batch, logits, hip_stream, a);
 }
 
 elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int32_t batch,
@@ -457,15 +537,69 @@ elasto_status_t elasto_forward_static(elasto_handle_t h, const void* images, int
                                ? std::min(kSplitWsBytes, (have - need) / 256 * 256) : 0;
   Acts a;
   scratch_layout(h->cfg, h->dims, h->lnseg, batch, ws_bytes, static_cast<uint8_t*>(base), &a);
-  return forward_impl(h, images, batch, logits, hip_stream, a);
+  return forward_parts(h, images, batch, logits, hip_stream, a);
 }
 
 }  // extern "C"
 
 namespace {
 
+// The activation buffers of the images from `b` on (every buffer holds a
+// fixed number of bytes per image), without the split-K workspace.
+Acts offset_acts(const elasto_handle_s* h, const Acts& a, int64_t b) {
+  const elasto_config_t& c = h->cfg;
+  const int64_t eb = c.dtype == ELASTO_BF16 ? 2 : 4, T = h->dims.T, D = c.dim;
+  auto adv = [&](void* p, int64_t per_image) {
+    return p ? static_cast<void*>(static_cast<uint8_t*>(p) + b * per_image) : nullptr;
+  };
+  Acts r;
+  r.x = adv(a.x, T * D * eb);
+  r.u = adv(a.u, T * D * eb);
+  r.o = adv(a.o, T * D * eb);
+  r.qkv = adv(a.qkv, T * 3 * D * eb);
+  r.g = adv(a.g, T * c.mlp_hidden * eb);
+  r.ucls = adv(a.ucls, D * eb);
+  r.xcls = a.xcls ? a.xcls + b * D : nullptr;
+  r.lnpart = a.lnpart ? a.lnpart + b * T * h->lnseg : nullptr;
+  return r;
+}
+
+elasto_status_t forward_parts(elasto_handle_t h, const void* images, int32_t batch, float* logits,
+                              void* hip_stream, const Acts& act) {
+  const elasto_config_t& c = h->cfg;
+  const int k = h->mode;
+  if (h->plans.empty() || 2 * (int64_t)batch <= c.max_batch || batch > c.max_batch)
+    return forward_impl(h, images, batch, logits, hip_stream, act, nullptr);
+  const size_t o = (size_t)k * h->nsites;
+  const int32_t b1 = (batch + 1) / 2, b2 = batch - b1;
+  const int64_t img_bytes = (int64_t)c.in_chans * c.img * c.img * 2;
+  if (!h->split[(size_t)k] || h->timed_class >= 0 || b2 < 1 || (b1 * img_bytes) % 16 != 0 ||
+      !images || !logits)
+    return forward_impl(h, images, batch, logits, hip_stream, act, h->plans.data() + o);
+  // Neither half gets the split-K workspace (they run at once, and each
+  // image's arithmetic must not depend on the half it falls in).
+  Acts first = act;
+  first.ws = nullptr;
+  first.ws_bytes = 0;
+  const Acts second = offset_acts(h, act, b1);
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (hipEventRecord(h->fork, s) != hipSuccess || hipStreamWaitEvent(h->side, h->fork, 0) != hipSuccess)
+    return fail(ELASTO_ERR_HIP, "forward: cannot fork to the side stream");
+  const uint8_t* ph = h->plans_half.data() + o;
+  elasto_status_t st = forward_impl(h, images, b1, logits, hip_stream, first, ph);
+  const elasto_status_t st2 =
+      forward_impl(h, static_cast<const uint8_t*>(images) + b1 * img_bytes, b2,
+                   logits + (int64_t)b1 * c.num_classes, h->side, second, ph);
+  if (st == ELASTO_OK) st = st2;
+  // Join even after an error, so that the caller's stream orders after both halves.
+  if (hipEventRecord(h->join, h->side) != hipSuccess || hipStreamWaitEvent(s, h->join, 0) != hipSuccess)
+    return fail(ELASTO_ERR_HIP, "forward: cannot join the side stream");
+  return st;
+}
+
 elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batch, float* logits,
-                             void* hip_stream, const Acts& act, PlanTuning* tune) {
+                             void* hip_stream, const Acts& act, const uint8_t* plans,
+                             PlanTuning* tune) {
   if (!images || !logits) return fail(ELASTO_ERR_INVALID_ARG, "images / logits is NULL");
   if (batch < 1 || batch > h->cfg.max_batch)
     return fail(ELASTO_ERR_BATCH_RANGE, "batch %d outside [1, %d]", batch, h->cfg.max_batch);
@@ -499,19 +633,18 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
   const bool fold = h->dfold != nullptr;
   const int wi = fold ? h->width_idx[(size_t)k] : 0;
   auto fold_ptr = [&](int l, int64_t off) { return h->dfold + (int64_t)l * h->fold_stride + off; };
-  // GEMM sites (handle.h): the tuned plan of the next site for batches of more
-  // than half of max_batch; in the tuning forwards, every plan timed (once
-  // per distinct shape) and the choice recorded.
-  const bool use_plans = !h->plans.empty() && 2 * (int64_t)batch > c.max_batch;
+  // GEMM sites (handle.h): the plan of the next site; in the tuning
+  // forwards, every plan timed (once per distinct shape) and the choice
+  // recorded.
   int site = 0;
   auto run = [&](int kc, Epi epi, GemmArgs& a) -> hipError_t {
-    const size_t i = (size_t)k * h->nsites + site++;
+    const int i = site++;
     if (tune) {
       const int64_t key[9] = {(int64_t)epi, a.M, a.N, a.K, a.lda, a.ldc, a.ln_in != nullptr,
                               a.ln_out != nullptr, a.ccls != nullptr};
       for (const PlanTuning::Seen& sn : tune->seen)
         if (std::equal(key, key + 9, sn.key)) {
-          h->plans[i] = sn.plan;
+          tune->target[i] = sn.plan;
           return hipSuccess;
         }
       const hipError_t te = time_plans(
@@ -519,14 +652,14 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
             a.plan = pl;
             return gemm(epi, a, s);
           },
-          s, tune->e0, tune->e1, &h->plans[i]);
+          s, tune->e0, tune->e1, &tune->target[i]);
       PlanTuning::Seen sn;
       std::copy(key, key + 9, sn.key);
-      sn.plan = h->plans[i];
+      sn.plan = tune->target[i];
       tune->seen.push_back(sn);
       return te;
     }
-    a.plan = use_plans ? (int)h->plans[i] : 0;
+    a.plan = plans ? (int)plans[i] : 0;
     return timed(h, kc, s, [&] { return gemm(epi, a, s); });
   };
 

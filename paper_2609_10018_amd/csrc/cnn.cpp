@@ -17,13 +17,20 @@
 //          shortcut buffer (which becomes cur)
 //   global average pool -> classifier GEMM (fp32 logits)
 //
-// Tile plans: at create, for batches of max_batch >= kTuneMinBatch, every
-// convolution and GEMM of the forward of every mode (a "site") is timed once
-// with each tile plan that can run it (kernels.h, kTilePlans) and keeps the
-// fastest, or the planner's own choice unless another plan is at least 3%
-// faster.  None of these GEMMs has LayerNorm work, so every plan gives
-// bit-identical outputs: the choice changes the speed only.  Forwards of
-// more than half of max_batch images use the plans; smaller ones the planner.
+// Tile plans and stream split: at create, for max_batch >= kTuneMinBatch,
+// every convolution and GEMM of the forward of every mode (a "site") is
+// timed with each tile plan that can run it (kernels.h, kTilePlans,
+// plans.h) and keeps the fastest, or the planner's own choice unless another
+// plan is faster by the margin (plans.h); the same is done for a forward of
+// half the images.  Then each mode's full forward is timed against two
+// half-batch forwards, the second on a side stream of the handle (images
+// are independent, so the halves only fork and join): a kernel's last
+// partial round of tiles then overlaps the other half's kernels.  The split
+// is kept where it is faster by the margin.  The choices are kept per
+// process for handles of the same shapes (plans.h).  None of these GEMMs has LayerNorm work, so every
+// plan and the split give bit-identical outputs: the choices change the
+// speed only.  Forwards of more than half of max_batch images use them;
+// smaller ones run whole with the planner.
 #include <hip/hip_runtime.h>
 #include <string.h>
 
@@ -146,15 +153,41 @@ struct elasto_cnn_s {
   void *col = nullptr, *stem_out = nullptr, *x = nullptr, *d = nullptr, *t1 = nullptr,
        *t2 = nullptr, *feat = nullptr;
   int64_t sz_io = 0, sz_t1 = 0;
+  // Per-image capacity (bf16 elements) of each activation buffer: a forward
+  // part starting at image slot s uses the buffer from s * capacity on, its
+  // images packed at each stage's own size.
+  int64_t per_col = 0, per_stem = 0, per_io = 0, per_t1 = 0, per_t2 = 0, per_feat = 0;
   // Tile plan per (mode, site), sites in forward order: per block reduce,
-  // 3x3, projection (if any), expand; then the classifier.  Empty: none.
+  // 3x3, projection (if any), expand; then the classifier; for whole
+  // forwards and for half-batch ones.  Empty: none.
   int nsites = 0;
-  std::vector<uint8_t> plans;
+  std::vector<uint8_t> plans, plans_half;
+  std::vector<uint8_t> split;       // per mode: run as two half-batch forwards
+  hipStream_t side = nullptr;       // the second half's stream
+  hipEvent_t fork = nullptr, join = nullptr;
 };
 
 namespace {
+// One part of a forward, launched on one stream with a plan per site, or
+// (tuning) recording the timed choices.  Its images occupy the activation
+// buffers' image slots from slot0 on, a region no other part touches while
+// it runs (the buffers are reused from stage to stage with other per-image
+// sizes, so each part keeps to its own slots).
+struct CnnPart {
+  int64_t slot0 = 0;
+  const uint8_t* plans = nullptr;  // [nsites], or nullptr: the planner
+  uint8_t* tune = nullptr;         // [nsites]: time every plan and record
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+};
 elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float* logits,
-                        hipStream_t s, hipEvent_t tune0, hipEvent_t tune1);
+                        hipStream_t s, const CnnPart& part);
+elasto_status_t cnn_forward(elasto_cnn_t h, const void* images, int32_t batch, float* logits,
+                            hipStream_t s);
+void release(elasto_cnn_t h) {
+  if (h->side) (void)hipStreamDestroy(h->side);
+  if (h->fork) (void)hipEventDestroy(h->fork);
+  if (h->join) (void)hipEventDestroy(h->join);
+}
 }
 
 extern "C" {
@@ -319,33 +352,101 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
   h->feat = p;
   h->sz_io = sz_io;
   h->sz_t1 = sz_t1;
+  h->per_col = fused ? 0 : col / B;
+  h->per_stem = fused ? 0 : hs * hs * cfg->stem;
+  h->per_io = io / B;
+  h->per_t1 = t1 / B;
+  h->per_t2 = t2 / B;
+  h->per_feat = F;
   h->nsites = 1;
   for (const BlockSpec& b : bs) h->nsites += b.down ? 4 : 3;
 
-  // Tile plans (file comment): the tuning forwards read their images from
-  // the projection buffer d (overwritten only after the stem has read them)
-  // and write their logits to t1 (free by then); their values do not matter.
+  // Tile plans and split (file comment): the tuning forwards read their
+  // images from the projection buffer d (overwritten only after the stem
+  // has read them) and write their logits to t1 (free by then); their values
+  // do not matter.
   if (B >= kTuneMinBatch && B * C * cfg->img * cfg->img * 2 <= sz_io &&
       B * cfg->num_classes * 4 <= sz_t1) {
     elasto_status_t st = ELASTO_OK;
+    std::vector<int64_t> key;
+    bool cached = false;
     try {
-      h->plans.assign((size_t)h->num_modes * h->nsites, 0);
+      key = {1, h->device, cfg->img, cfg->in_chans, cfg->stem, cfg->num_stages, cfg->expansion,
+             cfg->num_classes, cfg->max_batch, cfg->dtype, h->num_modes};
+      for (int i = 0; i < cfg->num_stages; ++i) {
+        key.push_back(cfg->widths[i]);
+        key.push_back(cfg->blocks[i]);
+      }
+      key.insert(key.end(), h->n_width.begin(), h->n_width.end());
+      TunedPlans tp;
+      cached = tuned_lookup(key, &tp);
+      if (cached) {
+        h->plans = tp.plans;
+        h->plans_half = tp.plans_half;
+        h->split = tp.split;
+      } else {
+        h->plans.assign((size_t)h->num_modes * h->nsites, 0);
+        h->plans_half.assign((size_t)h->num_modes * h->nsites, 0);
+        h->split.assign((size_t)h->num_modes, 0);
+      }
     } catch (...) {
       st = fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
     }
     hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (st == ELASTO_OK && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
-      st = fail(ELASTO_ERR_HIP, "cnn create: cannot create events");
-    for (int m = 0; st == ELASTO_OK && m < h->num_modes; ++m) {
+    if (st == ELASTO_OK &&
+        (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
+         hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) != hipSuccess ||
+         hipEventCreateWithFlags(&h->fork, hipEventDisableTiming) != hipSuccess ||
+         hipEventCreateWithFlags(&h->join, hipEventDisableTiming) != hipSuccess))
+      st = fail(ELASTO_ERR_HIP, "cnn create: cannot create streams / events");
+    const void* img = h->d;
+    float* lg = static_cast<float*>(h->t1);
+    const int32_t Bi = (int32_t)B;
+    // Whole forwards and two-stream splits of the mode, alternately (round 0
+    // untimed), and whether the split is faster by the margin.
+    auto choose_split = [&](size_t m) -> elasto_status_t {
+      float t[2] = {0.0f, 0.0f};
+      for (int r = 0; r <= kTuneReps; ++r)
+        for (int sp = 0; sp < 2; ++sp) {
+          h->split[m] = (uint8_t)sp;
+          if (hipEventRecord(e0, nullptr) != hipSuccess) return fail(ELASTO_ERR_HIP, "cnn create: event");
+          const elasto_status_t fs = cnn_forward(h, img, Bi, lg, nullptr);
+          if (fs != ELASTO_OK) return fs;
+          float ms = 0.0f;
+          if (hipEventRecord(e1, nullptr) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+              hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+            return fail(ELASTO_ERR_HIP, "cnn create: timing failed");
+          if (r == 1 || (r > 1 && ms < t[sp])) t[sp] = ms;
+        }
+      h->split[m] = t[1] < kTuneMargin * t[0] ? 1 : 0;
+      return ELASTO_OK;
+    };
+    for (int m = 0; st == ELASTO_OK && !cached && m < h->num_modes; ++m) {
       h->mode = m;
-      st = cnn_run(h, h->d, (int32_t)B, static_cast<float*>(h->t1), nullptr, e0, e1);
+      const size_t o = (size_t)m * h->nsites;
+      CnnPart full, half;
+      full.tune = h->plans.data() + o;
+      half.tune = h->plans_half.data() + o;
+      full.e0 = half.e0 = e0;
+      full.e1 = half.e1 = e1;
+      st = cnn_run(h, img, Bi, lg, nullptr, full);
+      if (st == ELASTO_OK) st = cnn_run(h, img, Bi / 2, lg, nullptr, half);
+      if (st == ELASTO_OK) st = choose_split((size_t)m);
     }
     if (st == ELASTO_OK && hipDeviceSynchronize() != hipSuccess)
       st = fail(ELASTO_ERR_HIP, "cnn create: tuning forward failed");
+    if (st == ELASTO_OK && !cached) {
+      try {
+        tuned_store(key, TunedPlans{h->plans, h->plans_half, h->split});
+      } catch (...) {
+        st = fail(ELASTO_ERR_OUT_OF_MEMORY, "host allocation failed");
+      }
+    }
     if (e0) (void)hipEventDestroy(e0);
     if (e1) (void)hipEventDestroy(e1);
     h->mode = 0;
     if (st != ELASTO_OK) {
+      release(h);
       (void)hipFree(h->dw);
       (void)hipFree(h->ds);
       delete h;
@@ -360,6 +461,7 @@ elasto_status_t elasto_cnn_create(const elasto_cnn_config_t* cfg, const elasto_c
 elasto_status_t elasto_cnn_destroy(elasto_cnn_t h) {
   if (!h) return ELASTO_OK;
   hipError_t e1 = hipSuccess, e2 = hipSuccess;
+  release(h);
   if (h->dw) e1 = hipFree(h->dw);
   if (h->ds) e2 = hipFree(h->ds);
   delete h;
@@ -419,21 +521,61 @@ elasto_status_t elasto_cnn_forward(elasto_cnn_t h, const void* images, int32_t b
   if (hipGetDevice(&cur_dev) != hipSuccess || cur_dev != h->device) {
     if (hipSetDevice(h->device) != hipSuccess) return fail(ELASTO_ERR_HIP, "cannot select device %d", h->device);
   }
-  return cnn_run(h, images, batch, logits, static_cast<hipStream_t>(hip_stream), nullptr, nullptr);
+  return cnn_forward(h, images, batch, logits, static_cast<hipStream_t>(hip_stream));
 }
 
 }  // extern "C"
 
 namespace {
-// One forward (the file comment); tuning forwards (tune0 != nullptr) time
-// every tile plan at each site and record the choices.
+// A forward of more than half of max_batch images with the tuned plans,
+// whole or (split) as two halves, the second on the side stream; smaller
+// batches whole with the planner.
+elasto_status_t cnn_forward(elasto_cnn_t h, const void* images, int32_t batch, float* logits,
+                            hipStream_t s) {
+  const elasto_cnn_config_t& c = h->cfg;
+  const int k = h->mode;
+  const bool tuned = !h->plans.empty() && 2 * (int64_t)batch > c.max_batch;
+  CnnPart whole;
+  if (!tuned) return cnn_run(h, images, batch, logits, s, whole);
+  const size_t o = (size_t)k * h->nsites;
+  if (!h->split[(size_t)k]) {
+    whole.plans = h->plans.data() + o;
+    return cnn_run(h, images, batch, logits, s, whole);
+  }
+  // The first part takes ceil(batch / 2) images in slots [0, ceil(max_batch / 2)),
+  // the second the rest from slot ceil(max_batch / 2) on.
+  const int32_t b1 = (batch + 1) / 2, b2 = batch - b1;
+  CnnPart first, second;
+  first.plans = second.plans = h->plans_half.data() + o;
+  second.slot0 = (c.max_batch + 1) / 2;
+  if (hipEventRecord(h->fork, s) != hipSuccess || hipStreamWaitEvent(h->side, h->fork, 0) != hipSuccess)
+    return fail(ELASTO_ERR_HIP, "cnn forward: cannot fork to the side stream");
+  elasto_status_t st = cnn_run(h, images, b1, logits, s, first);
+  const elasto_status_t st2 = cnn_run(
+      h, static_cast<const uint8_t*>(images) + (int64_t)b1 * c.in_chans * c.img * c.img * 2, b2,
+      logits + (int64_t)b1 * c.num_classes, h->side, second);
+  if (st == ELASTO_OK) st = st2;
+  // Join even after an error, so that the caller's stream orders after both halves.
+  if (hipEventRecord(h->join, h->side) != hipSuccess || hipStreamWaitEvent(s, h->join, 0) != hipSuccess)
+    return fail(ELASTO_ERR_HIP, "cnn forward: cannot join the side stream");
+  return st;
+}
+
+// One forward of `batch` images (the file comment) as part `part` of the
+// caller's batch; tuning parts time every tile plan at each site and record
+// the choices.
 elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float* logits,
-                        hipStream_t s, hipEvent_t tune0, hipEvent_t tune1) {
+                        hipStream_t s, const CnnPart& part) {
   const elasto_cnn_config_t& c = h->cfg;
   const int k = h->mode;
   const int64_t B = batch;
   auto Wp = [&](int64_t o) { return static_cast<const void*>(h->dw + o); };
   auto Fp = [&](int64_t o) { return reinterpret_cast<const float*>(h->dw + o); };
+  // Where the part's region starts in an activation buffer of `per` bf16
+  // elements of capacity per image (its images are packed from there).
+  auto act = [&](void* buf, int64_t per) {
+    return static_cast<void*>(static_cast<uint8_t*>(buf) + part.slot0 * per * 2);
+  };
   auto gemm = [&](Epi epi, const void* A, int64_t lda, int64_t wo, int64_t ldw, void* C, int64_t ldc,
                   int64_t bo, int64_t M, int N, int K, bool relu, int plan) {
     GemmArgs a;
@@ -461,15 +603,13 @@ elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float
     a.plan = plan;
     return launch_conv_bf16(a, s);
   };
-  // Site: launch(plan) with this forward's plan for the next site, or (tuning
-  // forwards) every plan, timed.
-  const bool tune = tune0 != nullptr;
-  const bool use_plans = !h->plans.empty() && 2 * (int64_t)batch > c.max_batch;
+  // Site: launch(plan) with the part's plan for the next site, or (tuning)
+  // every plan, timed.
   int site = 0;
   auto at_site = [&](auto&& launch) -> hipError_t {
-    const size_t i = (size_t)k * h->nsites + site++;
-    if (tune) return time_plans(launch, s, tune0, tune1, &h->plans[i]);
-    return launch(use_plans ? (int)h->plans[i] : 0);
+    const int i = site++;
+    if (part.tune) return time_plans(launch, s, part.e0, part.e1, &part.tune[i]);
+    return launch(part.plans ? (int)part.plans[i] : 0);
   };
   hipError_t e;
 #define ELASTO_TRY(call, what)                                                       \
@@ -481,40 +621,48 @@ elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float
   const int hs = c.img / 2;
   if (stem_pool_fused(c)) {
     ELASTO_TRY(launch_stem_pool(images, batch, c.in_chans, c.img, Wp(h->stem_w), kStemLdw,
-                                Fp(h->stem_b), c.stem, h->x, s),
+                                Fp(h->stem_b), c.stem, act(h->x, h->per_io), s),
                "stem + max pool");
   } else {
-    ELASTO_TRY(launch_pad_nhwc4(images, batch, c.in_chans, c.img, c.img, 3, h->col, s),
+    void* col = act(h->col, h->per_col);
+    void* stem_out = act(h->stem_out, h->per_stem);
+    ELASTO_TRY(launch_pad_nhwc4(images, batch, c.in_chans, c.img, c.img, 3, col, s),
                "stem input");
     ConvArgs a;
-    a.x = h->col; a.batch = batch; a.H = c.img + 6; a.W = c.img + 6; a.Cs = 4; a.Ca = 32;
+    a.x = col; a.batch = batch; a.H = c.img + 6; a.W = c.img + 6; a.Cs = 4; a.Ca = 32;
     a.KH = 7; a.KW = 1; a.stride = 2; a.pad = 0; a.row_window = 7;
     a.weight = Wp(h->stem_w); a.ldw = kStemLdw; a.wseg = 32;
-    a.C = h->stem_out; a.ldc = c.stem;
+    a.C = stem_out; a.ldc = c.stem;
     a.bias = Fp(h->stem_b);
     a.N = c.stem;
     a.relu = true;
     ELASTO_TRY(launch_conv_bf16(a, s), "stem");
-    ELASTO_TRY(launch_max_pool_3x3_s2(h->stem_out, batch, hs, hs, c.stem, h->x, s), "max pool");
+    ELASTO_TRY(launch_max_pool_3x3_s2(stem_out, batch, hs, hs, c.stem, act(h->x, h->per_io), s),
+               "max pool");
   }
-  void* cur = h->x;
-  void* other = h->d;
+  // Block input and projection output alternate between the x and d buffers.
+  void* curb = h->x;
+  void* othb = h->d;
   for (size_t bi = 0; bi < h->blocks.size(); ++bi) {
     const BlockSpec& b = h->blocks[bi];
     const BlockOff& o = h->boff[bi];
     const int n = h->n_width[(size_t)k * h->blocks.size() + bi];
     const int hi = b.hw_in, ho = b.hw_in / b.stride;
     const int64_t mi = B * hi * hi, mo = B * ho * ho;
+    void* cur = act(curb, h->per_io);
+    void* t1 = act(h->t1, h->per_t1);
+    void* t2 = act(h->t2, h->per_t2);
     ELASTO_TRY(at_site([&](int pl) {
-                 return gemm(Epi::Bias, cur, b.c_in, o.c1w, b.c_in, h->t1, b.width, o.c1b, mi, n,
+                 return gemm(Epi::Bias, cur, b.c_in, o.c1w, b.c_in, t1, b.width, o.c1b, mi, n,
                              b.c_in, true, pl);
                }), "1x1 reduce");
     ELASTO_TRY(at_site([&](int pl) {
-                 return conv(h->t1, hi, b.width, n, 3, b.stride, 1, o.c2w, 9 * b.width, b.width,
-                             h->t2, b.width, o.c2b, n, true, pl);
+                 return conv(t1, hi, b.width, n, 3, b.stride, 1, o.c2w, 9 * b.width, b.width,
+                             t2, b.width, o.c2b, n, true, pl);
                }), "3x3");
     void* shortcut = cur;
     if (b.down) {
+      void* other = act(othb, h->per_io);
       ELASTO_TRY(at_site([&](int pl) {
                    return b.stride > 1
                               ? conv(cur, hi, b.c_in, b.c_in, 1, b.stride, 0, o.dnw, b.c_in, b.c_in,
@@ -525,19 +673,18 @@ elasto_status_t cnn_run(elasto_cnn_t h, const void* images, int32_t batch, float
       shortcut = other;
     }
     ELASTO_TRY(at_site([&](int pl) {
-                 return gemm(Epi::BiasResid, h->t2, b.width, o.c3w, b.width, shortcut, b.c_out,
+                 return gemm(Epi::BiasResid, t2, b.width, o.c3w, b.width, shortcut, b.c_out,
                              o.c3b, mo, b.c_out, n, true, pl);
                }), "1x1 expand");
-    if (b.down) {
-      other = cur;
-      cur = shortcut;
-    }
+    if (b.down) std::swap(curb, othb);
   }
   const BlockSpec& last = h->blocks.back();
   const int hf = last.hw_in / last.stride;
-  ELASTO_TRY(launch_avg_pool(cur, batch, hf * hf, last.c_out, h->feat, s), "average pool");
+  void* feat = act(h->feat, h->per_feat);
+  ELASTO_TRY(launch_avg_pool(act(curb, h->per_io), batch, hf * hf, last.c_out, feat, s),
+             "average pool");
   ELASTO_TRY(at_site([&](int pl) {
-               return gemm(Epi::BiasF32, h->feat, last.c_out, h->fc_w, last.c_out, logits,
+               return gemm(Epi::BiasF32, feat, last.c_out, h->fc_w, last.c_out, logits,
                            c.num_classes, h->fc_b, B, c.num_classes, last.c_out, false, pl);
              }), "classifier");
 #undef ELASTO_TRY

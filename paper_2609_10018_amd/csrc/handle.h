@@ -41,7 +41,12 @@ struct elasto_handle_s {
   // embedding, per layer q/k/v, projection, fc1, fc2, then the head; chosen
   // at create by timing (plans.h).  Empty: the planner everywhere.
   int nsites = 0;
-  std::vector<uint8_t> plans;
+  std::vector<uint8_t> plans, plans_half;  // whole forwards / half-batch parts
+  // Per mode: run a forward of more than max_batch / 2 images as two halves,
+  // the second on the side stream (chosen at create by timing).
+  std::vector<uint8_t> split;
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   // kernel timing
   int timed_class = -1;
   std::vector<hipEvent_t> events;

@@ -120,11 +120,23 @@ hipError_t hipEventDestroy(hipEvent_t e) {
   delete reinterpret_cast<int*>(e);
   return hipSuccess;
 }
+hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned) { return hipEventCreate(e); }
 hipError_t hipEventRecord(hipEvent_t, hipStream_t) { return api(); }
+hipError_t hipStreamCreateWithFlags(hipStream_t* st, unsigned) {
+  tick();
+  *st = reinterpret_cast<hipStream_t>(new int(0));
+  return hipSuccess;
+}
+hipError_t hipStreamDestroy(hipStream_t st) {
+  tick();
+  delete reinterpret_cast<int*>(st);
+  return hipSuccess;
+}
+hipError_t hipStreamWaitEvent(hipStream_t, hipEvent_t, unsigned) { return api(); }
 hipError_t hipEventSynchronize(hipEvent_t) { return api(); }
 hipError_t hipEventElapsedTime(float* ms, hipEvent_t, hipEvent_t) {
   tick();
-  *ms = g_elapsed_decreasing ? (g_elapsed *= 0.99f) : 0.25f;
+  *ms = g_elapsed_decreasing ? (g_elapsed *= 0.9f) : 0.25f;
   return hipSuccess;
 }
 

@@ -115,15 +115,21 @@ def test_resnet50_small_batches(batch):
 
 
 def test_resnet50_tile_plans_do_not_change_outputs():
-    """The handle (max_batch 256) chose its tile plans by timing them at
-    create; a batch of 256 runs with them, one of 128 with the planner's
-    choices.  Every plan walks K in the same order, so the logits of the
-    shared images are bit-identical."""
+    """The handle (max_batch 256) chose its tile plans, and for each mode
+    whether to run as two half-batch forwards on two streams, by timing them
+    at create; a batch of 256 runs with those choices, one of 128 whole with
+    the planner's.  Every plan walks K in the same order and the images are
+    independent, so the logits of both halves are bit-identical to the
+    batch-of-128 forwards of the same images."""
     n = net("resnet50")
+    h = n.max_batch // 2
     for k in (0, 3, 5):
         full = n.run(k)
-        half = n.run(k, n.max_batch // 2)
-        np.testing.assert_array_equal(full[: n.max_batch // 2], half)
+        np.testing.assert_array_equal(full[:h], n.run(k, h))
+        second = torch.empty((h, n.cfg.num_classes), dtype=torch.float32, device="cuda")
+        n.net.forward(n.xd[h:], second)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(full[h:], second.cpu().numpy())
 
 
 def test_cnn_mode_info_matches_cost_model():

@@ -183,6 +183,30 @@ def test_forward_captured_in_hip_graphs():
         s.synchronize()
 
 
+def test_full_batch_forwards_repeat_and_capture():
+    """ViT-B at its full batch of 256: the handle chose at create, per mode,
+    tile plans and whether to run as two halves on two streams.  Every mode's
+    forward repeats bit for bit, and a captured HIP graph of it (the fork to
+    the handle's side stream and the join captured with it) replays the
+    eager result."""
+    m = model("vit_b")
+    s = torch.cuda.Stream()
+    logits = torch.empty((m.max_batch, m.cfg.num_classes), dtype=torch.float32, device="cuda")
+    for k in range(m.table.num_modes):
+        a = m.run(k)
+        np.testing.assert_array_equal(m.run(k), a)
+        m.vit.set_mode(k)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            m.vit.forward(m.xd, logits, s)
+        for _ in range(2):
+            logits.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(logits.cpu().numpy(), a)
+        del g
+
+
 def _poison_outside(w, cfg, table, k):
     """Copy of w with every weight outside mode k's active heads / units = NaN."""
     p = {key: np.array(v, copy=True) for key, v in w.items()}
