@@ -82,21 +82,35 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
   // 0 .. 2NT-1 are K, the next 2NT are V).  Lane l lands at block + 16 l,
   // i.e. row 8*blk + l/8, physical chunk l%8, so it fetches the logical chunk
   // that kv_off() places there.  Rows past the last token re-read token T-1:
-  // their scores are masked out and their probabilities are 0.
+  // their scores are masked out and their probabilities are 0.  Each wave
+  // issues its K blocks first, then as many V blocks (wave + 8i < 2NT for
+  // both), so the first scores are computed while V is still arriving.
+  constexpr int kLoadIters = (2 * NT + kWaves - 1) / kWaves;
 #pragma unroll
-  for (int i = 0; i < (4 * NT + kWaves - 1) / kWaves; ++i) {
-    const int blk = wave + kWaves * i;
-    if (blk < 4 * NT) {
-      const int isv = blk >= 2 * NT;
-      const int r = (blk - (isv ? 2 * NT : 0)) * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ (r & 7);
-      const uint16_t* src = base + (int64_t)min(r, T - 1) * p.qs + (1 + isv) * kHd + c * 8;
-      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)(smem + blk * 1024), 16, 0, 0);
+  for (int isv = 0; isv < 2; ++isv)
+#pragma unroll
+    for (int i = 0; i < kLoadIters; ++i) {
+      const int rb = wave + kWaves * i;  // block of 8 rows within K or V
+      if (rb < 2 * NT) {
+        const int r = rb * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ (r & 7);
+        const uint16_t* src = base + (int64_t)min(r, T - 1) * p.qs + (1 + isv) * kHd + c * 8;
+        __builtin_amdgcn_global_load_lds((global_void*)src,
+                                         (lds_void*)(smem + (isv * 2 * NT + rb) * 1024), 16, 0, 0);
+      }
     }
+  // Nothing reads the staged rows by register dependence.  K: wait until at
+  // most this wave's V loads are in flight (loads complete in issue order for
+  // the counter; the Q loads came first), then for every wave.
+  const int nkv = wave < 2 * NT ? (2 * NT - 1 - wave) / kWaves + 1 : 0;
+  static_assert(kLoadIters <= 4, "K/V loads per wave exceed the wait cases");
+  switch (nkv) {
+    case 0: __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xF << 8)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(1 | (0x7 << 4) | (0xF << 8)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(2 | (0x7 << 4) | (0xF << 8)); break;
+    case 3: __builtin_amdgcn_s_waitcnt(3 | (0x7 << 4) | (0xF << 8)); break;
+    default: __builtin_amdgcn_s_waitcnt(4 | (0x7 << 4) | (0xF << 8)); break;
   }
-  // Nothing reads the staged rows by register dependence: wait for every
-  // vector memory operation of this wave (vmcnt 0), then for every wave.
-  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
   __syncthreads();
 
   // Output rows of this (sequence, head slot): T rows of p.os elements from
@@ -149,6 +163,13 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     sum += __shfl_xor(sum, 16, 64);
     sum += __shfl_xor(sum, 32, 64);
     __builtin_amdgcn_sched_barrier(0);
+    // V: before the first product with it, every V load of every wave.  Each
+    // wave passes this barrier once (here on its first block, or after the
+    // loop when it has none).
+    if (qb == wave) {
+      __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
+      __syncthreads();
+    }
 
     // O^T = V^T P^T over key pairs of tiles (2kb, 2kb+1): k-slot 8*lg + r is
     // key 32kb + 4lg + r, k-slot 8*lg + 4 + r is key 32kb + 16 + 4lg + r.
@@ -196,6 +217,10 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     }
     qf[0] = qn[0];
     qf[1] = qn[1];
+  }
+  if (wave >= NT) {
+    __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
+    __syncthreads();
   }
 }
 
