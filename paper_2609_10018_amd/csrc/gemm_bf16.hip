@@ -850,6 +850,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 constexpr int kPersSlotStride = 72;     // bytes per row of a wave's 32x32 bf16 slot
 constexpr int kPersSlotStrideF32 = 80;  // bytes per row of a wave's 32x16 fp32 slot
 constexpr int kTilePers = 256;       // rows per persistent tile
+// Residual epilogue: 32-row blocks of the residual requested at a tile's last
+// K step (1 or 2; the others one block ahead of their use, in a ring of two).
+constexpr int kResPre = 1;
 
 template <Epi E, bool LNF>
 __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
@@ -862,7 +865,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   // fp32 staging) 32 rows x 16 fp32 columns.
   constexpr int ES = E == Epi::BiasResid ? kPersSlotStrideF32 : kPersSlotStride, SLOT = 32 * ES;
   constexpr int ROWST = LNF ? 2 * BM * 8 : 0;  // LayerNorm factors of two tiles' rows
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT + ROWST];
+  // Residual epilogue: per wave 1 KB for the bias of its 64 columns and the
+  // fp32 residual of the class-token row among its 128 rows (section below).
+  constexpr int AUX = E == Epi::BiasResid ? NW * 1024 : 0;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT + ROWST + AUX];
   auto bar = [] {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -917,6 +923,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   }
   char* const slot = smem + 2 * STAGE + wave * SLOT;
   float2* const rowst = reinterpret_cast<float2*>(smem + 2 * STAGE + NW * SLOT);
+  char* const aux = smem + 2 * STAGE + NW * SLOT + ROWST + wave * 1024;
+  // Residual epilogue: lane l holds row rloc = l/2 of each 32-row block of the
+  // wave, columns 8 (l%2) .. +7 of each 16-column pass.
+  const int rloc = lane >> 1, cloc = (lane & 1) * 8;
   int par = 0;  // half of rowst this tile uses
   int v = blockIdx.x;
   if (v >= total) return;
@@ -938,6 +948,30 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    // Residual epilogue: the bf16 residual chunks of two 32-row blocks (a
+    // ring: block i in slot i % 2), the wave's class-token row (row - wrow0)
+    // and its image.
+    u32x4 rz[2][TN][2];
+    int cls_rel = -1, cls_b = 0;
+    // Residual block i of this lane (rows of the wave as one buffer range:
+    // rows past M read as zeros and are never stored).
+    auto load_res = [&](int i, u32x4 (&dst)[TN][2]) {
+      const uint16_t* rsrc = p.res != nullptr ? p.res : static_cast<const uint16_t*>(p.C);
+      const int rld = (int)(p.res != nullptr ? p.ldres : p.ldc);
+      const int wr0 = __builtin_amdgcn_readfirstlane(m0 + wm * WTM);
+      const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(rsrc) + (int64_t)wr0 * rld, (short)0,
+          __builtin_amdgcn_readfirstlane(max(0, min(WTM, p.M - wr0)) * rld * 2), kRsrcWord3);
+      const int cb = min(n0 + wn * WTN + cloc, p.N - 8);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c = min(cb + j * 32 + h * 16, p.N - 8);
+          dst[j][h] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, ((rloc + i * 32) * rld + c) * 2, 0, 0));
+        }
+    };
     if constexpr (E != Epi::BiasResid) {
       // Fragments of two K quarters in flight: a quarter's MFMAs run while the
       // LDS reads of the next quarter are issued between them, so a wave never
@@ -1012,8 +1046,26 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     } else {
       // The residual epilogue needs more registers than the fragment
       // pipeline leaves: one quarter of fragments at a time.
-  #pragma clang loop unroll(disable)
-      for (int kt = 0; kt < nk; ++kt) {
+      //
+      // Its operands are requested at the tile's last K step, ahead of that
+      // step's tile loads, so that they arrive under its MFMAs instead of
+      // one 32-row block ahead of their use: the bf16 residual of the lane's
+      // four rows (registers), and by one direct load into this wave's LDS
+      // block, the bias of the wave's 64 columns (lanes 0-15) and the fp32
+      // residual of the class-token row among its 128 rows, if there is one
+      // (lanes 16-31; the launcher makes sure there is at most one).
+      const int wrow0 = m0 + wm * WTM;
+      if (p.ccls != nullptr) {
+        const int bi = (wrow0 + p.tokens - 1) / p.tokens, rc = bi * p.tokens;
+        if (rc < wrow0 + WTM && rc < p.M) {
+          cls_rel = rc - wrow0;
+          cls_b = bi;
+        }
+      }
+      // One K step; LAST (the tile's last) also requests the epilogue's
+      // operands, so that they occupy registers only from there on.
+      auto rstep = [&](int kt, auto last_tag) {
+        constexpr bool LAST = decltype(last_tag)::value;
         // After an epilogue the wave's last 16 memory operations are its
         // stores; everything issued before them (this step's loads) is done.
         if (kt == 0 && stores_out) wait_vm_lds<16>();
@@ -1021,16 +1073,15 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         __builtin_amdgcn_s_barrier();
         // Next step of this tile, or the first step of the next tile, into the
         // other stage (every wave finished reading it before the barrier).
-        // Folded LayerNorm: at the first step, two threads a row sum the row's
-        // segment statistics; the loads go out before this step's tile loads so
-        // that waiting for them does not wait for those.
-        LnStat lst{0.0f, 0.0f, 0.0f};
-        if constexpr (LNF) {
-          if (kt == 0)
-            ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, lst);
+        const bool go = !LAST || has_next;
+        if constexpr (LAST) {
+#pragma unroll
+          for (int i = 0; i < kResPre; ++i) load_res(i, rz[i & 1]);
+          const int l = lane & 31, c = min(n0 + wn * WTN + 4 * (l & 15), p.N - 4);
+          const float* src = (l >= 16 && cls_rel >= 0) ? p.ccls + (int64_t)cls_b * p.N + c : p.bias + c;
+          __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)aux, 16, 0, 0);
         }
-        const bool more = kt + 1 < nk, go = more || has_next;
-        const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0;
+        const int nr0 = !LAST ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = !LAST ? kt + 1 : 0;
         const int so = buf * STAGE;
         // Opaque copies: keeps the per-quarter addresses from being hoisted out
         // of the loop into registers.
@@ -1064,18 +1115,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   #pragma unroll
             for (int j = 0; j < TN; ++j)
               acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
-        }
-        if constexpr (LNF) {
-          // Published by a later barrier: the next step's, or the one below.
-          // rowst is double-buffered: a wave in the next tile has passed this
-          // tile's barriers, which every wave reaches after its epilogue.
-          if (kt == 0) {
-            ln_merge_dpp<kDppXor1>(lst);
-            if ((tid & 1) == 0) rowst[par * BM + (tid >> 1)] = ln_factors(lst, p.ln_eps);
-          }
+          // With the residual in registers, one quarter's fragments at a time.
+          if constexpr (LAST) __builtin_amdgcn_sched_barrier(0);
         }
         buf ^= 1;
-      }
+      };
+  #pragma clang loop unroll(disable)
+      for (int kt = 0; kt + 1 < nk; ++kt) rstep(kt, std::false_type{});
+      rstep(nk - 1, std::true_type{});
     }
     if constexpr (LNF) {
       if (nk == 1) {  // no later step barrier in this tile
@@ -1099,65 +1146,27 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       return *reinterpret_cast<const f32x4*>(v + c);
     };
     if constexpr (E == Epi::BiasResid) {
-      f32x4 bv[TN][4];
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) bv[j][g] = col_vec(p.bias, j, g);
       // C = residual + acc + bias: fp32 staging of acc + bias, 16 columns per
       // pass (i, j, h); lane l then holds row r = l/2 of the 32-row block,
       // columns 8 (l%2) .. +7 of the pass.  The residual comes from res (or C
       // in place), except on the class-token rows (row % tokens == 0) when
       // ccls is given: there it is the fp32 ccls row, which takes the fp32
       // result (and C its bf16 rounding when the LayerNorm statistics are
-      // produced).  A lane's 4 rows are 32 apart, so at most one of them is a
-      // class row: its fp32 residual chunks are loaded with the bias.
-      const uint16_t* rsrc = p.res != nullptr ? p.res : static_cast<const uint16_t*>(p.C);
-      const int64_t rld = p.res != nullptr ? p.ldres : p.ldc;
-      const int rloc = lane >> 1, cloc = (lane & 1) * 8;
+      // produced).  Everything the epilogue reads was requested at the last
+      // K step: wait for it (the next tile's first-step loads, issued after
+      // it, may stay in flight).
+      if (has_next)
+        wait_vm_lds<8>();
+      else
+        wait_vm_lds<0>();
+      asm volatile("" ::: "memory");
       const int row_l0 = m0 + wm * WTM + rloc;  // this lane's row in block i: row_l0 + 32 i
-      int cls_i = -1, cls_b = 0;
-      if (p.ccls != nullptr) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const int r = row_l0 + i * 32, bi = r / p.tokens;
-          if (r < p.M && r == bi * p.tokens) {
-            cls_i = i;
-            cls_b = bi;
-          }
-        }
-      }
-      f32x4 cres[TN][2][2];
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int c = min(n0 + wn * WTN + j * 32 + h * 16 + cloc, p.N - 8);
-          if (cls_i >= 0) {
-            const float* cp = p.ccls + (int64_t)cls_b * p.N + c;
-            cres[j][h][0] = *reinterpret_cast<const f32x4*>(cp);
-            cres[j][h][1] = *reinterpret_cast<const f32x4*>(cp + 4);
-          } else {
-            cres[j][h][0] = cres[j][h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-        }
-      auto load_res = [&](int i, u32x4 (&rz)[TN][2]) {
-        const int r = min(row_l0 + i * 32, p.M - 1);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int c = min(n0 + wn * WTN + j * 32 + h * 16 + cloc, p.N - 8);
-            rz[j][h] = *reinterpret_cast<const u32x4*>(rsrc + (int64_t)r * rld + c);
-          }
-      };
-      u32x4 rz[2][TN][2];
-      load_res(0, rz[0]);
+      const int cls_i = (cls_rel >= 0 && (cls_rel & 31) == rloc) ? cls_rel >> 5 : -1;
       const int seg = (n0 + wn * WTN) >> 6;  // this wave's 64 columns: one statistics segment
       const int wo = lr * ES + lg * 16, ro = rloc * ES + (lane & 1) * 32;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
-        if (i + 1 < TM) load_res(i + 1, rz[(i + 1) & 1]);
+        if (i + 1 >= kResPre && i + 1 < TM) load_res(i + 1, rz[(i + 1) & 1]);
         const int row = row_l0 + i * 32;
         const bool row_ok = row < p.M, cls = i == cls_i;
         // Statistics of the lane's four chunks of the segment: pairwise
@@ -1173,8 +1182,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
 #pragma unroll
             for (int gg = 0; gg < 2; ++gg) {
               const int g = 2 * h + gg;
-              const f32x4 w = {acc[i][j][4 * g] + bv[j][g][0], acc[i][j][4 * g + 1] + bv[j][g][1],
-                               acc[i][j][4 * g + 2] + bv[j][g][2], acc[i][j][4 * g + 3] + bv[j][g][3]};
+              // Bias of columns j*32 + 8g + 4lg .. +3 of the wave's 64.
+              const f32x4 bv = *reinterpret_cast<const f32x4*>(aux + (j * 32 + 8 * g + 4 * lg) * 4);
+              const f32x4 w = {acc[i][j][4 * g] + bv[0], acc[i][j][4 * g + 1] + bv[1],
+                               acc[i][j][4 * g + 2] + bv[2], acc[i][j][4 * g + 3] + bv[3]};
               *reinterpret_cast<f32x4*>(slot + wo + gg * 32) = w;
             }
             wait_lds();
@@ -1184,10 +1195,13 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
             const bool ok = row_ok && col + 8 <= p.N;
             float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
             if (cls) {
+              const char* cr = aux + 256 + (j * 32 + h * 16 + cloc) * 4;
+              const f32x4 c0 = *reinterpret_cast<const f32x4*>(cr);
+              const f32x4 c1 = *reinterpret_cast<const f32x4*>(cr + 16);
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                v[e] += cres[j][h][0][e];
-                v[4 + e] += cres[j][h][1][e];
+                v[e] += c0[e];
+                v[4 + e] += c1[e];
               }
               if (ok) {
                 float* cp = p.ccls + (int64_t)cls_b * p.N + col;
@@ -1461,6 +1475,9 @@ bool persistent_ok(const Params& p) {
     // Residual GEMMs: only with short K (the projection), where the epilogue is a
     // large share of a tile (measured: K = 128 -10%, K = 768 -1%, K = 3072 +2%).
     if (E == Epi::BiasResid && (p.K > 1024 || (p.res != nullptr && p.ldres % 8 != 0))) return false;
+    // A wave's 128 rows may hold one class-token row (its fp32 residual is
+    // staged in the wave's LDS block).
+    if (E == Epi::BiasResid && p.ccls != nullptr && p.tokens < 128) return false;
     return p.bias != nullptr && !p.relu && p.aux == nullptr && p.ksplit <= 1 && p.K >= kBK &&
            p.K % kBK == 0 && p.N % 8 == 0 &&
            p.ldc % 8 == 0 && (int64_t)kTilePers * p.ldc * 2 < ((int64_t)1 << 31);
