@@ -130,9 +130,10 @@ typedef struct {
  * rounded to nearest even on the BF16 path), makes one device allocation for
  * the weights and one for max_batch activation scratch, and copies.  The
  * current device at call time owns the handle.  Mode 0 is selected.
- * BF16 with max_batch >= 32: also tunes, per DN mode, on the default
- * stream (about a second at ViT-B batch 256; synchronises the device): every
- * GEMM is timed with each tile plan the GEMM kernels offer, for forwards of
+ * BF16: also tunes, per DN mode, on the default stream (about a second at
+ * ViT-B batch 256; synchronises the device): every GEMM is timed with each
+ * tile plan the GEMM kernels offer (at small batches also split-K plans,
+ * whose partial products go to the handle's workspace), for forwards of
  * max_batch and of half as many images, and the whole forward is timed
  * against two half-batch forwards of which the second runs on a stream the
  * handle owns (forked from and joined back into the caller's stream with

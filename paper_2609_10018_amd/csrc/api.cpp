@@ -284,7 +284,7 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
   const int64_t img_bytes = B * cfg->in_chans * cfg->img * cfg->img * 2;
   const int64_t qkv_bytes = B * h->dims.T * 3 * (int64_t)cfg->dim * 2;
   const int64_t g_bytes = B * h->dims.T * (int64_t)cfg->mlp_hidden * 2;
-  if (bf && B >= kTuneMinBatch && img_bytes <= qkv_bytes && B * cfg->num_classes * 4 <= g_bytes) {
+  if (bf && img_bytes <= qkv_bytes && B * cfg->num_classes * 4 <= g_bytes) {
     elasto_status_t st = ELASTO_OK;
     PlanTuning tn;
     std::vector<int64_t> key;
@@ -660,7 +660,16 @@ elasto_status_t forward_impl(elasto_handle_t h, const void* images, int32_t batc
       return te;
     }
     a.plan = plans ? (int)plans[i] : 0;
-    return timed(h, kc, s, [&] { return gemm(epi, a, s); });
+    return timed(h, kc, s, [&] {
+      hipError_t ge = gemm(epi, a, s);
+      // A split plan chosen with the handle's workspace may not fit a smaller
+      // one (the forward in the static scratch): the planner decides there.
+      if (ge == hipErrorNotSupported && a.plan >= kSplitPlan0) {
+        a.plan = 0;
+        ge = gemm(epi, a, s);
+      }
+      return ge;
+    });
   };
 
   hipError_t e;

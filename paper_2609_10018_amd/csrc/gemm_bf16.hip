@@ -1534,7 +1534,10 @@ hipError_t launch_forced(const Params& p, hipStream_t s) {
         if (persistent_ok<E>(p)) return launch_persistent<E>(p, p.M, s);
       }
       return hipErrorNotSupported;
-    default: return hipErrorInvalidValue;
+    default:
+      // Split-K plans (7 and up) apply to small-M bf16 GEMMs only
+      // (launch_gemm_bf16 takes them before this point).
+      return p.plan < kTilePlans ? hipErrorNotSupported : hipErrorInvalidValue;
   }
 }
 
@@ -1634,6 +1637,23 @@ int split_plan(const Params& p, int64_t ws_bytes, int* kchunk) {
   const int steps = (nk + best - 1) / best;
   *kchunk = steps * kBK;
   return (nk + steps - 1) / steps;
+}
+
+// A forced split into about `chunks` K-chunks (split plans): only where the
+// planner could split (the 128x128 tiles fill under half the CUs), with at
+// least two chunks and the partials within the workspace.  Returns the chunk
+// count (1: not applicable) and the chunk length.
+int forced_split(const Params& p, int64_t ws_bytes, int chunks, int* kchunk) {
+  constexpr int kCUs = 256;
+  const int64_t tiles = (int64_t)((p.M + 127) / 128) * ((p.N + 127) / 128);
+  const int nk = (p.K + kBK - 1) / kBK;
+  if (tiles * 2 > kCUs || chunks < 2 || nk < 2) return 1;
+  const int steps = (nk + chunks - 1) / chunks;
+  const int c = (nk + steps - 1) / steps;
+  const int64_t ldp = (p.N + 7) / 8 * 8;
+  if (c < 2 || (int64_t)c * p.M * ldp * 4 > ws_bytes) return 1;
+  *kchunk = steps * kBK;
+  return c;
 }
 
 template <Epi E>
@@ -1742,18 +1762,25 @@ hipError_t launch_gemm_bf16(Epi epi, const GemmArgs& a, hipStream_t s) {
   if (a.plan < 0 || a.plan >= kTilePlans) return hipErrorInvalidValue;
   if (a.aux != nullptr && epi == Epi::BiasGelu && (a.ldaux < a.N || a.ldaux % 8 != 0))
     return hipErrorInvalidValue;
-  // Small M: split K over more workgroups when the caller gave a workspace.
-  if (a.ws != nullptr && a.ksplit <= 1 && !a.relu && a.aux == nullptr && p.bias != nullptr &&
-      (epi == Epi::Bias || epi == Epi::BiasGelu || epi == Epi::BiasResid)) {
-    int kchunk = 0;
-    const int ksplit = split_plan(p, a.ws_bytes, &kchunk);
-    if (ksplit > 1) {
-      if (a.plan != 0) return hipErrorNotSupported;  // split K sums in another order
-      switch (epi) {
-        case Epi::Bias: return launch_split<Epi::Bias>(p, a.ws, ksplit, kchunk, s);
-        case Epi::BiasGelu: return launch_split<Epi::BiasGelu>(p, a.ws, ksplit, kchunk, s);
-        default: return launch_split<Epi::BiasResid>(p, a.ws, ksplit, kchunk, s);
-      }
+  // Small M: split K over more workgroups when the caller gave a workspace,
+  // in as many chunks as the planner's model chooses (plan 0) or as a split
+  // plan forces (kSplitPlan0 and up); a forced tile plan never splits.
+  const bool split_ok = a.ws != nullptr && a.ksplit <= 1 && !a.relu && a.aux == nullptr &&
+                        p.bias != nullptr &&
+                        (epi == Epi::Bias || epi == Epi::BiasGelu || epi == Epi::BiasResid);
+  int ksplit = 1, kchunk = 0;
+  if (a.plan >= kSplitPlan0) {
+    if (!split_ok) return hipErrorNotSupported;
+    ksplit = forced_split(p, a.ws_bytes, kSplitChunks[a.plan - kSplitPlan0], &kchunk);
+    if (ksplit < 2) return hipErrorNotSupported;
+  } else if (a.plan == 0 && split_ok) {
+    ksplit = split_plan(p, a.ws_bytes, &kchunk);
+  }
+  if (ksplit > 1) {
+    switch (epi) {
+      case Epi::Bias: return launch_split<Epi::Bias>(p, a.ws, ksplit, kchunk, s);
+      case Epi::BiasGelu: return launch_split<Epi::BiasGelu>(p, a.ws, ksplit, kchunk, s);
+      default: return launch_split<Epi::BiasResid>(p, a.ws, ksplit, kchunk, s);
     }
   }
   switch (epi) {

@@ -80,7 +80,7 @@ struct GemmArgs {
   int64_t ws_bytes = 0;
   // Tile plan (see kTilePlans): 0 lets the planner choose; another value
   // runs that one configuration, or returns hipErrorNotSupported where it
-  // cannot take these arguments (or where the planner would split K).
+  // cannot take these arguments.
   int plan = 0;
 };
 
@@ -91,7 +91,14 @@ struct GemmArgs {
 // it).  Every plan walks K in the same order with the same MFMA
 // instruction, so for a GEMM with no LayerNorm work (ln_in, ln_out) and no
 // class-token rows (ccls) the outputs are bit-identical whatever the plan.
-constexpr int kTilePlans = 7;
+// Plans kSplitPlan0 + i split K into about kSplitChunks[i] chunks (bf16 Bias /
+// BiasGelu / BiasResid with a workspace, where the 128x128 tiles would fill
+// under half the CUs; the partials are summed in chunk order, so the bits
+// differ from the unsplit plans').  A forced tile plan (1-6) never splits;
+// plan 0 splits where the planner's cost model says so.
+constexpr int kSplitPlan0 = 7;
+constexpr int kSplitChunks[] = {2, 3, 4, 6, 8, 12, 16};
+constexpr int kTilePlans = kSplitPlan0 + (int)(sizeof(kSplitChunks) / sizeof(kSplitChunks[0]));
 
 // Largest split-K workspace the planner uses: chunks are limited to the CU
 // count over the 128x128 tile count, so chunks x M x N stays below

@@ -14,7 +14,7 @@
 namespace elasto {
 
 constexpr int kTuneReps = 5;         // timed launches per plan (the fastest counts)
-constexpr int kTuneMinBatch = 32;    // handles for fewer images are not tuned
+constexpr int kTuneMinBatch = 32;    // elastic-CNN handles for fewer images are not tuned
 constexpr float kTuneMargin = 0.99f; // another choice must beat the default by 1%
 
 // Times `launch(plan)` for every tile plan: each once untimed, then

@@ -258,16 +258,24 @@ def test_prefix_read_nan_poison(name, k):
                                           ("vit_ti_emb", 3, 1)])
 def test_prefix_read_nan_poison_small_batch(name, k, batch):
     """The split-K path of small batches (each K chunk a slice of the prefix,
-    the last one ragged) reads no weight outside mode k's prefix either."""
-    clean = model(name)
+    the last one ragged) reads no weight outside mode k's prefix either.  The
+    reference is a clean handle of the same max_batch: handles of the same
+    shapes take the same create-time plan choices (split-K ones included), so
+    the two must agree bit for bit."""
+    full = model(name)
+    clean = Model(name, max_batch=batch, weights=full.w)
+    clean.xd = full.xd[:batch].contiguous()  # the same images
     ref = clean.run(k, batch)
+    clean.vit.close()
     poisoned = Model(name, max_batch=batch,
-                     weights=_poison_outside(clean.w, clean.cfg, clean.table, k))
-    poisoned.xd = clean.xd[:batch].contiguous()  # the same images
+                     weights=_poison_outside(full.w, full.cfg, full.table, k))
+    poisoned.xd = full.xd[:batch].contiguous()
     got = poisoned.run(k, batch)
     poisoned.vit.close()
     assert np.isfinite(got).all()
     np.testing.assert_allclose(got, ref, rtol=0, atol=0)
+    # and both are the forward of the full-batch handle within bf16 rounding
+    assert rel_err(got, full.run(k, batch)) <= BF16_TOL
 
 
 def test_error_paths_on_device():
