@@ -2,7 +2,9 @@
 // o = softmax(q k^T * scale) v per (sequence, head slot).
 //
 // bf16 path (head_dim 64): one workgroup of 8 waves per (sequence, head
-// slot), so no wave takes more than two of the (up to 15) query blocks.  K and
+// slot), so no wave takes more than two of the (up to 15) query blocks (two
+// workgroups, each with a share of the blocks, when the pairs are too few to
+// fill the CUs: small batches).  K and
 // V are staged whole in LDS by direct global->LDS loads, both in token-row
 // layout (rows of 128 B, 16-byte chunks XOR-swizzled); padding keys past the
 // last token repeat that token and are masked (zero probability).  Each wave
@@ -24,6 +26,8 @@
 //
 // fp32 path: a plain per-query loop (two passes over the keys: max, then
 // exp-sum and weighted V sum), fp32 FMA throughout.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -49,6 +53,7 @@ struct AttnP {
   uint16_t* o;
   int64_t os;
   int T, heads;
+  int parts;  // workgroups per (sequence, head slot), each a share of the query blocks
   float scale_log2;
 };
 
@@ -63,7 +68,10 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
   const char* vl = smem + KV;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int b = blockIdx.x / p.heads, s = blockIdx.x - b * p.heads;
+  const int bs = blockIdx.x / p.parts, part = blockIdx.x - bs * p.parts;
+  const int b = bs / p.heads, s = bs - b * p.heads;
+  // Query blocks of this workgroup: part * 8 + wave, then every 8 * parts.
+  const int qb0 = part * kWaves + wave, qstep = kWaves * p.parts;
   const uint16_t* base = p.qkv + (int64_t)b * T * p.qs + (int64_t)s * 3 * kHd;
 
   const int lq = lane & 15, lg = lane >> 4;
@@ -76,7 +84,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     qf[1] = *reinterpret_cast<const bf16x8*>(qp + 32);
   };
   bf16x8 qf[2];
-  if (wave < NT) load_q(wave, qf);
+  if (qb0 < NT) load_q(qb0, qf);
 
   // K and V: direct global->LDS loads in 1-KB blocks of 8 token rows (blocks
   // 0 .. 2NT-1 are K, the next 2NT are V).  Lane l lands at block + 16 l,
@@ -119,7 +127,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
   const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
       p.o + (int64_t)b * T * p.os + (int64_t)s * kHd, (short)0, nrec, kRsrcWord3);
   const float c2 = p.scale_log2;
-  for (int qb = wave; qb < NT; qb += kWaves) {
+  for (int qb = qb0; qb < NT; qb += qstep) {
     const int q0 = qb * 16;
     f32x4 st[NT];
 #pragma unroll
@@ -136,7 +144,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     }
     __builtin_amdgcn_sched_barrier(0);
     bf16x8 qn[2];
-    if (qb + kWaves < NT) load_q(qb + kWaves, qn);
+    if (qb + qstep < NT) load_q(qb + qstep, qn);
     // Keys of the last tile at or past T do not exist.
     bool valid[4];
 #pragma unroll
@@ -166,7 +174,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     // V: before the first product with it, every V load of every wave.  Each
     // wave passes this barrier once (here on its first block, or after the
     // loop when it has none).
-    if (qb == wave) {
+    if (qb == qb0) {
       __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
       __syncthreads();
     }
@@ -218,16 +226,22 @@ __global__ __launch_bounds__(kThreads, 2) void attention_bf16_kernel(AttnP p) {
     qf[0] = qn[0];
     qf[1] = qn[1];
   }
-  if (wave >= NT) {
+  if (qb0 >= NT) {
     __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
     __syncthreads();
   }
 }
 
 template <int NT>
-hipError_t launch_attn_nt(const AttnP& p, int batch, int heads, hipStream_t s) {
+hipError_t launch_attn_nt(AttnP p, int batch, int heads, hipStream_t s) {
   const size_t lds = 2 * (size_t)NT * 16 * 128;
-  hipLaunchKernelGGL(attention_bf16_kernel<NT>, dim3((unsigned)(batch * heads)), dim3(kThreads),
+  // Few (sequence, head slot) pairs (small batches, narrow modes): split each
+  // one's query blocks over more workgroups (each stages K and V itself), so
+  // that more CUs work and a wave takes one block instead of two.
+  constexpr int kCUs = 256;
+  const int pairs = batch * heads;
+  p.parts = std::max(1, std::min((NT + kWaves - 1) / kWaves, kCUs / std::max(pairs, 1)));
+  hipLaunchKernelGGL(attention_bf16_kernel<NT>, dim3((unsigned)(pairs * p.parts)), dim3(kThreads),
                      lds, s, p);
   return hipGetLastError();
 }
