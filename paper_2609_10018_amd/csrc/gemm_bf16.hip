@@ -853,6 +853,9 @@ constexpr int kTilePers = 256;       // rows per persistent tile
 // Residual epilogue: 32-row blocks of the residual requested at a tile's last
 // K step (1 or 2; the others one block ahead of their use, in a ring of two).
 constexpr int kResPre = 1;
+// Residual epilogue kernel with the two-quarter fragment pipeline of the
+// other epilogues (true) or one quarter of fragments at a time (false).
+constexpr bool kResPipelined = true;
 
 template <Epi E, bool LNF>
 __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
@@ -972,7 +975,26 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
               u32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, ((rloc + i * 32) * rld + c) * 2, 0, 0));
         }
     };
-    if constexpr (E != Epi::BiasResid) {
+    // Residual epilogue: the wave's class-token row, and the request of the
+    // epilogue's operands at the tile's last K step (below).
+    if constexpr (E == Epi::BiasResid) {
+      const int wrow0 = m0 + wm * WTM;
+      if (p.ccls != nullptr) {
+        const int bi = (wrow0 + p.tokens - 1) / p.tokens, rc = bi * p.tokens;
+        if (rc < wrow0 + WTM && rc < p.M) {
+          cls_rel = rc - wrow0;
+          cls_b = bi;
+        }
+      }
+    }
+    auto res_request = [&]() {
+#pragma unroll
+      for (int i = 0; i < kResPre; ++i) load_res(i, rz[i & 1]);
+      const int l = lane & 31, c = min(n0 + wn * WTN + 4 * (l & 15), p.N - 4);
+      const float* src = (l >= 16 && cls_rel >= 0) ? p.ccls + (int64_t)cls_b * p.N + c : p.bias + c;
+      __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)aux, 16, 0, 0);
+    };
+    if constexpr (E != Epi::BiasResid || kResPipelined) {
       // Fragments of two K quarters in flight: a quarter's MFMAs run while the
       // LDS reads of the next quarter are issued between them, so a wave never
       // waits on reads issued just before.  A step's last quarter is
@@ -993,6 +1015,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
           ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, \
                   lst);                                                                        \
         const bool more = kt + 1 < nk;                                                         \
+        if (E == Epi::BiasResid && !more) res_request();                                       \
         const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0; \
         const int so = buf * STAGE;                                                            \
         int xl = pcx, pr = prow, ab[TM], bb[TN];                                               \
@@ -1054,14 +1077,6 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       // block, the bias of the wave's 64 columns (lanes 0-15) and the fp32
       // residual of the class-token row among its 128 rows, if there is one
       // (lanes 16-31; the launcher makes sure there is at most one).
-      const int wrow0 = m0 + wm * WTM;
-      if (p.ccls != nullptr) {
-        const int bi = (wrow0 + p.tokens - 1) / p.tokens, rc = bi * p.tokens;
-        if (rc < wrow0 + WTM && rc < p.M) {
-          cls_rel = rc - wrow0;
-          cls_b = bi;
-        }
-      }
       // One K step; LAST (the tile's last) also requests the epilogue's
       // operands, so that they occupy registers only from there on.
       auto rstep = [&](int kt, auto last_tag) {
@@ -1074,13 +1089,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         // Next step of this tile, or the first step of the next tile, into the
         // other stage (every wave finished reading it before the barrier).
         const bool go = !LAST || has_next;
-        if constexpr (LAST) {
-#pragma unroll
-          for (int i = 0; i < kResPre; ++i) load_res(i, rz[i & 1]);
-          const int l = lane & 31, c = min(n0 + wn * WTN + 4 * (l & 15), p.N - 4);
-          const float* src = (l >= 16 && cls_rel >= 0) ? p.ccls + (int64_t)cls_b * p.N + c : p.bias + c;
-          __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)aux, 16, 0, 0);
-        }
+        if constexpr (LAST) res_request();
         const int nr0 = !LAST ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = !LAST ? kt + 1 : 0;
         const int so = buf * STAGE;
         // Opaque copies: keeps the per-quarter addresses from being hoisted out
@@ -1155,7 +1164,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       // produced).  Everything the epilogue reads was requested at the last
       // K step: wait for it (the next tile's first-step loads, issued after
       // it, may stay in flight).
-      if (has_next)
+      if (kResPipelined || has_next)
         wait_vm_lds<8>();
       else
         wait_vm_lds<0>();
@@ -1472,9 +1481,7 @@ bool persistent_ok(const Params& p) {
   if constexpr (E != Epi::Bias && E != Epi::BiasGelu && E != Epi::BiasResid) {
     return false;
   } else {
-    // Residual GEMMs: only with short K (the projection), where the epilogue is a
-    // large share of a tile (measured: K = 128 -10%, K = 768 -1%, K = 3072 +2%).
-    if (E == Epi::BiasResid && (p.K > 1024 || (p.res != nullptr && p.ldres % 8 != 0))) return false;
+    if (E == Epi::BiasResid && p.res != nullptr && p.ldres % 8 != 0) return false;
     // A wave's 128 rows may hold one class-token row (its fp32 residual is
     // staged in the wave's LDS block).
     if (E == Epi::BiasResid && p.ccls != nullptr && p.tokens < 128) return false;
@@ -1482,6 +1489,14 @@ bool persistent_ok(const Params& p) {
            p.K % kBK == 0 && p.N % 8 == 0 &&
            p.ldc % 8 == 0 && (int64_t)kTilePers * p.ldc * 2 < ((int64_t)1 << 31);
   }
+}
+
+// Whether the planner (plan 0) takes the persistent kernel: for the residual
+// GEMMs only with short K (the projection), where the epilogue is a large
+// share of a tile; the forced plan 6 runs it wherever persistent_ok holds.
+template <Epi E>
+bool persistent_default(const Params& p) {
+  return persistent_ok<E>(p) && (E != Epi::BiasResid || p.K <= 1024);
 }
 
 // Rows [0, rows) of the 256x256 tiling with the persistent kernel.
@@ -1575,7 +1590,7 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
     if (t < best_t - 0.1) {
       Params head = p;
       head.M = (int)head_rows;
-      hipError_t e = (!CONV && persistent_ok<E>(p))
+      hipError_t e = (!CONV && persistent_default<E>(p))
                          ? launch_persistent<E>(p, (int)head_rows, s)
                          : launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
       if (e != hipSuccess) return e;
@@ -1592,7 +1607,7 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
   }
   switch (best) {
     case 0:
-      if (!CONV && persistent_ok<E>(p)) return launch_persistent<E>(p, p.M, s);
+      if (!CONV && persistent_default<E>(p)) return launch_persistent<E>(p, p.M, s);
       return launch_cfg<256, 256, 2, 4, E, CONV>(p, 0, s);
     case 1: return launch_cfg<256, 128, 2, 2, E, CONV>(p, 0, s);
     case 2:
