@@ -1491,9 +1491,10 @@ bool persistent_ok(const Params& p) {
   }
 }
 
-// Whether the planner (plan 0) takes the persistent kernel: for the residual
-// GEMMs only with short K (the projection), where the epilogue is a large
-// share of a tile; the forced plan 6 runs it wherever persistent_ok holds.
+// Whether the planner (plan 0) takes the persistent kernel for a whole
+// launch: for the residual GEMMs only with short K (the projection), where
+// the epilogue is a large share of a tile; a split plan's head and the forced
+// plan 6 run it wherever persistent_ok holds.
 template <Epi E>
 bool persistent_default(const Params& p) {
   return persistent_ok<E>(p) && (E != Epi::BiasResid || p.K <= 1024);
@@ -1590,7 +1591,8 @@ hipError_t launch_epi(const Params& p, hipStream_t s) {
     if (t < best_t - 0.1) {
       Params head = p;
       head.M = (int)head_rows;
-      hipError_t e = (!CONV && persistent_default<E>(p))
+      // (the head's tiles are whole rounds: persistent at any K)
+      hipError_t e = (!CONV && persistent_ok<E>(p))
                          ? launch_persistent<E>(p, (int)head_rows, s)
                          : launch_cfg<256, 256, 2, 4, E, CONV>(head, 0, s);
       if (e != hipSuccess) return e;
