@@ -853,9 +853,6 @@ constexpr int kTilePers = 256;       // rows per persistent tile
 // Residual epilogue: 32-row blocks of the residual requested at a tile's last
 // K step (1 or 2; the others one block ahead of their use, in a ring of two).
 constexpr int kResPre = 1;
-// Residual epilogue kernel with the two-quarter fragment pipeline of the
-// other epilogues (true) or one quarter of fragments at a time (false).
-constexpr bool kResPipelined = true;
 
 template <Epi E, bool LNF>
 __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
@@ -901,7 +898,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   const int lld = (int)(loads_a ? p.lda : p.ldw);
   const int llim = (loads_a ? p.M : p.N) - 1;
   const int loff = (wave & 3) * 64;
-  const int nk = p.K / kBK;
+  // K steps; a ragged last step (kpart = K % 64 columns; residual epilogue
+  // only) is loaded whole (the operands' row strides reach past it) and its
+  // fragments are masked.
+  const int nk = (p.K + kBK - 1) / kBK, kpart = p.K % kBK;
   auto load1 = [&](int stage, int r0, int kt, int i, int xl, int pr) {
     const int rb = min(r0 + loff + 8 * i, llim);
     const int rl = min(r0 + loff + 8 * i + pr, llim) - rb;
@@ -994,7 +994,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       const float* src = (l >= 16 && cls_rel >= 0) ? p.ccls + (int64_t)cls_b * p.N + c : p.bias + c;
       __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)aux, 16, 0, 0);
     };
-    if constexpr (E != Epi::BiasResid || kResPipelined) {
+    {
       // Fragments of two K quarters in flight: a quarter's MFMAs run while the
       // LDS reads of the next quarter are issued between them, so a wave never
       // waits on reads issued just before.  A step's last quarter is
@@ -1004,6 +1004,20 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       // eight tile loads (the last step of the last tile re-reads its own first
       // step into the idle stage), so each quarter is one straight-line block.
       bf16x8 fa[2][TM], fb[2][TN];
+      // Ragged last step: zero both operands' elements at k >= K (this lane's
+      // fragments of quarter kk hold k = 16 kk + 8 lg .. +7 of the step), so
+      // that whatever lies past K in the rows never enters a product.
+      auto mask_tail = [&](bf16x8* fa_, bf16x8* fb_, int kk) {
+        const int k0 = 16 * kk + 8 * lg;
+        u32x4 m;
+  #pragma unroll
+        for (int d = 0; d < 4; ++d)
+          m[d] = (k0 + 2 * d < kpart ? 0x0000ffffu : 0u) | (k0 + 2 * d + 1 < kpart ? 0xffff0000u : 0u);
+  #pragma unroll
+        for (int i = 0; i < TM; ++i) fa_[i] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, fa_[i]) & m);
+  #pragma unroll
+        for (int j = 0; j < TN; ++j) fb_[j] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, fb_[j]) & m);
+      };
   #define ELASTO_PERS_STEP(FIRST)                                                              \
       {                                                                                        \
         if ((FIRST) && stores_out) wait_vm_lds<16>();                                          \
@@ -1030,6 +1044,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
             fa[rs][i] = *reinterpret_cast<const bf16x8*>(smem + ((ab[i] + so) ^ kx));          \
           _Pragma("unroll") for (int j = 0; j < TN; ++j)                                       \
             fb[rs][j] = *reinterpret_cast<const bf16x8*>(smem + ((bb[j] + so) ^ kx));          \
+          if (E == Epi::BiasResid && kpart != 0 && !more) mask_tail(fa[rs], fb[rs], kk);       \
           if (kk < 3) {                                                                        \
             _Pragma("unroll") for (int t = (8 * kk + 2) / 3; t < (8 * (kk + 1) + 2) / 3; ++t)  \
               load1(buf ^ 1, nr0, nkt, t, xl, pr);                                             \
@@ -1066,72 +1081,6 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[1][j], fa[1][i], acc[i][j], 0, 0, 0);
-    } else {
-      // The residual epilogue needs more registers than the fragment
-      // pipeline leaves: one quarter of fragments at a time.
-      //
-      // Its operands are requested at the tile's last K step, ahead of that
-      // step's tile loads, so that they arrive under its MFMAs instead of
-      // one 32-row block ahead of their use: the bf16 residual of the lane's
-      // four rows (registers), and by one direct load into this wave's LDS
-      // block, the bias of the wave's 64 columns (lanes 0-15) and the fp32
-      // residual of the class-token row among its 128 rows, if there is one
-      // (lanes 16-31; the launcher makes sure there is at most one).
-      // One K step; LAST (the tile's last) also requests the epilogue's
-      // operands, so that they occupy registers only from there on.
-      auto rstep = [&](int kt, auto last_tag) {
-        constexpr bool LAST = decltype(last_tag)::value;
-        // After an epilogue the wave's last 16 memory operations are its
-        // stores; everything issued before them (this step's loads) is done.
-        if (kt == 0 && stores_out) wait_vm_lds<16>();
-        else wait_vm_lds<0>();
-        __builtin_amdgcn_s_barrier();
-        // Next step of this tile, or the first step of the next tile, into the
-        // other stage (every wave finished reading it before the barrier).
-        const bool go = !LAST || has_next;
-        if constexpr (LAST) res_request();
-        const int nr0 = !LAST ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = !LAST ? kt + 1 : 0;
-        const int so = buf * STAGE;
-        // Opaque copies: keeps the per-quarter addresses from being hoisted out
-        // of the loop into registers.
-        int xl = pcx, pr = prow, ab[TM], bb[TN];
-  #pragma unroll
-        for (int i = 0; i < TM; ++i) ab[i] = abase[i];
-  #pragma unroll
-        for (int j = 0; j < TN; ++j) bb[j] = bbase[j];
-        asm volatile("" : "+v"(xl), "+v"(pr));
-  #pragma unroll
-        for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(ab[i]));
-  #pragma unroll
-        for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(bb[j]));
-  #pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk) {
-          if (go && kk < 3) {
-  #pragma unroll
-            for (int t = (8 * kk + 2) / 3; t < (8 * (kk + 1) + 2) / 3; ++t)
-              load1(buf ^ 1, nr0, nkt, t, xl, pr);
-          }
-          const int kx = kk << 5;
-          bf16x8 af[TM], bf[TN];
-  #pragma unroll
-          for (int i = 0; i < TM; ++i)
-            af[i] = *reinterpret_cast<const bf16x8*>(smem + ((ab[i] + so) ^ kx));
-  #pragma unroll
-          for (int j = 0; j < TN; ++j)
-            bf[j] = *reinterpret_cast<const bf16x8*>(smem + ((bb[j] + so) ^ kx));
-  #pragma unroll
-          for (int i = 0; i < TM; ++i)
-  #pragma unroll
-            for (int j = 0; j < TN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
-          // With the residual in registers, one quarter's fragments at a time.
-          if constexpr (LAST) __builtin_amdgcn_sched_barrier(0);
-        }
-        buf ^= 1;
-      };
-  #pragma clang loop unroll(disable)
-      for (int kt = 0; kt + 1 < nk; ++kt) rstep(kt, std::false_type{});
-      rstep(nk - 1, std::true_type{});
     }
     if constexpr (LNF) {
       if (nk == 1) {  // no later step barrier in this tile
@@ -1164,10 +1113,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       // produced).  Everything the epilogue reads was requested at the last
       // K step: wait for it (the next tile's first-step loads, issued after
       // it, may stay in flight).
-      if (kResPipelined || has_next)
-        wait_vm_lds<8>();
-      else
-        wait_vm_lds<0>();
+      wait_vm_lds<8>();
       asm volatile("" ::: "memory");
       const int row_l0 = m0 + wm * WTM + rloc;  // this lane's row in block i: row_l0 + 32 i
       const int cls_i = (cls_rel >= 0 && (cls_rel & 31) == rloc) ? cls_rel >> 5 : -1;
@@ -1485,8 +1431,13 @@ bool persistent_ok(const Params& p) {
     // A wave's 128 rows may hold one class-token row (its fp32 residual is
     // staged in the wave's LDS block).
     if (E == Epi::BiasResid && p.ccls != nullptr && p.tokens < 128) return false;
-    return p.bias != nullptr && !p.relu && p.aux == nullptr && p.ksplit <= 1 && p.K >= kBK &&
-           p.K % kBK == 0 && p.N % 8 == 0 &&
+    // K: whole 64-column steps, or (residual GEMMs: fc2 of narrow modes) a
+    // ragged last step that the operands' row strides cover (it is loaded
+    // whole and masked in registers).
+    const int64_t kpad = (p.K + kBK - 1) / kBK * kBK;
+    const bool k_ok = p.K % kBK == 0 || (E == Epi::BiasResid && p.lda >= kpad && p.ldw >= kpad);
+    return p.bias != nullptr && !p.relu && p.aux == nullptr && p.ksplit <= 1 && p.K >= 1 && k_ok &&
+           p.N % 8 == 0 &&
            p.ldc % 8 == 0 && (int64_t)kTilePers * p.ldc * 2 < ((int64_t)1 << 31);
   }
 }
