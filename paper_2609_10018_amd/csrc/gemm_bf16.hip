@@ -853,6 +853,9 @@ constexpr int kTilePers = 256;       // rows per persistent tile
 // Residual epilogue: 32-row blocks of the residual requested at a tile's last
 // K step (1 or 2; the others one block ahead of their use, in a ring of two).
 constexpr int kResPre = 1;
+// Residual blocks held in registers by the epilogue (a ring): kResRing - 1
+// blocks of loads stay in flight ahead of the block being processed.
+constexpr int kResRing = 3;
 
 template <Epi E, bool LNF>
 __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
@@ -954,7 +957,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     // Residual epilogue: the bf16 residual chunks of two 32-row blocks (a
     // ring: block i in slot i % 2), the wave's class-token row (row - wrow0)
     // and its image.
-    u32x4 rz[2][TN][2];
+    u32x4 rz[kResRing][TN][2];
     int cls_rel = -1, cls_b = 0;
     // Residual block i of this lane (rows of the wave as one buffer range:
     // rows past M read as zeros and are never stored).
@@ -989,7 +992,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     }
     auto res_request = [&]() {
 #pragma unroll
-      for (int i = 0; i < kResPre; ++i) load_res(i, rz[i & 1]);
+      for (int i = 0; i < kResPre; ++i) load_res(i, rz[i % kResRing]);
       const int l = lane & 31, c = min(n0 + wn * WTN + 4 * (l & 15), p.N - 4);
       const float* src = (l >= 16 && cls_rel >= 0) ? p.ccls + (int64_t)cls_b * p.N + c : p.bias + c;
       __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)aux, 16, 0, 0);
@@ -1121,7 +1124,13 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       const int wo = lr * ES + lg * 16, ro = rloc * ES + (lane & 1) * 32;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
-        if (i + 1 >= kResPre && i + 1 < TM) load_res(i + 1, rz[(i + 1) & 1]);
+        // Keep kResRing - 1 blocks ahead in flight (slot of block i - 1 is free).
+        if (i == 0) {
+#pragma unroll
+          for (int b = kResPre; b < kResRing - 1 && b < TM; ++b) load_res(b, rz[b % kResRing]);
+        }
+        if (i + kResRing - 1 >= kResPre && i + kResRing - 1 < TM)
+          load_res(i + kResRing - 1, rz[(i + kResRing - 1) % kResRing]);
         const int row = row_l0 + i * 32;
         const bool row_ok = row < p.M, cls = i == cls_i;
         // Statistics of the lane's four chunks of the segment: pairwise
@@ -1164,7 +1173,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
                 *reinterpret_cast<f32x4*>(cp + 4) = f32x4{v[4], v[5], v[6], v[7]};
               }
             } else {
-              const u32x4 x = rz[i & 1][j][h];
+              const u32x4 x = rz[i % kResRing][j][h];
 #pragma unroll
               for (int e = 0; e < 8; ++e)
                 v[e] += __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16));
