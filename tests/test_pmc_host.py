@@ -76,8 +76,20 @@ def _write_counters(path, names, counters):
         w.writerow(["GPU", 1024])
 
 
+MARK = "void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<float>, std::array<char*, 1> >(...)"
+
+
+def test_after_mark_drops_the_tuning_dispatches():
+    tuning = forward_names(1) * 3
+    names = tuning + [MARK] + forward_names(2)
+    kept, vals = pmc.after_mark(names, list(range(len(names))))
+    assert kept == forward_names(2) and vals[0] == len(tuning) + 1
+    assert pmc.after_mark(forward_names(1), [0] * 14)[0] == forward_names(1)  # no marker
+
+
 def test_summarize_synthetic(tmp_path):
-    names = forward_names(2) + [COPY] * 3
+    # dispatches before the marker (create-time tuning) must not count
+    names = [G.format(256, 256, 1)] * 5 + [MARK] + forward_names(2) + [COPY] * 3
     out = str(tmp_path)
     # trace: each dispatch 10 us, except fc1 dispatches 30 us
     os.makedirs(os.path.join(out, "trace"))
