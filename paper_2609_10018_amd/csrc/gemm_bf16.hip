@@ -868,9 +868,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
   // fp32 staging) 32 rows x 16 fp32 columns.
   constexpr int ES = E == Epi::BiasResid ? kPersSlotStrideF32 : kPersSlotStride, SLOT = 32 * ES;
   constexpr int ROWST = LNF ? 2 * BM * 8 : 0;  // LayerNorm factors of two tiles' rows
-  // Residual epilogue: per wave 1 KB for the bias of its 64 columns and the
-  // fp32 residual of the class-token row among its 128 rows (section below).
-  constexpr int AUX = E == Epi::BiasResid ? NW * 1024 : 0;
+  // Per wave 1 KB for the epilogue's column vectors of its 64 columns: the
+  // bias, and the folded-LayerNorm column sums or (residual epilogue) the
+  // fp32 residual of the class-token row among its 128 rows (below).
+  constexpr int AUX = NW * 1024;
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + NW * SLOT + ROWST + AUX];
   auto bar = [] {
     asm volatile("" ::: "memory");
@@ -990,11 +991,26 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
         }
       }
     }
-    auto res_request = [&]() {
+    // The epilogue's operands, requested at the tile's last K step (ahead of
+    // that step's tile loads): residual epilogue, the first residual blocks
+    // (registers); every epilogue, by one direct load into this wave's LDS
+    // block, the bias of its 64 columns (lanes 0-15, bytes 0-255) and the
+    // folded-LayerNorm column sums or the class-token row's fp32 residual
+    // (lanes 16-31, bytes 256-511; lanes 32-63 repeat lanes 0-31).
+    auto epi_request = [&]() {
+      if constexpr (E == Epi::BiasResid) {
 #pragma unroll
-      for (int i = 0; i < kResPre; ++i) load_res(i, rz[i % kResRing]);
+        for (int i = 0; i < kResPre; ++i) load_res(i, rz[i % kResRing]);
+      }
       const int l = lane & 31, c = min(n0 + wn * WTN + 4 * (l & 15), p.N - 4);
-      const float* src = (l >= 16 && cls_rel >= 0) ? p.ccls + (int64_t)cls_b * p.N + c : p.bias + c;
+      const float* src = p.bias + c;
+      if (l >= 16) {
+        if constexpr (E == Epi::BiasResid) {
+          if (cls_rel >= 0) src = p.ccls + (int64_t)cls_b * p.N + c;
+        } else if constexpr (LNF) {
+          src = p.ln_colsum + c;
+        }
+      }
       __builtin_amdgcn_global_load_lds((global_void*)src, (lds_void*)aux, 16, 0, 0);
     };
     {
@@ -1032,7 +1048,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
           ln_sums(p.ln_in + (int64_t)min(m0 + (tid >> 1), p.M - 1) * p.ln_ld, p.K, tid & 1, 2, \
                   lst);                                                                        \
         const bool more = kt + 1 < nk;                                                         \
-        if (E == Epi::BiasResid && !more) res_request();                                       \
+        if (!more) epi_request();                                                              \
         const int nr0 = more ? (loads_a ? m0 : n0) : (loads_a ? m1 : n1), nkt = more ? kt + 1 : 0; \
         const int so = buf * STAGE;                                                            \
         int xl = pcx, pr = prow, ab[TM], bb[TN];                                               \
@@ -1098,14 +1114,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
     const int nrec = rows_valid * (int)p.ldc * 2;
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<uint16_t*>(p.C) + (int64_t)m0 * p.ldc, (short)0, nrec, kRsrcWord3);
-    // Bias (and, folded LayerNorm, column sums) of this lane's columns in
-    // 32-column block j, group g: columns n0 + wn*64 + j*32 + 8g + 4lg + 0..3,
-    // clamped into [0, N) (the columns past N are computed from re-read rows
-    // and never stored).
-    auto col_vec = [&](const float* v, int j, int g) {
-      const int c = min(n0 + wn * WTN + j * 32 + 8 * g + 4 * lg, p.N - 4);
-      return *reinterpret_cast<const f32x4*>(v + c);
-    };
+    // The column vectors in the wave's LDS block hold columns
+    // n0 + wn*64 + 4q .. +3 at 16q, clamped into [0, N) (the columns past N
+    // are computed from re-read rows and never stored).
     if constexpr (E == Epi::BiasResid) {
       // C = residual + acc + bias: fp32 staging of acc + bias, 16 columns per
       // pass (i, j, h); lane l then holds row r = l/2 of the 32-row block,
@@ -1219,29 +1230,32 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
       }
       const int lane_st = ((wm * WTM + (lane >> 2)) * (int)p.ldc + n0 + wn * WTN + (lane & 3) * 8) * 2;
       const int wofs = lr * ES + lg * 8, rofs = (lane >> 2) * ES + (lane & 3) * 16;
-      // Column blocks outermost, so only one block's bias and column sums
-      // are held at a time.
+      // The column vectors were requested at the last K step (the next tile's
+      // first-step loads, issued after them, may stay in flight).
+      wait_vm_lds<8>();
+      asm volatile("" ::: "memory");
+      // Row blocks outermost: the two 64-byte halves of a wave's 128-byte row
+      // segment are stored one pass apart.
   #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        f32x4 bv[4], cs[4];
+      for (int i = 0; i < TM; ++i) {
   #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          bv[g] = col_vec(p.bias, j, g);
-          if constexpr (LNF) cs[g] = col_vec(p.ln_colsum, j, g);
-        }
-  #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+        for (int j = 0; j < TN; ++j) {
         int lst = lane_st, wo = wofs, ro = rofs;
         asm volatile("" : "+v"(lst), "+v"(wo), "+v"(ro));
   #pragma unroll
           for (int g = 0; g < 4; ++g) {
+            // Bias (and column sums) of columns j*32 + 8g + 4lg .. +3 of the wave's 64.
+            const int vo = (j * 32 + 8 * g + 4 * lg) * 4;
+            const f32x4 bv = *reinterpret_cast<const f32x4*>(aux + vo);
+            f32x4 cs;
+            if constexpr (LNF) cs = *reinterpret_cast<const f32x4*>(aux + 256 + vo);
             float t[4];
   #pragma unroll
             for (int e = 0; e < 4; ++e) {
               if constexpr (LNF)
-                t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[g][e], bv[g][e]));
+                t[e] = fmaf(acc[i][j][4 * g + e], rs[i].x, fmaf(rs[i].y, cs[e], bv[e]));
               else
-                t[e] = acc[i][j][4 * g + e] + bv[g][e];
+                t[e] = acc[i][j][4 * g + e] + bv[e];
               if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
             }
             u32x2 w;
