@@ -1322,6 +1322,24 @@ __global__ __launch_bounds__(64) void splitk_epilogue_kernel(SplitEpi q) {
   static_assert(E == Epi::Bias || E == Epi::BiasGelu || E == Epi::BiasResid, "split-K epilogues");
   const int64_t g = (int64_t)blockIdx.x * 64 + threadIdx.x;
   const int row = (int)(g / q.cpr), cc = (int)(g - (int64_t)row * q.cpr);
+  // Folded LayerNorm: the factors of each row the block touches (at most
+  // 64 / 8 + 1 rows: cpr >= 8), merged once per row by one lane, not by
+  // every thread of the row.
+  float2 rs = make_float2(0.0f, 0.0f);
+  if constexpr (E == Epi::Bias || E == Epi::BiasGelu) {
+    if (q.ln_in != nullptr) {
+      __shared__ float2 fac[64 / 8 + 1];
+      const int r0 = (int)((int64_t)blockIdx.x * 64 / q.cpr);
+      const int r = r0 + (int)threadIdx.x;
+      if (threadIdx.x <= 64 / 8 && r < q.M && (int64_t)r * q.cpr < (int64_t)blockIdx.x * 64 + 64) {
+        LnStat st{0.0f, 0.0f, 0.0f};
+        ln_sums(q.ln_in + (int64_t)r * q.ln_ld, q.K, 0, 1, st);
+        fac[threadIdx.x] = ln_factors(st, q.ln_eps);
+      }
+      __syncthreads();
+      if (row < q.M) rs = fac[row - r0];
+    }
+  }
   if (row >= q.M) return;  // whole 8-lane groups: cpr is a multiple of 8
   const int col = cc * 8;
   const bool col_in = col < q.N, full = col + 8 <= q.N;
@@ -1354,9 +1372,6 @@ __global__ __launch_bounds__(64) void splitk_epilogue_kernel(SplitEpi q) {
   if constexpr (E == Epi::Bias || E == Epi::BiasGelu) {
     if (!col_in) return;
     if (q.ln_in != nullptr) {
-      LnStat st{0.0f, 0.0f, 0.0f};
-      ln_sums(q.ln_in + (int64_t)row * q.ln_ld, q.K, 0, 1, st);
-      const float2 rs = ln_factors(st, q.ln_eps);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float cs = col + e < q.N ? q.ln_colsum[col + e] : 0.0f;
