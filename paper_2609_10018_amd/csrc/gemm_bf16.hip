@@ -845,8 +845,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 // stores outstanding, so they drain under its main loop instead of stalling
 // the CU.  Operands are swapped in the MFMA (D = W A^T) so that a lane holds 4
 // consecutive output columns; accumulators live in AGPRs.
-// Requirements (checked by the launcher): a bias, no ReLU, K % 64 == 0,
-// N % 8 == 0, ldc % 8 == 0 (and ldres % 8 == 0), no aux output, no split K.
+// Requirements (checked by the launcher, persistent_ok): a bias, ReLU only on
+// the Bias (no folded LayerNorm) and BiasResid epilogues, K % 64 == 0 or (the
+// residual epilogue) row strides that cover a ragged last step, N % 8 == 0,
+// ldc % 8 == 0 (and ldres % 8 == 0), no aux output, no split K, and with
+// class-token rows at least 128 tokens.
 constexpr int kPersSlotStride = 72;     // bytes per row of a wave's 32x32 bf16 slot
 constexpr int kPersSlotStrideF32 = 80;  // bytes per row of a wave's 32x16 fp32 slot
 constexpr int kTilePers = 256;       // rows per persistent tile
@@ -1188,6 +1191,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
 #pragma unroll
               for (int e = 0; e < 8; ++e)
                 v[e] += __uint_as_float((e & 1) ? (x[e >> 1] & 0xffff0000u) : (x[e >> 1] << 16));
+              if (p.relu) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e], 0.0f);
+              }
             }
             u32x4 w;
 #pragma unroll
@@ -1257,6 +1264,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_persistent(Params p) {
               else
                 t[e] = acc[i][j][4 * g + e] + bv[e];
               if constexpr (E == Epi::BiasGelu) t[e] = gelu_poly(t[e]);
+              if constexpr (E == Epi::Bias && !LNF) {
+                if (p.relu) t[e] = fmaxf(t[e], 0.0f);
+              }
             }
             u32x2 w;
             w[0] = pack_bf16x2(t[0], t[1]);
@@ -1474,7 +1484,10 @@ bool persistent_ok(const Params& p) {
     // whole and masked in registers).
     const int64_t kpad = (p.K + kBK - 1) / kBK * kBK;
     const bool k_ok = p.K % kBK == 0 || (E == Epi::BiasResid && p.lda >= kpad && p.ldw >= kpad);
-    return p.bias != nullptr && !p.relu && p.aux == nullptr && p.ksplit <= 1 && p.K >= 1 && k_ok &&
+    // ReLU (convolution blocks): on the Bias and BiasResid epilogues, not on
+    // a folded-LayerNorm consumer.
+    const bool relu_ok = !p.relu || (E != Epi::BiasGelu && p.ln_in == nullptr);
+    return p.bias != nullptr && relu_ok && p.aux == nullptr && p.ksplit <= 1 && p.K >= 1 && k_ok &&
            p.N % 8 == 0 &&
            p.ldc % 8 == 0 && (int64_t)kTilePers * p.ldc * 2 < ((int64_t)1 << 31);
   }
