@@ -838,7 +838,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(Params p) {
 // workgroup per CU walks 256x256 tiles v = blockIdx.x + gridDim.x * j (same
 // XCD-aware order as above).  Its epilogue is wave-local: each wave converts
 // its 128x64 block to bf16 in registers, transposes it through a private
-// 32x32 LDS slot and writes 16-byte row chunks with buffer stores.  Every wave
+// 32x32 LDS slot (the residual epilogue: 32x16 fp32 values, before the
+// residual add and the one rounding) and writes 16-byte row chunks with
+// buffer stores.  The epilogue's column vectors come through a second
+// per-wave LDS block, loaded at the tile's last K step.  Every wave
 // issues exactly 16 stores per tile (rows past M / chunks past N get an offset
 // past the buffer's end and are dropped), after the first K step of the next
 // tile has been put in flight; the next tile's first wait then leaves those 16
