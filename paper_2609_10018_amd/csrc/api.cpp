@@ -320,8 +320,8 @@ elasto_status_t elasto_create(const elasto_config_t* cfg, const elasto_weights_t
     half.ws = nullptr;
     half.ws_bytes = 0;
     float* lg = static_cast<float*>(h->g);
-    // Whole forwards and two-stream splits of the mode, alternately (round 0
-    // untimed), and whether the split is faster by the margin.
+    // Whole forwards and two-stream splits of the mode, alternately (the
+    // first pass untimed), and whether the split is faster by the margin.
     auto choose_split = [&](size_t m) -> elasto_status_t {
       float t[2] = {0.0f, 0.0f};
       for (int r = 0; r <= kTuneReps; ++r)

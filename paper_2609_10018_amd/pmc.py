@@ -1,7 +1,7 @@
 """rocprofv3 runs and summaries for the elastic-ViT forward (ViT-B/16, bf16,
 batch 256, one DN mode, mode 0 by default).
 
-    PYTHONPATH=<repo> python -m paper_2609_10018_amd.pmc --out gpurun_out/pmc [--mode K]
+    PYTHONPATH=<repo> python -m paper_2609_10018_amd.pmc --out <dir> [--mode K]
 
 runs four profiled passes of ``bench.py`` (each a child process under its own
 time limit) and writes ``summary.md`` and ``traffic.json`` into ``--out``:
@@ -300,7 +300,7 @@ def summarize(out, cmds, mode):
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "pmc"))
+    ap.add_argument("--out", default=os.path.join(ROOT, "pmc_out"))
     ap.add_argument("--summarize-only", action="store_true")
     ap.add_argument("--mode", type=int, default=0, help="DN mode to profile")
     args = ap.parse_args()
